@@ -1,0 +1,101 @@
+"""Reference model of the HBM weight arena: placement and LRU eviction (oracle).
+
+Test infrastructure only. Rules it follows:
+
+* All device memory for models is reserved once and managed internally, so no native
+  allocation happens per swap (paper Sec. 4.4, "Memory block allocation").
+* Eviction only invalidates a model's device region; the host copy is always kept and
+  nothing is copied back (Sec. 4.3, "Model eviction").
+* Victims are chosen least-recently-used (Sec. 5.4; the paper's LRU baseline in Sec. 7.3).
+
+Readings where the paper is silent: a logical clock ticks once per request, so there are
+no ties; a model is placed in the lowest-addressed free gap that fits (first fit); while
+no gap fits, the least recently used resident model is evicted, one at a time. An
+eviction is counted as a fragmentation eviction when the total free space already
+sufficed before it. A model larger than the whole arena is refused with no state change.
+"""
+from __future__ import annotations
+
+
+def round_up(n: int, a: int) -> int:
+    return (n + a - 1) // a * a
+
+
+class NoSpace(Exception):
+    pass
+
+
+class ArenaSim:
+    def __init__(self, capacity: int, align: int = 256):
+        self.capacity = capacity
+        self.align = align
+        self.size = {}          # model id -> extent bytes
+        self.where = {}         # resident model id -> offset
+        self.last = {}          # model id -> clock of last request
+        self.clock = 0
+        self.hits = self.misses = self.evictions = self.frag_evictions = 0
+        self.bytes_swapped = 0
+
+    def register(self, mid: int, nbytes: int) -> None:
+        self.size[mid] = round_up(nbytes, self.align)
+        self.last[mid] = 0
+
+    def unregister(self, mid: int) -> None:
+        self.where.pop(mid, None)
+        del self.size[mid], self.last[mid]
+
+    def used(self) -> int:
+        return sum(self.size[m] for m in self.where)
+
+    def gaps(self):
+        """Free gaps (offset, length) in address order."""
+        out, cur = [], 0
+        for off, m in sorted((o, m) for m, o in self.where.items()):
+            if off > cur:
+                out.append((cur, off - cur))
+            cur = off + self.size[m]
+        if cur < self.capacity:
+            out.append((cur, self.capacity - cur))
+        return out
+
+    def first_fit(self, need: int):
+        for off, ln in self.gaps():
+            if ln >= need:
+                return off
+        return None
+
+    def request(self, mid: int) -> dict:
+        need = self.size[mid]
+        if need > self.capacity:
+            raise NoSpace(mid)
+        self.clock += 1
+        self.last[mid] = self.clock
+        if mid in self.where:
+            self.hits += 1
+            return {"hit": True, "offset": self.where[mid], "evicted": []}
+        self.misses += 1
+        evicted = []
+        off = self.first_fit(need)
+        while off is None:
+            victim = min(self.where, key=lambda m: self.last[m])
+            if self.capacity - self.used() >= need:
+                self.frag_evictions += 1
+            del self.where[victim]
+            self.evictions += 1
+            evicted.append(victim)
+            off = self.first_fit(need)
+        self.where[mid] = off
+        self.bytes_swapped += self.size[mid]
+        return {"hit": False, "offset": off, "evicted": evicted}
+
+    def evict(self, mid: int) -> None:
+        self.where.pop(mid, None)
+
+    def largest_free(self) -> int:
+        return max((ln for _, ln in self.gaps()), default=0)
+
+    def stats(self) -> dict:
+        return {"capacity": self.capacity, "used": self.used(), "largest_free": self.largest_free(),
+                "resident": len(self.where), "hits": self.hits, "misses": self.misses,
+                "evictions": self.evictions, "frag_evictions": self.frag_evictions,
+                "bytes_swapped": self.bytes_swapped}
