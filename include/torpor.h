@@ -1,0 +1,198 @@
+/*
+ * torpor.h - pipelined model swap-in and execution on one AMD MI355X (gfx950).
+ *
+ * The operation (paper Sec. 1 and Sec. 3, "late binding"; Sec. 4.3, "Model swapping and
+ * pipeline execution"): functions publish models that stay in host memory while idle;
+ * when a request arrives for a model that is not on the GPU, its weights are swapped
+ * from a pinned host pool into GPU memory, grouped into transfers of about the size at
+ * which transfer throughput stops improving, and each layer starts computing as soon
+ * as the group holding it has arrived, so transfer and compute overlap within one
+ * forward pass. Eviction only invalidates the GPU copy (Sec. 4.3, "Model eviction").
+ * GPU memory is reserved once and managed internally, with no native allocation per
+ * swap (Sec. 4.4, "Memory block allocation"); a parameter's device address is its
+ * region base plus its unchanged offset (Sec. 4.4, "Memory address management").
+ * Only the final output needs a host synchronisation (Sec. 4.2).
+ *
+ * Conventions for every call:
+ *   - Return value: TP_OK (0) or a negative TP_E_* code; tp_last_error() then returns a
+ *     thread-local message. Validation errors change no state.
+ *   - Device pointers are plain HIP device addresses; streams are hipStream_t passed as
+ *     void* (NULL = the null stream). Nothing in this interface allocates per request.
+ *   - A context is used from one host thread at a time.
+ */
+#ifndef TORPOR_H
+#define TORPOR_H
+
+#include <stdint.h>
+
+#ifndef TP_API
+#define TP_API __attribute__((visibility("default")))
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t tp_status;
+enum {
+  TP_OK = 0,
+  TP_E_INVAL = -1,   /* malformed argument, descriptor or layout */
+  TP_E_NOENT = -2,   /* unknown model id */
+  TP_E_NOSPC = -3,   /* model larger than the arena, or workspace too small */
+  TP_E_HIP = -4,     /* a HIP runtime call failed (message names it) */
+  TP_E_STATE = -5    /* call not valid in the current state */
+};
+
+typedef enum { TP_F32 = 0, TP_BF16 = 1 } tp_dtype;
+
+/* Model families (dims[] meaning per family):
+ *   TP_ARCH_MLP      {layers, width, act(TP_ACT_*)}; layers x Linear(width, width) + bias,
+ *                    activation after every layer but the last.
+ *   TP_ARCH_RESNET50 {classes, image}; ResNet-50 v1.5, batch-norm folded into conv
+ *                    biases, NHWC input [B][image][image][3], image % 32 == 0.
+ *   TP_ARCH_BERT     {layers, d, heads, ffn, seq, vocab, maxpos}; post-LN encoder,
+ *                    head dim 64, token type 0, no mask, LN eps 1e-12. */
+typedef enum { TP_ARCH_MLP = 0, TP_ARCH_RESNET50 = 1, TP_ARCH_BERT = 2 } tp_arch;
+enum { TP_ACT_NONE = 0, TP_ACT_RELU = 1, TP_ACT_GELU = 2 };
+
+/* Tensor roles. MLP and ResNet use W/B (ResNet: layer = conv index in first-use order,
+ * the FC is the last layer). BERT: layer 0 holds the embeddings, layers 1..L the encoder. */
+enum {
+  TP_ROLE_W = 0, TP_ROLE_B = 1,
+  TP_ROLE_TOK_EMB = 10, TP_ROLE_POS_EMB = 11, TP_ROLE_TYPE_EMB = 12,
+  TP_ROLE_EMB_LN_G = 13, TP_ROLE_EMB_LN_B = 14,
+  TP_ROLE_QKV_W = 20, TP_ROLE_QKV_B = 21, TP_ROLE_O_W = 22, TP_ROLE_O_B = 23,
+  TP_ROLE_LN1_G = 24, TP_ROLE_LN1_B = 25, TP_ROLE_FFN1_W = 26, TP_ROLE_FFN1_B = 27,
+  TP_ROLE_FFN2_W = 28, TP_ROLE_FFN2_B = 29, TP_ROLE_LN2_G = 30, TP_ROLE_LN2_B = 31
+};
+
+/* One tensor inside the host weight buffer. Linear weights are [out][in], conv weights
+ * OHWI, the fused BERT QKV weight is [3d][d] with rows Q (heads x 64), K, V; LN gamma and
+ * beta are separate [d] tensors. Unused shape entries are 0. */
+typedef struct {
+  uint32_t layer;     /* first-use unit the tensor belongs to */
+  uint32_t role;      /* TP_ROLE_* */
+  uint64_t offset;    /* byte offset in the host buffer, multiple of 256 */
+  uint64_t bytes;     /* byte size = prod(shape) * element size */
+  int64_t shape[4];
+} tp_tensor_desc;
+
+/* Host weight layout of one model. Tensors are listed in first-use order: layers never
+ * decrease and offsets strictly increase; tensors do not overlap. */
+typedef struct {
+  int32_t arch;        /* tp_arch */
+  int32_t dtype;       /* tp_dtype of every weight; BERT and ResNet require TP_BF16 */
+  int32_t dims[8];
+  uint32_t n_tensors;
+  const tp_tensor_desc* tensors;
+} tp_model_desc;
+
+enum { TP_COPY_MEMCPY = 0, TP_COPY_GATHER = 1 };
+enum {
+  TP_FLAG_POISON = 1,    /* evicted extents are filled with 0xFF (NaN for fp32/bf16) */
+  TP_FLAG_THROTTLE = 2   /* a bounded delay kernel precedes every chunk on the copy stream */
+};
+
+/* Context configuration. arena_dev/work_dev are caller-owned device buffers that must
+ * stay valid until tp_destroy; the library never frees them. copy_stream: NULL makes
+ * the library create (and later destroy) one non-blocking stream. chunk_min_bytes is
+ * the transfer group size G (0 = one chunk per layer). copy_method: TP_COPY_MEMCPY uses
+ * hipMemcpyAsync; TP_COPY_GATHER runs a copy kernel reading host-mapped pinned memory
+ * with gather_wgs workgroups (0 = default). throttle_us: delay per chunk under
+ * TP_FLAG_THROTTLE. */
+typedef struct {
+  void* arena_dev;
+  uint64_t arena_bytes;
+  void* work_dev;
+  uint64_t work_bytes;
+  void* copy_stream;
+  uint64_t chunk_min_bytes;
+  int32_t copy_method;
+  int32_t gather_wgs;
+  int32_t flags;
+  int32_t throttle_us;
+} tp_config;
+
+typedef struct {
+  uint64_t capacity, used, largest_free;
+  uint32_t resident, registered;
+  uint64_t hits, misses, evictions, frag_evictions, bytes_swapped;
+} tp_arena_stats_t;
+
+typedef struct {
+  uint64_t host_bytes;     /* size of the model's pinned host copy (= extent size) */
+  uint64_t param_bytes;    /* sum of tensor sizes (no padding) */
+  uint32_t n_chunks;
+  int32_t resident;
+  uint64_t extent_offset;  /* arena offset of the model's extent when resident */
+  uint64_t last_use_clock; /* logical clock of the last request, 0 if never used */
+} tp_model_info_t;
+
+/* Creates a context bound to the current HIP device. The arena (Sec. 4.4: all GPU
+ * memory reserved up front) must be 256-byte aligned. Errors: TP_E_INVAL for NULL or
+ * misaligned buffers, TP_E_HIP if stream or event creation fails. */
+TP_API tp_status tp_create(const tp_config* cfg, struct tp_ctx** out);
+
+/* Waits for all outstanding work of the context, then frees its pinned host copies,
+ * events and (if it created it) the copy stream. Never frees caller buffers. */
+TP_API tp_status tp_destroy(struct tp_ctx* ctx);
+
+/* Publishes a model (Sec. 3: idle models live in host memory). Copies host_bytes bytes
+ * from host_weights into a library-owned pinned, device-mapped host buffer (Sec. 4.3:
+ * pinned memory pool), so the caller may free its buffer on return. Validates the
+ * descriptor against the family's architecture (every tensor present once with the
+ * expected shape, aligned, in bounds, non-overlapping, in first-use order) and builds
+ * the transfer-chunk plan. The model starts non-resident. Errors: TP_E_INVAL,
+ * TP_E_HIP (pinned allocation failed). */
+TP_API tp_status tp_register_model(struct tp_ctx* ctx, const tp_model_desc* desc,
+                            const void* host_weights, uint64_t host_bytes, int32_t* model_id);
+
+/* Evicts (if resident) after the model's last use has completed, then frees its host
+ * copy and events. Synchronises on that model's work. */
+TP_API tp_status tp_unregister_model(struct tp_ctx* ctx, int32_t model_id);
+
+/* Runs one forward pass of a batch (Sec. 4.3). If the model is not resident an extent
+ * is admitted (first fit; least recently used models are invalidated until one fits)
+ * and its chunks are enqueued on the copy stream, each followed by an event; every
+ * layer's first kernel on `stream` waits for the event of the chunk holding that layer.
+ * Inputs: MLP [batch][width] in the model dtype; ResNet bf16 NHWC
+ * [batch][image][image][3]; BERT int32 token ids [batch][seq] (ids outside [0, vocab)
+ * are clamped). Output (fp32): MLP [batch][width]; ResNet [batch][classes]; BERT
+ * [batch][seq][d]. Asynchronous: returns after enqueueing; the caller synchronises
+ * `stream`. Requests are totally ordered: a request on a stream other than the previous
+ * request's first waits for that request. Errors (synchronous, no state change):
+ * TP_E_NOENT, TP_E_INVAL (batch < 1, NULL pointers), TP_E_NOSPC (model larger than the
+ * arena, or workspace smaller than tp_workspace_bytes). On an enqueue failure the model
+ * is left non-resident and TP_E_HIP is returned. */
+TP_API tp_status tp_infer(struct tp_ctx* ctx, int32_t model_id, const void* input_dev, int32_t batch,
+                   void* output_dev, void* stream);
+
+/* Enqueues the swap-in alone (admission + chunk copies, no compute), as a request with
+ * no output; a following tp_infer of the same model is a hit. `stream` is made to wait
+ * for the copies. Same errors as tp_infer. */
+TP_API tp_status tp_swap_in(struct tp_ctx* ctx, int32_t model_id, void* stream);
+
+/* Invalidates the model's device copy; nothing is copied back (Sec. 4.3). The extent is
+ * reused only after the model's last enqueued use completes. Not an error if the model
+ * is not resident. */
+TP_API tp_status tp_evict(struct tp_ctx* ctx, int32_t model_id);
+
+TP_API tp_status tp_is_resident(struct tp_ctx* ctx, int32_t model_id, int32_t* resident);
+TP_API tp_status tp_arena_stats(struct tp_ctx* ctx, tp_arena_stats_t* out);
+TP_API tp_status tp_model_info(struct tp_ctx* ctx, int32_t model_id, tp_model_info_t* out);
+
+/* Chunk plan of a registered model: fills up to `cap` entries of [begin, end) host
+ * byte ranges and the first layer each chunk holds; *n receives the chunk count. */
+TP_API tp_status tp_model_chunks(struct tp_ctx* ctx, int32_t model_id, uint64_t* begin, uint64_t* end,
+                          uint32_t* first_layer, uint32_t cap, uint32_t* n);
+
+/* Workspace bytes tp_infer needs for this model at this batch size (host-only). */
+TP_API tp_status tp_workspace_bytes(const tp_model_desc* desc, int32_t batch, uint64_t* bytes);
+
+/* Thread-local message describing the last non-OK status ("" if none). */
+TP_API const char* tp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TORPOR_H */

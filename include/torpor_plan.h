@@ -1,0 +1,49 @@
+/*
+ * torpor_plan.h - host-only planning calls of libtorpor (no GPU needed).
+ *
+ * They expose the bookkeeping the runtime uses, so that capacity planners (and the
+ * test suite) can ask what a request sequence would do without touching a device:
+ * descriptor validation, the transfer-chunk plan (paper Sec. 4.3: parameters grouped
+ * into transfers of about the throughput-elbow size, whole layers per group), and an
+ * arena model with first-fit placement and least-recently-used eviction that only
+ * invalidates (Sec. 4.3 "Model eviction"; Sec. 4.4 "Memory block allocation"; Sec. 5.4).
+ * Same status codes and tp_last_error() as torpor.h.
+ */
+#ifndef TORPOR_PLAN_H
+#define TORPOR_PLAN_H
+
+#include "torpor.h"
+
+#ifndef TP_API
+#define TP_API __attribute__((visibility("default")))
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Validates a descriptor exactly as tp_register_model does. */
+TP_API tp_status tph_validate(const tp_model_desc* desc, uint64_t host_bytes);
+
+/* Chunk plan for group size chunk_min_bytes; same outputs as tp_model_chunks. */
+TP_API tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes,
+                   uint64_t* begin, uint64_t* end, uint32_t* first_layer, uint32_t cap, uint32_t* n);
+
+struct tph_arena;
+/* An arena of `capacity` bytes whose extents are rounded up to `align` (power of two). */
+TP_API tp_status tph_arena_create(uint64_t capacity, uint64_t align, struct tph_arena** out);
+TP_API tp_status tph_arena_destroy(struct tph_arena* a);
+TP_API tp_status tph_arena_register(struct tph_arena* a, int32_t model_id, uint64_t bytes);
+TP_API tp_status tph_arena_unregister(struct tph_arena* a, int32_t model_id);
+/* One request: *hit, the extent *offset, and up to `cap` victims in eviction order
+ * (*n_victims receives their count). TP_E_NOSPC (no state change) if the model is
+ * larger than the arena. */
+TP_API tp_status tph_arena_request(struct tph_arena* a, int32_t model_id, int32_t* hit, uint64_t* offset,
+                            int32_t* victims, uint32_t cap, uint32_t* n_victims);
+TP_API tp_status tph_arena_evict(struct tph_arena* a, int32_t model_id);
+TP_API tp_status tph_arena_stats(struct tph_arena* a, tp_arena_stats_t* out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TORPOR_PLAN_H */

@@ -1,0 +1,98 @@
+#include "arena.hpp"
+
+#include <algorithm>
+
+namespace tp {
+
+tp_status Arena::add_model(int32_t id, uint64_t bytes) {
+  if (models_.count(id)) return TP_E_STATE;
+  Rec r;
+  r.bytes = (bytes + align_ - 1) / align_ * align_;
+  models_[id] = r;
+  return TP_OK;
+}
+
+void Arena::remove_model(int32_t id) {
+  evict(id);
+  models_.erase(id);
+}
+
+uint64_t Arena::used() const {
+  uint64_t u = 0;
+  for (int32_t id : by_addr_) u += models_.at(id).bytes;
+  return u;
+}
+
+bool Arena::first_fit(uint64_t need, uint64_t* off) const {
+  uint64_t cur = 0;
+  for (int32_t id : by_addr_) {
+    const Rec& r = models_.at(id);
+    if (r.offset >= cur + need) { *off = cur; return true; }
+    cur = r.offset + r.bytes;
+  }
+  if (capacity_ >= cur + need) { *off = cur; return true; }
+  return false;
+}
+
+Arena::Decision Arena::request(int32_t id) {
+  Rec& me = models_.at(id);
+  me.last = ++clock_;
+  Decision d;
+  if (me.resident) {
+    ++hits_;
+    d.hit = true;
+    d.offset = me.offset;
+    return d;
+  }
+  ++misses_;
+  uint64_t off = 0;
+  while (!first_fit(me.bytes, &off)) {
+    // least recently used resident model (never the requester: it is not resident)
+    int32_t victim = -1;
+    uint64_t oldest = UINT64_MAX;
+    for (int32_t r : by_addr_) {
+      const uint64_t t = models_.at(r).last;
+      if (t < oldest) { oldest = t; victim = r; }
+    }
+    if (capacity_ - used() >= me.bytes) ++frag_evictions_;
+    evict(victim);
+    ++evictions_;
+    d.victims.push_back(victim);
+  }
+  me.resident = true;
+  me.offset = off;
+  by_addr_.insert(std::upper_bound(by_addr_.begin(), by_addr_.end(), off,
+                                   [&](uint64_t o, int32_t r) { return o < models_.at(r).offset; }),
+                  id);
+  swapped_ += me.bytes;
+  d.offset = off;
+  return d;
+}
+
+void Arena::evict(int32_t id) {
+  auto it = models_.find(id);
+  if (it == models_.end() || !it->second.resident) return;
+  it->second.resident = false;
+  by_addr_.erase(std::find(by_addr_.begin(), by_addr_.end(), id));
+}
+
+void Arena::stats(tp_arena_stats_t* s) const {
+  s->capacity = capacity_;
+  s->used = used();
+  uint64_t cur = 0, largest = 0;
+  for (int32_t id : by_addr_) {
+    const Rec& r = models_.at(id);
+    largest = std::max(largest, r.offset - cur);
+    cur = r.offset + r.bytes;
+  }
+  s->largest_free = std::max(largest, capacity_ - cur);
+  s->resident = (uint32_t)by_addr_.size();
+  s->registered = (uint32_t)models_.size();
+  s->hits = hits_;
+  s->misses = misses_;
+  s->evictions = evictions_;
+  s->frag_evictions = frag_evictions_;
+  s->bytes_swapped = swapped_;
+}
+
+}  // namespace tp

@@ -1,0 +1,56 @@
+// The HBM weight arena's bookkeeping: one reserved device range, one contiguous extent
+// per resident model, placement in the lowest-addressed free gap that fits, and
+// least-recently-used eviction (invalidate only) until a gap fits. Host-only C++; the
+// runtime attaches device-side ordering (events) to the decisions made here.
+#pragma once
+#include <cstdint>
+#include <unordered_map>
+#include <vector>
+
+#include "torpor.h"
+
+namespace tp {
+
+class Arena {
+ public:
+  Arena(uint64_t capacity, uint64_t align) : capacity_(capacity), align_(align) {}
+
+  struct Decision {
+    bool hit = false;
+    uint64_t offset = 0;
+    std::vector<int32_t> victims;   // evicted by this request, in eviction order
+  };
+
+  tp_status add_model(int32_t id, uint64_t bytes);
+  void remove_model(int32_t id);               // also drops residency
+  bool known(int32_t id) const { return models_.count(id) != 0; }
+  bool fits_at_all(int32_t id) const { return models_.at(id).bytes <= capacity_; }
+
+  // One request for model `id`: ticks the clock, counts a hit or miss, and on a miss
+  // chooses victims and an offset. Caller checks fits_at_all() first.
+  Decision request(int32_t id);
+
+  void evict(int32_t id);                       // explicit invalidation; no counters
+  bool resident(int32_t id) const { return models_.at(id).resident; }
+  uint64_t offset(int32_t id) const { return models_.at(id).offset; }
+  uint64_t bytes(int32_t id) const { return models_.at(id).bytes; }
+  uint64_t last_use(int32_t id) const { return models_.at(id).last; }
+
+  void stats(tp_arena_stats_t* s) const;
+
+ private:
+  struct Rec {
+    uint64_t bytes = 0, offset = 0, last = 0;
+    bool resident = false;
+  };
+  bool first_fit(uint64_t need, uint64_t* off) const;
+  uint64_t used() const;
+
+  uint64_t capacity_, align_;
+  uint64_t clock_ = 0;
+  uint64_t hits_ = 0, misses_ = 0, evictions_ = 0, frag_evictions_ = 0, swapped_ = 0;
+  std::unordered_map<int32_t, Rec> models_;
+  std::vector<int32_t> by_addr_;                // resident ids sorted by offset
+};
+
+}  // namespace tp

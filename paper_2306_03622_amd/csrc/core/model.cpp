@@ -1,0 +1,245 @@
+#include "model.hpp"
+
+#include <algorithm>
+#include <cstdio>
+
+namespace tp {
+
+std::vector<ConvShape> resnet50_convs() {
+  std::vector<ConvShape> v;
+  v.push_back({64, 7, 3, 2, 3});
+  const int blocks[4] = {3, 4, 6, 3}, mids[4] = {64, 128, 256, 512};
+  int cin = 64;
+  for (int s = 0; s < 4; ++s) {
+    const int mid = mids[s], out = 4 * mid;
+    for (int b = 0; b < blocks[s]; ++b) {
+      const int stride = (s > 0 && b == 0) ? 2 : 1;
+      v.push_back({mid, 1, cin, 1, 0});
+      v.push_back({mid, 3, mid, stride, 1});
+      v.push_back({out, 1, mid, 1, 0});
+      if (b == 0) v.push_back({out, 1, cin, stride, 0});
+      cin = out;
+    }
+  }
+  return v;
+}
+
+std::vector<ConvGeom> resnet50_geometry(int image) {
+  const auto convs = resnet50_convs();
+  std::vector<ConvGeom> g;
+  auto out = [](int h, const ConvShape& c) { return (h + 2 * c.pad - c.k) / c.stride + 1; };
+  const int h1 = out(image, convs[0]);
+  g.push_back({convs[0], image, h1});
+  int cur = (h1 + 2 - 3) / 2 + 1;   // max-pool
+  size_t i = 1;
+  const int blocks[4] = {3, 4, 6, 3};
+  for (int s = 0; s < 4; ++s) {
+    for (int b = 0; b < blocks[s]; ++b) {
+      const int h_in = cur;
+      const int h_a = out(h_in, convs[i]);
+      g.push_back({convs[i], h_in, h_a}); ++i;                       // 1x1
+      const int h_b = out(h_a, convs[i]);
+      g.push_back({convs[i], h_a, h_b}); ++i;                        // 3x3 (stride)
+      g.push_back({convs[i], h_b, out(h_b, convs[i])}); ++i;         // 1x1
+      if (b == 0) { g.push_back({convs[i], h_in, out(h_in, convs[i])}); ++i; }   // shortcut
+      cur = h_b;
+    }
+  }
+  return g;
+}
+
+namespace {
+
+struct Want {
+  uint32_t layer, role;
+  int64_t shape[4];
+};
+
+std::string fmt(const char* f, long long a = 0, long long b = 0, long long c = 0, long long d = 0) {
+  char buf[256];
+  std::snprintf(buf, sizeof buf, f, a, b, c, d);
+  return buf;
+}
+
+bool expected(const tp_model_desc* d, std::vector<Want>* w, uint32_t* n_layers, std::string* err) {
+  const int32_t* D = d->dims;
+  auto add = [&](uint32_t l, uint32_t r, int64_t a, int64_t b = 0, int64_t c = 0, int64_t e = 0) {
+    w->push_back({l, r, {a, b, c, e}});
+  };
+  switch (d->arch) {
+    case TP_ARCH_MLP: {
+      const int L = D[0], W = D[1], act = D[2];
+      if (L < 1 || L > 4096 || W < 8 || W % 8 || W > 65536 || act < 0 || act > 2) {
+        *err = fmt("MLP dims {layers=%lld, width=%lld, act=%lld}: need layers>=1, width%%8==0, act in 0..2",
+                   L, W, act);
+        return false;
+      }
+      if (d->dtype != TP_F32 && d->dtype != TP_BF16) { *err = "MLP dtype must be TP_F32 or TP_BF16"; return false; }
+      for (int l = 0; l < L; ++l) { add(l, TP_ROLE_W, W, W); add(l, TP_ROLE_B, W); }
+      *n_layers = L;
+      return true;
+    }
+    case TP_ARCH_RESNET50: {
+      const int classes = D[0], image = D[1];
+      if (classes < 1 || classes > 65536 || image < 32 || image % 32 || image > 1024) {
+        *err = fmt("ResNet dims {classes=%lld, image=%lld}: need classes>=1, image%%32==0, 32<=image<=1024",
+                   classes, image);
+        return false;
+      }
+      if (d->dtype != TP_BF16) { *err = "ResNet dtype must be TP_BF16"; return false; }
+      auto convs = resnet50_convs();
+      uint32_t l = 0;
+      for (auto& c : convs) { add(l, TP_ROLE_W, c.cout, c.k, c.k, c.cin); add(l, TP_ROLE_B, c.cout); ++l; }
+      add(l, TP_ROLE_W, classes, 2048); add(l, TP_ROLE_B, classes);
+      *n_layers = l + 1;
+      return true;
+    }
+    case TP_ARCH_BERT: {
+      const int L = D[0], dm = D[1], H = D[2], F = D[3], S = D[4], V = D[5], P = D[6];
+      if (L < 1 || H < 1 || dm != 64 * H || dm > 1024 || F < 8 || F % 8 || F > 16384 || S < 32 || S % 32 ||
+          S > 256 || P < S || V < 1) {
+        *err = "BERT dims {layers, d, heads, ffn, seq, vocab, maxpos}: need d == 64*heads <= 1024, "
+               "ffn%8==0, seq%32==0, 32<=seq<=256, maxpos>=seq, vocab>=1";
+        return false;
+      }
+      if (d->dtype != TP_BF16) { *err = "BERT dtype must be TP_BF16"; return false; }
+      add(0, TP_ROLE_TOK_EMB, V, dm); add(0, TP_ROLE_POS_EMB, P, dm); add(0, TP_ROLE_TYPE_EMB, 2, dm);
+      add(0, TP_ROLE_EMB_LN_G, dm); add(0, TP_ROLE_EMB_LN_B, dm);
+      for (int l = 1; l <= L; ++l) {
+        add(l, TP_ROLE_QKV_W, 3 * dm, dm); add(l, TP_ROLE_QKV_B, 3 * dm);
+        add(l, TP_ROLE_O_W, dm, dm); add(l, TP_ROLE_O_B, dm);
+        add(l, TP_ROLE_LN1_G, dm); add(l, TP_ROLE_LN1_B, dm);
+        add(l, TP_ROLE_FFN1_W, F, dm); add(l, TP_ROLE_FFN1_B, F);
+        add(l, TP_ROLE_FFN2_W, dm, F); add(l, TP_ROLE_FFN2_B, dm);
+        add(l, TP_ROLE_LN2_G, dm); add(l, TP_ROLE_LN2_B, dm);
+      }
+      *n_layers = L + 1;
+      return true;
+    }
+    default:
+      *err = fmt("unknown arch %lld", d->arch);
+      return false;
+  }
+}
+
+}  // namespace
+
+tp_status validate_model(const tp_model_desc* d, uint64_t host_bytes, ModelSpec* out, std::string* err) {
+  if (!d || !out) { *err = "NULL descriptor"; return TP_E_INVAL; }
+  if (d->n_tensors == 0 || !d->tensors) { *err = "descriptor has no tensors"; return TP_E_INVAL; }
+  std::vector<Want> want;
+  uint32_t n_layers = 0;
+  if (!expected(d, &want, &n_layers, err)) return TP_E_INVAL;
+  if (d->n_tensors != want.size()) {
+    *err = fmt("descriptor lists %lld tensors, the architecture has %lld", d->n_tensors, (long long)want.size());
+    return TP_E_INVAL;
+  }
+  const uint64_t esz = d->dtype == TP_F32 ? 4 : 2;
+  ModelSpec m;
+  m.arch = d->arch;
+  m.dtype = d->dtype;
+  std::copy(d->dims, d->dims + 8, m.dims);
+  m.n_layers = n_layers;
+  m.lookup.assign((size_t)n_layers * ModelSpec::kRoles, -1);
+  m.tensors.assign(d->tensors, d->tensors + d->n_tensors);
+  uint64_t prev_end = 0;
+  uint32_t prev_layer = 0;
+  for (uint32_t i = 0; i < d->n_tensors; ++i) {
+    const tp_tensor_desc& t = d->tensors[i];
+    if (t.layer >= n_layers || t.role >= (uint32_t)ModelSpec::kRoles) {
+      *err = fmt("tensor %lld: layer %lld / role %lld out of range", i, t.layer, t.role);
+      return TP_E_INVAL;
+    }
+    int32_t& slot = m.lookup[t.layer * ModelSpec::kRoles + t.role];
+    if (slot >= 0) { *err = fmt("tensor %lld: duplicate (layer %lld, role %lld)", i, t.layer, t.role); return TP_E_INVAL; }
+    slot = (int32_t)i;
+    if (i > 0 && t.layer < prev_layer) {
+      *err = fmt("tensor %lld: layers must not decrease (first-use order)", i);
+      return TP_E_INVAL;
+    }
+    if (t.offset % 256) { *err = fmt("tensor %lld: offset %lld not 256-byte aligned", i, (long long)t.offset); return TP_E_INVAL; }
+    if (i > 0 && t.offset < prev_end) { *err = fmt("tensor %lld overlaps or precedes the previous one", i); return TP_E_INVAL; }
+    if (t.offset + t.bytes > host_bytes || t.offset + t.bytes < t.offset) {
+      *err = fmt("tensor %lld: [%lld, +%lld) exceeds the host buffer", i, (long long)t.offset, (long long)t.bytes);
+      return TP_E_INVAL;
+    }
+    prev_end = t.offset + t.bytes;
+    prev_layer = t.layer;
+    m.param_bytes += t.bytes;
+  }
+  for (const Want& w : want) {
+    const int32_t idx = m.lookup[w.layer * ModelSpec::kRoles + w.role];
+    if (idx < 0) { *err = fmt("missing tensor (layer %lld, role %lld)", w.layer, w.role); return TP_E_INVAL; }
+    const tp_tensor_desc& t = m.tensors[idx];
+    uint64_t n = 1;
+    for (int k = 0; k < 4; ++k) {
+      if (t.shape[k] != w.shape[k]) {
+        *err = fmt("tensor (layer %lld, role %lld): shape[%lld] = %lld differs from the architecture",
+                   w.layer, w.role, k, t.shape[k]);
+        return TP_E_INVAL;
+      }
+      if (w.shape[k]) n *= (uint64_t)w.shape[k];
+    }
+    if (t.bytes != n * esz) {
+      *err = fmt("tensor (layer %lld, role %lld): %lld bytes, shape needs %lld", w.layer, w.role,
+                 (long long)t.bytes, (long long)(n * esz));
+      return TP_E_INVAL;
+    }
+  }
+  m.host_bytes = round_up(host_bytes, 256);
+  *out = std::move(m);
+  return TP_OK;
+}
+
+std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes) {
+  // per-layer byte spans in first-use order
+  struct Span { uint32_t layer; uint64_t begin, end; };
+  std::vector<Span> spans;
+  for (const auto& t : m.tensors) {
+    if (!spans.empty() && spans.back().layer == t.layer) spans.back().end = t.offset + t.bytes;
+    else spans.push_back({t.layer, t.offset, t.offset + t.bytes});
+  }
+  std::vector<Chunk> out;
+  bool open = false;
+  Chunk cur{};
+  for (const Span& s : spans) {
+    if (!open) {
+      cur.begin = out.empty() ? 0 : s.begin;
+      cur.first_layer = s.layer;
+      open = true;
+    }
+    cur.end = s.end;
+    cur.last_layer = s.layer;
+    if (cur.end - cur.begin >= min_bytes) { out.push_back(cur); open = false; }
+  }
+  if (open) out.push_back(cur);
+  for (size_t i = 0; i + 1 < out.size(); ++i) out[i].end = out[i + 1].begin;
+  out.back().end = m.host_bytes;
+  return out;
+}
+
+uint64_t workspace_bytes(const ModelSpec& m, int32_t batch) {
+  const uint64_t B = (uint64_t)std::max(batch, 1);
+  switch (m.arch) {
+    case TP_ARCH_MLP: {
+      const uint64_t esz = m.dtype == TP_F32 ? 4 : 2;
+      return 2 * round_up(B * m.dims[1] * esz, 256);
+    }
+    case TP_ARCH_RESNET50: {
+      // five activation buffers sized for the largest per-sample activation, plus the
+      // pooled features
+      uint64_t best = 0;
+      for (const auto& g : resnet50_geometry(m.dims[1]))
+        best = std::max(best, (uint64_t)g.hout * g.hout * g.c.cout);
+      return 5 * round_up(B * best * 2, 256) + round_up(B * 2048 * 2, 256);
+    }
+    case TP_ARCH_BERT: {
+      const uint64_t M = B * m.dims[4], d = m.dims[1], F = m.dims[3];
+      return round_up(M * d * 2, 256) * 2 + round_up(M * 3 * d * 2, 256) + round_up(M * d * 4, 256) +
+             round_up(M * F * 2, 256);
+    }
+  }
+  return 0;
+}
+
+}  // namespace tp

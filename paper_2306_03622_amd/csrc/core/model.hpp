@@ -1,0 +1,61 @@
+// Model descriptors: validation against each family's architecture, the transfer-chunk
+// plan and workspace sizing. Host-only C++ (no HIP).
+#pragma once
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "torpor.h"
+
+namespace tp {
+
+struct ConvShape {      // one convolution of the ResNet family, in first-use order
+  int cout, k, cin, stride, pad;
+};
+
+// The 53 convolutions of ResNet-50 v1.5 (per bottleneck: 1x1, 3x3 carrying the stage
+// stride, 1x1, then the projection shortcut in each stage's first block).
+std::vector<ConvShape> resnet50_convs();
+
+struct ConvGeom {       // a convolution with its input and output spatial size
+  ConvShape c;
+  int hin, hout;
+};
+// Geometry of every convolution at a square input of `image` pixels (conv1, then the
+// 3x3/2 pad-1 max-pool, then the bottlenecks; the shortcut reads the block input).
+std::vector<ConvGeom> resnet50_geometry(int image);
+
+struct Chunk {
+  uint64_t begin, end;          // host byte range [begin, end)
+  uint32_t first_layer, last_layer;
+};
+
+struct ModelSpec {
+  int32_t arch = 0, dtype = 0;
+  int32_t dims[8] = {};
+  std::vector<tp_tensor_desc> tensors;
+  uint64_t host_bytes = 0;      // rounded up to 256
+  uint64_t param_bytes = 0;
+  uint32_t n_layers = 0;
+  std::vector<int32_t> lookup;  // (layer * kRoles + role) -> tensor index, -1 if absent
+  static constexpr int kRoles = 32;
+
+  const tp_tensor_desc& t(uint32_t layer, uint32_t role) const {
+    return tensors[lookup[layer * kRoles + role]];
+  }
+};
+
+// Validates `d` against its family (see torpor.h) and fills `out`. Returns TP_OK or
+// TP_E_INVAL with a message in *err.
+tp_status validate_model(const tp_model_desc* d, uint64_t host_bytes, ModelSpec* out, std::string* err);
+
+// Greedy grouping in first-use order: whole layers only; a chunk is closed at the first
+// layer boundary where it holds >= min_bytes. Chunks tile [0, host_bytes).
+std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes);
+
+// Workspace needed by the executors for `batch` samples (each buffer 256-aligned).
+uint64_t workspace_bytes(const ModelSpec& m, int32_t batch);
+
+inline uint64_t round_up(uint64_t n, uint64_t a) { return (n + a - 1) / a * a; }
+
+}  // namespace tp

@@ -1,0 +1,92 @@
+// Host-only planning calls (torpor_plan.h) over the arena and model bookkeeping.
+#include <new>
+
+#include "arena.hpp"
+#include "errors.hpp"
+#include "model.hpp"
+#include "torpor_plan.h"
+
+using namespace tp;
+
+struct tph_arena {
+  Arena a;
+  tph_arena(uint64_t c, uint64_t al) : a(c, al) {}
+};
+
+extern "C" {
+
+tp_status tph_validate(const tp_model_desc* desc, uint64_t host_bytes) {
+  ModelSpec m;
+  std::string err;
+  tp_status s = validate_model(desc, host_bytes, &m, &err);
+  return s == TP_OK ? ok() : fail(s, err);
+}
+
+tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes, uint64_t* begin,
+                   uint64_t* end, uint32_t* first_layer, uint32_t cap, uint32_t* n) {
+  ModelSpec m;
+  std::string err;
+  tp_status s = validate_model(desc, host_bytes, &m, &err);
+  if (s != TP_OK) return fail(s, err);
+  if (!n) return fail(TP_E_INVAL, "tph_plan: n is NULL");
+  const auto plan = plan_chunks(m, chunk_min_bytes);
+  *n = (uint32_t)plan.size();
+  for (uint32_t i = 0; i < plan.size() && i < cap; ++i) {
+    if (begin) begin[i] = plan[i].begin;
+    if (end) end[i] = plan[i].end;
+    if (first_layer) first_layer[i] = plan[i].first_layer;
+  }
+  return ok();
+}
+
+tp_status tph_arena_create(uint64_t capacity, uint64_t align, tph_arena** out) {
+  if (!out || align == 0 || (align & (align - 1))) return fail(TP_E_INVAL, "tph_arena_create: bad arguments");
+  *out = new (std::nothrow) tph_arena(capacity, align);
+  return *out ? ok() : fail(TP_E_NOSPC, "out of host memory");
+}
+
+tp_status tph_arena_destroy(tph_arena* a) {
+  delete a;
+  return ok();
+}
+
+tp_status tph_arena_register(tph_arena* a, int32_t id, uint64_t bytes) {
+  if (!a) return fail(TP_E_INVAL, "NULL arena");
+  if (a->a.add_model(id, bytes) != TP_OK) return fail(TP_E_STATE, "model id already registered");
+  return ok();
+}
+
+tp_status tph_arena_unregister(tph_arena* a, int32_t id) {
+  if (!a) return fail(TP_E_INVAL, "NULL arena");
+  if (!a->a.known(id)) return fail(TP_E_NOENT, "unknown model id");
+  a->a.remove_model(id);
+  return ok();
+}
+
+tp_status tph_arena_request(tph_arena* a, int32_t id, int32_t* hit, uint64_t* offset, int32_t* victims,
+                            uint32_t cap, uint32_t* n_victims) {
+  if (!a) return fail(TP_E_INVAL, "NULL arena");
+  if (!a->a.known(id)) return fail(TP_E_NOENT, "unknown model id");
+  if (!a->a.fits_at_all(id)) return fail(TP_E_NOSPC, "model larger than the arena");
+  Arena::Decision d = a->a.request(id);
+  if (hit) *hit = d.hit;
+  if (offset) *offset = d.offset;
+  if (n_victims) *n_victims = (uint32_t)d.victims.size();
+  for (uint32_t i = 0; victims && i < d.victims.size() && i < cap; ++i) victims[i] = d.victims[i];
+  return ok();
+}
+
+tp_status tph_arena_evict(tph_arena* a, int32_t id) {
+  if (!a) return fail(TP_E_INVAL, "NULL arena");
+  if (!a->a.known(id)) return fail(TP_E_NOENT, "unknown model id");
+  a->a.evict(id);
+  return ok();
+}
+
+tp_status tph_arena_stats(tph_arena* a, tp_arena_stats_t* out) {
+  if (!a || !out) return fail(TP_E_INVAL, "NULL argument");
+  a->a.stats(out);
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,348 @@
+// The C ABI of libtorpor (torpor.h): registration into a pinned host pool, admission
+// into the HBM arena, the chunked swap-in on the copy stream with one event per chunk,
+// and the per-layer handoff to the caller's compute stream.
+#include "runtime.hpp"
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+
+#include "../core/errors.hpp"
+#include "../kernels/kernels.hpp"
+
+using namespace tp;
+
+namespace {
+
+tp_status hip_fail(hipError_t e, const char* what) {
+  return fail(TP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define TP_HIP(call)                                  \
+  do {                                                \
+    hipError_t e_ = (call);                           \
+    if (e_ != hipSuccess) return hip_fail(e_, #call); \
+  } while (0)
+
+Model* find(tp_ctx* c, int32_t id) {
+  auto it = c->models.find(id);
+  return it == c->models.end() ? nullptr : it->second.get();
+}
+
+void free_model(Model* m) {
+  for (hipEvent_t e : m->chunk_ev)
+    if (e) (void)hipEventDestroy(e);
+  if (m->last_use) (void)hipEventDestroy(m->last_use);
+  if (m->host) (void)hipHostFree(m->host);
+}
+
+// The extent [off, off + len) of model `id` was invalidated; its old owner's enqueued
+// work may still read it, so whoever writes it next must first wait for that work.
+tp_status retire(tp_ctx* c, int32_t id, uint64_t off, uint64_t len) {
+  c->retired.push_back({off, len, id});
+  if (c->cfg.flags & TP_FLAG_POISON) {
+    Model* m = find(c, id);
+    if (m && m->used) TP_HIP(hipStreamWaitEvent(c->copy, m->last_use, 0));
+    TP_HIP(hipMemsetAsync(c->arena + off, 0xFF, len, c->copy));
+  }
+  return ok();
+}
+
+// Orders the copy stream after every retired owner of bytes in [off, off + len) and
+// drops those bytes from the retired set (the new owner's own last use guards them now).
+tp_status claim(tp_ctx* c, uint64_t off, uint64_t len) {
+  std::vector<tp_ctx::Retired> keep;
+  const uint64_t end = off + len;
+  for (const auto& r : c->retired) {
+    const uint64_t rend = r.off + r.len;
+    if (rend <= off || r.off >= end) {
+      keep.push_back(r);
+      continue;
+    }
+    Model* m = find(c, r.model);
+    if (m && m->used) TP_HIP(hipStreamWaitEvent(c->copy, m->last_use, 0));
+    if (r.off < off) keep.push_back({r.off, off - r.off, r.model});
+    if (rend > end) keep.push_back({end, rend - end, r.model});
+  }
+  c->retired.swap(keep);
+  return ok();
+}
+
+tp_status enqueue_swap(tp_ctx* c, Model* m, uint64_t off) {
+  char* dst = c->arena + off;
+  for (size_t i = 0; i < m->chunks.size(); ++i) {
+    const Chunk& ch = m->chunks[i];
+    const uint64_t n = ch.end - ch.begin;
+    if (c->cfg.flags & TP_FLAG_THROTTLE) TP_HIP(k::delay(c->cfg.throttle_us, c->copy));
+    if (c->cfg.copy_method == TP_COPY_GATHER)
+      TP_HIP(k::gather_copy(static_cast<char*>(m->host_dev) + ch.begin, dst + ch.begin, n, c->cfg.gather_wgs,
+                            c->copy));
+    else
+      TP_HIP(hipMemcpyAsync(dst + ch.begin, static_cast<char*>(m->host) + ch.begin, n, hipMemcpyHostToDevice,
+                            c->copy));
+    TP_HIP(hipEventRecord(m->chunk_ev[i], c->copy));
+  }
+  return ok();
+}
+
+// One request's admission: a hit, or victims invalidated, their readers waited for, and
+// the model's chunks enqueued. On failure the model is left non-resident.
+tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
+  Arena::Decision d = c->policy->request(m->id);
+  *swapped = !d.hit;
+  if (d.hit) return ok();
+  tp_status s = TP_OK;
+  for (int32_t v : d.victims)
+    if (s == TP_OK) s = retire(c, v, c->policy->offset(v), c->policy->bytes(v));
+  if (s == TP_OK) s = claim(c, d.offset, m->spec.host_bytes);
+  if (s == TP_OK) s = enqueue_swap(c, m, d.offset);
+  if (s != TP_OK) {
+    const std::string msg = last_error();
+    c->policy->evict(m->id);
+    (void)retire(c, m->id, d.offset, m->spec.host_bytes);
+    return fail(s, msg);
+  }
+  return ok();
+}
+
+tp_status begin_request(tp_ctx* c, hipStream_t stream) {
+  if (c->any_request && stream != c->last_stream) TP_HIP(hipStreamWaitEvent(stream, c->req_done, 0));
+  return ok();
+}
+
+tp_status end_request(tp_ctx* c, Model* m, hipStream_t stream) {
+  TP_HIP(hipEventRecord(m->last_use, stream));
+  m->used = true;
+  TP_HIP(hipEventRecord(c->req_done, stream));
+  c->last_stream = stream;
+  c->any_request = true;
+  return ok();
+}
+
+tp_status check_request(tp_ctx* c, int32_t id, Model** out) {
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  Model* m = find(c, id);
+  if (!m) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  if (!c->policy->fits_at_all(id))
+    return fail(TP_E_NOSPC, "model of " + std::to_string(m->spec.host_bytes) + " bytes exceeds the arena of " +
+                                std::to_string(c->cfg.arena_bytes) + " bytes");
+  *out = m;
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
+  if (!cfg || !out) return fail(TP_E_INVAL, "tp_create: NULL argument");
+  if (!cfg->arena_dev || cfg->arena_bytes == 0) return fail(TP_E_INVAL, "tp_create: empty arena");
+  if ((uintptr_t)cfg->arena_dev % 256) return fail(TP_E_INVAL, "tp_create: arena must be 256-byte aligned");
+  if (cfg->work_bytes && (!cfg->work_dev || (uintptr_t)cfg->work_dev % 256))
+    return fail(TP_E_INVAL, "tp_create: workspace must be non-NULL and 256-byte aligned");
+  if (cfg->copy_method != TP_COPY_MEMCPY && cfg->copy_method != TP_COPY_GATHER)
+    return fail(TP_E_INVAL, "tp_create: unknown copy_method");
+  if (cfg->gather_wgs < 0 || cfg->gather_wgs > 4096 || cfg->throttle_us < 0 || cfg->throttle_us > 100000)
+    return fail(TP_E_INVAL, "tp_create: gather_wgs or throttle_us out of range");
+  std::unique_ptr<tp_ctx> c(new (std::nothrow) tp_ctx);
+  if (!c) return fail(TP_E_NOSPC, "out of host memory");
+  c->cfg = *cfg;
+  if (c->cfg.gather_wgs == 0) c->cfg.gather_wgs = 64;
+  c->arena = static_cast<char*>(cfg->arena_dev);
+  c->work = static_cast<char*>(cfg->work_dev);
+  c->policy.reset(new Arena(cfg->arena_bytes, 256));
+  TP_HIP(hipGetDevice(&c->device));
+  if (cfg->copy_stream) {
+    c->copy = static_cast<hipStream_t>(cfg->copy_stream);
+  } else {
+    TP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
+    c->own_copy = true;
+  }
+  hipError_t e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    if (c->own_copy) (void)hipStreamDestroy(c->copy);
+    return hip_fail(e, "hipEventCreateWithFlags");
+  }
+  *out = c.release();
+  return ok();
+}
+
+tp_status tp_destroy(tp_ctx* c) {
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  hipError_t e = hipStreamSynchronize(c->copy);
+  if (e == hipSuccess && c->any_request) e = hipEventSynchronize(c->req_done);
+  for (auto& kv : c->models) {
+    if (kv.second->used) (void)hipEventSynchronize(kv.second->last_use);
+    free_model(kv.second.get());
+  }
+  (void)hipEventDestroy(c->req_done);
+  if (c->own_copy) (void)hipStreamDestroy(c->copy);
+  delete c;
+  return e == hipSuccess ? ok() : hip_fail(e, "tp_destroy synchronisation");
+}
+
+tp_status tp_register_model(tp_ctx* c, const tp_model_desc* desc, const void* host_weights, uint64_t host_bytes,
+                            int32_t* model_id) {
+  if (!c || !desc || !host_weights || !model_id || host_bytes == 0) return fail(TP_E_INVAL, "tp_register_model: NULL argument");
+  std::unique_ptr<Model> m(new (std::nothrow) Model);
+  if (!m) return fail(TP_E_NOSPC, "out of host memory");
+  std::string err;
+  tp_status s = validate_model(desc, host_bytes, &m->spec, &err);
+  if (s != TP_OK) return fail(s, err);
+  m->id = c->next_id;
+  m->chunks = plan_chunks(m->spec, c->cfg.chunk_min_bytes);
+  m->chunk_of_layer.assign(m->spec.n_layers, 0);
+  for (size_t i = 0; i < m->chunks.size(); ++i)
+    for (uint32_t l = m->chunks[i].first_layer; l <= m->chunks[i].last_layer; ++l) m->chunk_of_layer[l] = (uint32_t)i;
+  const uint64_t nb = m->spec.host_bytes;
+  hipError_t e = hipHostMalloc(&m->host, nb, hipHostMallocMapped);
+  if (e != hipSuccess) { m->host = nullptr; return hip_fail(e, "hipHostMalloc (pinned model copy)"); }
+  std::memcpy(m->host, host_weights, host_bytes);
+  if (nb > host_bytes) std::memset(static_cast<char*>(m->host) + host_bytes, 0, nb - host_bytes);
+  e = hipHostGetDevicePointer(&m->host_dev, m->host, 0);
+  m->chunk_ev.assign(m->chunks.size(), nullptr);
+  for (size_t i = 0; e == hipSuccess && i < m->chunks.size(); ++i)
+    e = hipEventCreateWithFlags(&m->chunk_ev[i], hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->last_use, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    free_model(m.get());
+    return hip_fail(e, "tp_register_model: event or mapping setup");
+  }
+  if (c->policy->add_model(m->id, nb) != TP_OK) {
+    free_model(m.get());
+    return fail(TP_E_STATE, "model id collision");
+  }
+  *model_id = m->id;
+  c->models[m->id] = std::move(m);
+  ++c->next_id;
+  return ok();
+}
+
+tp_status tp_unregister_model(tp_ctx* c, int32_t id) {
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  Model* m = find(c, id);
+  if (!m) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  // the copy stream may still read the host copy; the last use may still read the extent
+  TP_HIP(hipStreamSynchronize(c->copy));
+  if (m->used) TP_HIP(hipEventSynchronize(m->last_use));
+  if (c->policy->resident(id)) c->policy->evict(id);
+  c->retired.erase(std::remove_if(c->retired.begin(), c->retired.end(),
+                                  [&](const tp_ctx::Retired& r) { return r.model == id; }),
+                   c->retired.end());
+  c->policy->remove_model(id);
+  free_model(m);
+  c->models.erase(id);
+  return ok();
+}
+
+tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, void* output_dev, void* stream_) {
+  Model* m = nullptr;
+  tp_status s = check_request(c, id, &m);
+  if (s != TP_OK) return s;
+  if (batch < 1 || !input_dev || !output_dev) return fail(TP_E_INVAL, "tp_infer: batch < 1 or NULL buffer");
+  const uint64_t need = workspace_bytes(m->spec, batch);
+  if (need > c->cfg.work_bytes)
+    return fail(TP_E_NOSPC, "tp_infer: workspace of " + std::to_string(c->cfg.work_bytes) + " bytes, need " +
+                                std::to_string(need));
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if ((s = begin_request(c, stream)) != TP_OK) return s;
+  bool swapped = false;
+  if ((s = admit(c, m, &swapped)) != TP_OK) return s;
+  const uint64_t off = c->policy->offset(id);
+  Waiter w;
+  w.m = m;
+  w.stream = stream;
+  w.swapping = swapped;
+  ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w};
+  hipError_t e = hipErrorInvalidValue;
+  switch (m->spec.arch) {
+    case TP_ARCH_MLP: e = run_mlp(x); break;
+    case TP_ARCH_RESNET50: e = run_resnet(x); break;
+    case TP_ARCH_BERT: e = run_bert(x); break;
+  }
+  if (e != hipSuccess) {
+    // keep the ordering intact, then leave the model non-resident
+    (void)end_request(c, m, stream);
+    c->policy->evict(id);
+    (void)retire(c, id, off, m->spec.host_bytes);
+    return hip_fail(e, "tp_infer: kernel launch");
+  }
+  return end_request(c, m, stream);
+}
+
+tp_status tp_swap_in(tp_ctx* c, int32_t id, void* stream_) {
+  Model* m = nullptr;
+  tp_status s = check_request(c, id, &m);
+  if (s != TP_OK) return s;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if ((s = begin_request(c, stream)) != TP_OK) return s;
+  bool swapped = false;
+  if ((s = admit(c, m, &swapped)) != TP_OK) return s;
+  if (swapped) TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev.back(), 0));
+  return end_request(c, m, stream);
+}
+
+tp_status tp_evict(tp_ctx* c, int32_t id) {
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  if (!find(c, id)) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  if (!c->policy->resident(id)) return ok();
+  const uint64_t off = c->policy->offset(id), len = c->policy->bytes(id);
+  c->policy->evict(id);
+  return retire(c, id, off, len);
+}
+
+tp_status tp_is_resident(tp_ctx* c, int32_t id, int32_t* resident) {
+  if (!c || !resident) return fail(TP_E_INVAL, "NULL argument");
+  if (!find(c, id)) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  *resident = c->policy->resident(id) ? 1 : 0;
+  return ok();
+}
+
+tp_status tp_arena_stats(tp_ctx* c, tp_arena_stats_t* out) {
+  if (!c || !out) return fail(TP_E_INVAL, "NULL argument");
+  c->policy->stats(out);
+  return ok();
+}
+
+tp_status tp_model_info(tp_ctx* c, int32_t id, tp_model_info_t* out) {
+  if (!c || !out) return fail(TP_E_INVAL, "NULL argument");
+  Model* m = find(c, id);
+  if (!m) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  out->host_bytes = m->spec.host_bytes;
+  out->param_bytes = m->spec.param_bytes;
+  out->n_chunks = (uint32_t)m->chunks.size();
+  out->resident = c->policy->resident(id) ? 1 : 0;
+  out->extent_offset = c->policy->offset(id);
+  out->last_use_clock = c->policy->last_use(id);
+  return ok();
+}
+
+tp_status tp_model_chunks(tp_ctx* c, int32_t id, uint64_t* begin, uint64_t* end, uint32_t* first_layer,
+                          uint32_t cap, uint32_t* n) {
+  if (!c || !n) return fail(TP_E_INVAL, "NULL argument");
+  Model* m = find(c, id);
+  if (!m) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  *n = (uint32_t)m->chunks.size();
+  for (uint32_t i = 0; i < m->chunks.size() && i < cap; ++i) {
+    if (begin) begin[i] = m->chunks[i].begin;
+    if (end) end[i] = m->chunks[i].end;
+    if (first_layer) first_layer[i] = m->chunks[i].first_layer;
+  }
+  return ok();
+}
+
+tp_status tp_workspace_bytes(const tp_model_desc* desc, int32_t batch, uint64_t* bytes) {
+  if (!desc || !bytes || batch < 1) return fail(TP_E_INVAL, "tp_workspace_bytes: bad argument");
+  if (!desc->tensors || desc->n_tensors == 0) return fail(TP_E_INVAL, "descriptor has no tensors");
+  uint64_t host = 0;
+  for (uint32_t i = 0; i < desc->n_tensors; ++i)
+    host = std::max(host, desc->tensors[i].offset + desc->tensors[i].bytes);
+  ModelSpec m;
+  std::string err;
+  tp_status s = validate_model(desc, host, &m, &err);
+  if (s != TP_OK) return fail(s, err);
+  *bytes = workspace_bytes(m, batch);
+  return ok();
+}
+
+}  // extern "C"

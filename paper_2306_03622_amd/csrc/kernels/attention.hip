@@ -1,0 +1,127 @@
+// Multi-head self-attention for head dim 64 and short sequences (S <= 256, S % 32 == 0),
+// one workgroup per (sample, head, 64 queries); each wave owns 16 queries.
+//
+// K of the head is staged row-major in LDS and V transposed ([d][key]). Scores are
+// computed as S^T = K Q^T on MFMA (A = 16 keys, B = 16 queries), so lane l holds the
+// scores of query l % 16 against keys 16 t + 4 (l / 16) + e. The softmax reductions
+// over keys therefore stay inside a lane plus two cross-lane exchanges (lanes l ^ 16,
+// l ^ 32), in fp32. The normalised probabilities, rounded to bf16, are used directly as
+// the A operand of O = P V: a 32-key MFMA k-block takes the lane's own values from two
+// consecutive score tiles, and the matching V entries are read from the transposed copy
+// with the same key order, so no data moves between lanes.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace tp {
+namespace k {
+namespace {
+
+template <int SMAX>
+__global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ qkv, int S, int H,
+                                                   uint16_t* __restrict__ out) {
+  constexpr int LDK = 72, LDV = SMAX + 8, NT = SMAX / 16;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[SMAX * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[64 * LDV];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int D = H * 64, ld = 3 * D;
+  const uint16_t* base = qkv + (size_t)b * S * ld;
+
+  for (int v = tid; v < S * 8; v += 256) {
+    const int key = v >> 3, d8 = (v & 7) << 3;
+    const uint16_t* row = base + (size_t)key * ld + h * 64 + d8;
+    *reinterpret_cast<uint4*>(&Ks[key * LDK + d8]) = *reinterpret_cast<const uint4*>(row + D);
+    const uint4 vv = *reinterpret_cast<const uint4*>(row + 2 * D);
+    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      Vt[(d8 + 2 * e) * LDV + key] = (uint16_t)(w[e] & 0xffff);
+      Vt[(d8 + 2 * e + 1) * LDV + key] = (uint16_t)(w[e] >> 16);
+    }
+  }
+  __syncthreads();
+
+  const int q0 = blockIdx.x * 64 + wave * 16;
+  if (q0 >= S) return;
+  const int nt = S >> 4;
+  const uint16_t* qrow = base + (size_t)(q0 + r) * ld + h * 64 + (g << 3);
+  const uint4 qf0 = *reinterpret_cast<const uint4*>(qrow);
+  const uint4 qf1 = *reinterpret_cast<const uint4*>(qrow + 32);
+
+  f32x4 sc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (t < nt) {
+      const uint16_t* krow = &Ks[(16 * t + r) * LDK + (g << 3)];
+      sc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(*reinterpret_cast<const uint4*>(krow)),
+                                                      as_bf16x8(qf0), sc[t], 0, 0, 0);
+      sc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(*reinterpret_cast<const uint4*>(krow + 32)),
+                                                      as_bf16x8(qf1), sc[t], 0, 0, 0);
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+    if (t < nt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[t][e]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  float sum = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+    if (t < nt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = expf((sc[t][e] - mx) * 0.125f);
+        sc[t][e] = p;
+        sum += p;
+      }
+  sum += __shfl_xor(sum, 16, 64);
+  sum += __shfl_xor(sum, 32, 64);
+  const float inv = 1.f / sum;
+
+  f32x4 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < NT / 2; ++u) {
+    if (2 * u < nt) {
+      const f32x4 p0 = sc[2 * u], p1 = sc[2 * u + 1];
+      uint4 pa;
+      pa.x = (uint32_t)f2bf(p0[0] * inv) | ((uint32_t)f2bf(p0[1] * inv) << 16);
+      pa.y = (uint32_t)f2bf(p0[2] * inv) | ((uint32_t)f2bf(p0[3] * inv) << 16);
+      pa.z = (uint32_t)f2bf(p1[0] * inv) | ((uint32_t)f2bf(p1[1] * inv) << 16);
+      pa.w = (uint32_t)f2bf(p1[2] * inv) | ((uint32_t)f2bf(p1[3] * inv) << 16);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        const uint16_t* vr = &Vt[(16 * dt + r) * LDV + 32 * u + 4 * g];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pa), as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)),
+                                                        o[dt], 0, 0, 0);
+      }
+    }
+  }
+  // lane holds O[query q0 + 4 g + e][d = 16 dt + r]
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      out[((size_t)b * S + q0 + 4 * g + e) * D + h * 64 + 16 * dt + r] = f2bf(o[dt][e]);
+}
+
+}  // namespace
+
+hipError_t attention(const uint16_t* qkv, int B, int S, int H, uint16_t* out, hipStream_t s) {
+  if (!qkv || !out || B < 1 || H < 1 || S < 32 || (S & 31) || S > 256) return hipErrorInvalidValue;
+  dim3 grid((S + 63) / 64, H, B);
+  if (S <= 128) hipLaunchKernelGGL((k_attention<128>), grid, dim3(256), 0, s, qkv, S, H, out);
+  else hipLaunchKernelGGL((k_attention<256>), grid, dim3(256), 0, s, qkv, S, H, out);
+  return hipGetLastError();
+}
+
+}  // namespace k
+}  // namespace tp

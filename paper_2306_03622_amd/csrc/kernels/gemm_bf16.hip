@@ -1,0 +1,311 @@
+// bf16 contractions on gfx950 MFMA (v_mfma_f32_16x16x32_bf16), fp32 accumulate, with a
+// fused epilogue (bias, optional residual, ReLU/GELU, bf16 or fp32 store).
+//
+// Convention for every kernel here: the MFMA "A" operand is a 16-row block of the weight
+// matrix W[N][K] (rows = output features n) and the "B" operand a 16-row block of the
+// activations X[M][K] (rows = tokens / output pixels m). Both are read as 8 consecutive
+// k per lane, lane l covering row (l % 16) and k-slot (l / 16), so one accumulator
+// register e of lane l holds D[n = 4 (l / 16) + e][m = l % 16]: four consecutive output
+// features of one row, which the epilogue stores as one vector.
+//
+// Two kernels:
+//   * k_gemv: skinny M (<= 32). The weights dominate the traffic (HBM-bound), so each
+//     workgroup owns 16 weight rows and its 16 waves stream disjoint 128-wide k-blocks
+//     with 4 x 16-byte loads per lane in flight, then reduce across waves through LDS in
+//     a fixed order.
+//   * k_gemm: LDS-tiled BN x BM x 32 tiles, 4 waves in a 2 x 2 arrangement, global loads
+//     of the next k-stage issued before the MFMAs of the current one. The activation
+//     loader is either a plain row-major matrix or an NHWC implicit-GEMM (im2col) gather
+//     for convolutions, k = (kh * KW + kw) * C + c, matching OHWI weight rows.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace tp {
+namespace k {
+
+namespace {
+
+enum { X_ROWS = 0, X_CONV8 = 1, X_CONV1 = 2 };
+
+struct GemmArgs {
+  const uint16_t* x;
+  const uint16_t* w;
+  int M, N, K;
+  int H, W, C, KW, stride, pad, Ho, Wo;   // convolution geometry (X_CONV*)
+  Epilogue ep;
+};
+
+__device__ __forceinline__ void store_row4(const GemmArgs& a, int m, int n0, f32x4 acc) {
+  if (m >= a.M || n0 >= a.N) return;
+  const Epilogue& ep = a.ep;
+  const size_t base = (size_t)m * a.N + n0;
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = acc[e];
+  const bool full = (n0 + 3 < a.N) && ((a.N & 3) == 0);
+  if (full) {
+    if (ep.bias) {
+      const uint2 b = *reinterpret_cast<const uint2*>(ep.bias + n0);
+      v[0] += bf2f(b.x & 0xffff); v[1] += bf2f(b.x >> 16); v[2] += bf2f(b.y & 0xffff); v[3] += bf2f(b.y >> 16);
+    }
+    if (ep.res) {
+      if (ep.res_f32) {
+        const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(ep.res) + base);
+        v[0] += r.x; v[1] += r.y; v[2] += r.z; v[3] += r.w;
+      } else {
+        const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(ep.res) + base);
+        v[0] += bf2f(r.x & 0xffff); v[1] += bf2f(r.x >> 16); v[2] += bf2f(r.y & 0xffff); v[3] += bf2f(r.y >> 16);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = act_apply(v[e], ep.act);
+    if (ep.out_f32) {
+      *reinterpret_cast<float4*>(static_cast<float*>(ep.out) + base) = make_float4(v[0], v[1], v[2], v[3]);
+    } else {
+      uint2 o;
+      o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+      o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(ep.out) + base) = o;
+    }
+    return;
+  }
+  for (int e = 0; e < 4 && n0 + e < a.N; ++e) {
+    float t = v[e];
+    if (ep.bias) t += bf2f(ep.bias[n0 + e]);
+    if (ep.res) t += ep.res_f32 ? static_cast<const float*>(ep.res)[base + e]
+                                : bf2f(static_cast<const uint16_t*>(ep.res)[base + e]);
+    t = act_apply(t, ep.act);
+    if (ep.out_f32) static_cast<float*>(ep.out)[base + e] = t;
+    else static_cast<uint16_t*>(ep.out)[base + e] = f2bf(t);
+  }
+}
+
+// ------------------------------------------------------------------ skinny M
+
+template <int MT, int NW>
+__global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, q = lane >> 4;
+  const int n0 = blockIdx.x * 16;
+  const bool nvalid = n0 + r < a.N;
+  const uint16_t* wrow = a.w + (size_t)(nvalid ? n0 + r : 0) * a.K;
+  const uint4 zero = make_uint4(0, 0, 0, 0);
+  f32x4 acc[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nkb = (a.K + 127) >> 7;
+  for (int kb = wave; kb < nkb; kb += NW) {
+    const int kbase = (kb << 7) + (q << 5);
+    uint4 av[4], bv[MT][4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kk = kbase + (j << 3);
+      av[j] = (nvalid && kk < a.K) ? *reinterpret_cast<const uint4*>(wrow + kk) : zero;
+    }
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const int m = (t << 4) + r;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kk = kbase + (j << 3);
+        bv[t][j] = (m < a.M && kk < a.K) ? *reinterpret_cast<const uint4*>(a.x + (size_t)m * a.K + kk) : zero;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[j]), as_bf16x8(bv[t][j]), acc[t], 0, 0, 0);
+  }
+  __shared__ f32x4 red[NW][MT][64];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) red[wave][t][lane] = acc[t];
+  __syncthreads();
+  if (wave < MT) {
+    f32x4 s = red[0][wave][lane];
+    for (int w = 1; w < NW; ++w) s += red[w][wave][lane];
+    store_row4(a, (wave << 4) + r, n0 + (q << 2), s);
+  }
+}
+
+// ------------------------------------------------------------------ tiled
+
+struct RowInfo {
+  int b, ih0, iw0;   // conv: sample and top-left input corner; rows: b = m
+  bool valid;
+};
+
+template <int MODE>
+__device__ __forceinline__ RowInfo row_info(const GemmArgs& a, int m) {
+  RowInfo ri;
+  ri.valid = m < a.M;
+  if (MODE == X_ROWS) {
+    ri.b = m; ri.ih0 = 0; ri.iw0 = 0;
+  } else {
+    const int mm = ri.valid ? m : 0;
+    const int hw = a.Ho * a.Wo;
+    ri.b = mm / hw;
+    const int rem = mm - ri.b * hw;
+    const int oh = rem / a.Wo, ow = rem - (rem / a.Wo) * a.Wo;
+    ri.ih0 = oh * a.stride - a.pad;
+    ri.iw0 = ow * a.stride - a.pad;
+  }
+  return ri;
+}
+
+template <int MODE>
+__device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, int k) {
+  const uint4 zero = make_uint4(0, 0, 0, 0);
+  if (!ri.valid || k >= a.K) return zero;
+  if (MODE == X_ROWS) return *reinterpret_cast<const uint4*>(a.x + (size_t)ri.b * a.K + k);
+  if (MODE == X_CONV8) {
+    const int tap = k / a.C, c = k - tap * a.C;
+    const int kh = tap / a.KW, kw = tap - kh * a.KW;
+    const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
+    if (ih < 0 || ih >= a.H || iw < 0 || iw >= a.W) return zero;
+    return *reinterpret_cast<const uint4*>(a.x + (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c);
+  }
+  uint16_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int kk = k + e;
+    v[e] = 0;
+    if (kk < a.K) {
+      const int tap = kk / a.C, c = kk - tap * a.C;
+      const int kh = tap / a.KW, kw = tap - kh * a.KW;
+      const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
+      if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) v[e] = a.x[(((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c];
+    }
+  }
+  return make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16), v[4] | ((uint32_t)v[5] << 16),
+                    v[6] | ((uint32_t)v[7] << 16));
+}
+
+template <bool WVEC>
+__device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
+  if (n >= a.N || k >= a.K) return make_uint4(0, 0, 0, 0);
+  const uint16_t* p = a.w + (size_t)n * a.K + k;
+  if (WVEC) return *reinterpret_cast<const uint4*>(p);
+  uint16_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (k + e < a.K) ? p[e] : (uint16_t)0;
+  return make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16), v[4] | ((uint32_t)v[5] << 16),
+                    v[6] | ((uint32_t)v[7] << 16));
+}
+
+template <int BN, int BM, int MODE, bool WVEC>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+  constexpr int BK = 32, LDK = BK + 8;
+  constexpr int VA = BN / 64, VB = BM / 64;      // 16-byte vectors per thread per stage
+  constexpr int NB = BN / 32, MB = BM / 32;      // 16 x 16 MFMA blocks per wave
+  __shared__ __attribute__((aligned(16))) uint16_t As[BN * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[BM * LDK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int n_base = blockIdx.x * BN, m_base = blockIdx.y * BM;
+  const int kq = (tid & 3) << 3;
+
+  RowInfo ri[VB];
+#pragma unroll
+  for (int p = 0; p < VB; ++p) ri[p] = row_info<MODE>(a, m_base + (tid >> 2) + 64 * p);
+
+  f32x4 acc[NB][MB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int j = 0; j < MB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  uint4 ra[VA], rb[VB];
+  const int nst = (a.K + BK - 1) / BK;
+  auto load_stage = [&](int s) {
+    const int k = s * BK + kq;
+#pragma unroll
+    for (int p = 0; p < VA; ++p) ra[p] = load_w8<WVEC>(a, n_base + (tid >> 2) + 64 * p, k);
+#pragma unroll
+    for (int p = 0; p < VB; ++p) rb[p] = load_x8<MODE>(a, ri[p], k);
+  };
+  load_stage(0);
+  for (int s = 0; s < nst; ++s) {
+#pragma unroll
+    for (int p = 0; p < VA; ++p) *reinterpret_cast<uint4*>(&As[((tid >> 2) + 64 * p) * LDK + kq]) = ra[p];
+#pragma unroll
+    for (int p = 0; p < VB; ++p) *reinterpret_cast<uint4*>(&Bs[((tid >> 2) + 64 * p) * LDK + kq]) = rb[p];
+    __syncthreads();
+    if (s + 1 < nst) load_stage(s + 1);
+    uint4 fa[NB], fb[MB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      fa[i] = *reinterpret_cast<const uint4*>(&As[(wn * (BN / 2) + i * 16 + (lane & 15)) * LDK + ((lane >> 4) << 3)]);
+#pragma unroll
+    for (int j = 0; j < MB; ++j)
+      fb[j] = *reinterpret_cast<const uint4*>(&Bs[(wm * (BM / 2) + j * 16 + (lane & 15)) * LDK + ((lane >> 4) << 3)]);
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+#pragma unroll
+      for (int j = 0; j < MB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[i]), as_bf16x8(fb[j]), acc[i][j], 0, 0, 0);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+#pragma unroll
+    for (int j = 0; j < MB; ++j)
+      store_row4(a, m_base + wm * (BM / 2) + j * 16 + (lane & 15),
+                 n_base + wn * (BN / 2) + i * 16 + ((lane >> 4) << 2), acc[i][j]);
+}
+
+template <int BN, int BM, int MODE, bool WVEC>
+hipError_t launch_tiled(const GemmArgs& a, hipStream_t s) {
+  dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM);
+  hipLaunchKernelGGL((k_gemm<BN, BM, MODE, WVEC>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int MODE, bool WVEC>
+hipError_t pick_tiled(const GemmArgs& a, hipStream_t s) {
+  const long tiles128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
+  if (tiles128 >= 240) return launch_tiled<128, 128, MODE, WVEC>(a, s);
+  return launch_tiled<64, 64, MODE, WVEC>(a, s);
+}
+
+bool ep_ok(const Epilogue& ep) { return ep.out != nullptr && ep.act >= 0 && ep.act <= 2; }
+
+}  // namespace
+
+hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N, const Epilogue& ep,
+                       hipStream_t s) {
+  if (!x || !w || M < 1 || N < 1 || K < 8 || (K & 7) || !ep_ok(ep)) return hipErrorInvalidValue;
+  GemmArgs a{};
+  a.x = x; a.w = w; a.M = M; a.N = N; a.K = K; a.ep = ep;
+  if (M <= 16) {
+    hipLaunchKernelGGL((k_gemv<1, 16>), dim3((N + 15) / 16), dim3(1024), 0, s, a);
+    return hipGetLastError();
+  }
+  if (M <= 32) {
+    hipLaunchKernelGGL((k_gemv<2, 16>), dim3((N + 15) / 16), dim3(1024), 0, s, a);
+    return hipGetLastError();
+  }
+  return pick_tiled<X_ROWS, true>(a, s);
+}
+
+hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16_t* w, int O, int KH, int KW,
+                     int stride, int pad, const Epilogue& ep, hipStream_t s) {
+  if (!x || !w || B < 1 || H < 1 || W < 1 || C < 1 || O < 1 || KH < 1 || KW < 1 || stride < 1 || pad < 0 ||
+      !ep_ok(ep))
+    return hipErrorInvalidValue;
+  const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
+  if (Ho < 1 || Wo < 1) return hipErrorInvalidValue;
+  if (KH == 1 && KW == 1 && stride == 1 && pad == 0 && (C & 7) == 0)
+    return linear_bf16(x, B * H * W, C, w, O, ep, s);
+  GemmArgs a{};
+  a.x = x; a.w = w; a.M = B * Ho * Wo; a.N = O; a.K = KH * KW * C;
+  a.H = H; a.W = W; a.C = C; a.KW = KW; a.stride = stride; a.pad = pad; a.Ho = Ho; a.Wo = Wo;
+  a.ep = ep;
+  if ((C & 7) == 0) return pick_tiled<X_CONV8, true>(a, s);
+  if ((a.K & 7) == 0) return pick_tiled<X_CONV1, true>(a, s);
+  return pick_tiled<X_CONV1, false>(a, s);
+}
+
+}  // namespace k
+}  // namespace tp

@@ -1,0 +1,112 @@
+// Pooling (NHWC bf16), the host-to-device gather copy, and the bounded delay kernel.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace tp {
+namespace k {
+namespace {
+
+// one thread per (sample, output pixel, 8 channels); padded taps are skipped (never win)
+__global__ __launch_bounds__(256) void k_maxpool3s2(const uint16_t* __restrict__ x, int B, int H, int W, int C,
+                                                    int Ho, int Wo, uint16_t* __restrict__ y) {
+  const int c8n = C >> 3;
+  const long total = (long)B * Ho * Wo * c8n;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int c8 = (int)(i % c8n);
+  long p = i / c8n;
+  const int ow = (int)(p % Wo);
+  p /= Wo;
+  const int oh = (int)(p % Ho);
+  const int b = (int)(p / Ho);
+  float m[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
+  for (int dh = 0; dh < 3; ++dh) {
+    const int ih = oh * 2 - 1 + dh;
+    if (ih < 0 || ih >= H) continue;
+    for (int dw = 0; dw < 3; ++dw) {
+      const int iw = ow * 2 - 1 + dw;
+      if (iw < 0 || iw >= W) continue;
+      const uint4 v = *reinterpret_cast<const uint4*>(x + (((size_t)b * H + ih) * W + iw) * C + c8 * 8);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        m[2 * e] = fmaxf(m[2 * e], bf2f(w[e] & 0xffff));
+        m[2 * e + 1] = fmaxf(m[2 * e + 1], bf2f(w[e] >> 16));
+      }
+    }
+  }
+  uint4 o;
+  o.x = (uint32_t)f2bf(m[0]) | ((uint32_t)f2bf(m[1]) << 16);
+  o.y = (uint32_t)f2bf(m[2]) | ((uint32_t)f2bf(m[3]) << 16);
+  o.z = (uint32_t)f2bf(m[4]) | ((uint32_t)f2bf(m[5]) << 16);
+  o.w = (uint32_t)f2bf(m[6]) | ((uint32_t)f2bf(m[7]) << 16);
+  *reinterpret_cast<uint4*>(y + (((size_t)b * Ho + oh) * Wo + ow) * C + c8 * 8) = o;
+}
+
+// one thread per (sample, channel), positions summed in order in fp32
+__global__ __launch_bounds__(256) void k_avgpool(const uint16_t* __restrict__ x, int B, int HW, int C,
+                                                 uint16_t* __restrict__ y) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= B * C) return;
+  const int b = i / C, c = i - b * C;
+  const uint16_t* p = x + (size_t)b * HW * C + c;
+  float s = 0.f;
+  for (int j = 0; j < HW; ++j) s += bf2f(p[(size_t)j * C]);
+  y[i] = f2bf(s / (float)HW);
+}
+
+// grid-stride copy with U independent 16-byte loads in flight per thread
+__global__ __launch_bounds__(256) void k_gather(const uint4* __restrict__ src, uint4* __restrict__ dst, uint64_t n) {
+  constexpr int U = 8;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  for (; i + (U - 1) * stride < n; i += U * stride) {
+    uint4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = src[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < U; ++u) dst[i + u * stride] = v[u];
+  }
+  for (; i < n; i += stride) dst[i] = src[i];
+}
+
+__global__ void k_delay(int iters) {
+  for (int i = 0; i < iters; ++i) __builtin_amdgcn_s_sleep(127);
+}
+
+}  // namespace
+
+hipError_t maxpool3s2(const uint16_t* x, int B, int H, int W, int C, uint16_t* y, hipStream_t s) {
+  if (!x || !y || B < 1 || H < 1 || W < 1 || C < 8 || (C & 7)) return hipErrorInvalidValue;
+  const int Ho = (H + 2 - 3) / 2 + 1, Wo = (W + 2 - 3) / 2 + 1;
+  const long total = (long)B * Ho * Wo * (C >> 3);
+  hipLaunchKernelGGL(k_maxpool3s2, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, B, H, W, C, Ho, Wo, y);
+  return hipGetLastError();
+}
+
+hipError_t avgpool(const uint16_t* x, int B, int HW, int C, uint16_t* y, hipStream_t s) {
+  if (!x || !y || B < 1 || HW < 1 || C < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_avgpool, dim3((B * C + 255) / 256), dim3(256), 0, s, x, B, HW, C, y);
+  return hipGetLastError();
+}
+
+hipError_t gather_copy(const void* src, void* dst, uint64_t bytes, int wgs, hipStream_t s) {
+  if (!src || !dst || (bytes & 15) || wgs < 1 || ((uintptr_t)src & 15) || ((uintptr_t)dst & 15))
+    return hipErrorInvalidValue;
+  if (bytes == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather, dim3(wgs), dim3(256), 0, s, static_cast<const uint4*>(src), static_cast<uint4*>(dst),
+                     bytes >> 4);
+  return hipGetLastError();
+}
+
+hipError_t delay(int us, hipStream_t s) {
+  // s_sleep 127 is about 127 * 64 cycles, ~3.4 us at 2.4 GHz
+  const int iters = us <= 3 ? 1 : us / 3;
+  hipLaunchKernelGGL(k_delay, dim3(1), dim3(64), 0, s, iters);
+  return hipGetLastError();
+}
+
+}  // namespace k
+}  // namespace tp

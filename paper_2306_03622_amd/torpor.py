@@ -1,0 +1,389 @@
+"""ctypes binding of libtorpor (include/torpor.h, include/torpor_plan.h).
+
+Argument marshalling only: every step of swap-in and execution runs in the library's
+HIP code. The functions keep the C names; failures raise ``TorporError`` carrying the
+status code and ``tp_last_error()``. ``Runtime`` is a convenience wrapper that lets
+torch allocate the arena and workspace once and passes torch streams through.
+
+The library is loaded from this package directory; if it is missing, importing
+``lib()`` raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtorpor.so")
+HOST_LIB_PATH = os.path.join(_HERE, "libtorpor_host.so")
+
+TP_OK, TP_E_INVAL, TP_E_NOENT, TP_E_NOSPC, TP_E_HIP, TP_E_STATE = 0, -1, -2, -3, -4, -5
+TP_F32, TP_BF16 = 0, 1
+TP_ARCH_MLP, TP_ARCH_RESNET50, TP_ARCH_BERT = 0, 1, 2
+TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
+TP_COPY_MEMCPY, TP_COPY_GATHER = 0, 1
+TP_FLAG_POISON, TP_FLAG_THROTTLE = 1, 2
+ROLES = {
+    "w": 0, "b": 1,
+    "tok_emb": 10, "pos_emb": 11, "type_emb": 12, "emb_ln_g": 13, "emb_ln_b": 14,
+    "qkv_w": 20, "qkv_b": 21, "o_w": 22, "o_b": 23, "ln1_g": 24, "ln1_b": 25,
+    "ffn1_w": 26, "ffn1_b": 27, "ffn2_w": 28, "ffn2_b": 29, "ln2_g": 30, "ln2_b": 31,
+}
+ARCHS = {"mlp": TP_ARCH_MLP, "resnet50": TP_ARCH_RESNET50, "bert": TP_ARCH_BERT}
+DTYPES = {"f32": TP_F32, "bf16": TP_BF16}
+
+
+class tp_tensor_desc(C.Structure):
+    _fields_ = [("layer", C.c_uint32), ("role", C.c_uint32), ("offset", C.c_uint64), ("bytes", C.c_uint64),
+                ("shape", C.c_int64 * 4)]
+
+
+class tp_model_desc(C.Structure):
+    _fields_ = [("arch", C.c_int32), ("dtype", C.c_int32), ("dims", C.c_int32 * 8), ("n_tensors", C.c_uint32),
+                ("tensors", C.POINTER(tp_tensor_desc))]
+
+
+class tp_config(C.Structure):
+    _fields_ = [("arena_dev", C.c_void_p), ("arena_bytes", C.c_uint64), ("work_dev", C.c_void_p),
+                ("work_bytes", C.c_uint64), ("copy_stream", C.c_void_p), ("chunk_min_bytes", C.c_uint64),
+                ("copy_method", C.c_int32), ("gather_wgs", C.c_int32), ("flags", C.c_int32),
+                ("throttle_us", C.c_int32)]
+
+
+class tp_arena_stats_t(C.Structure):
+    _fields_ = [("capacity", C.c_uint64), ("used", C.c_uint64), ("largest_free", C.c_uint64),
+                ("resident", C.c_uint32), ("registered", C.c_uint32), ("hits", C.c_uint64),
+                ("misses", C.c_uint64), ("evictions", C.c_uint64), ("frag_evictions", C.c_uint64),
+                ("bytes_swapped", C.c_uint64)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class tp_model_info_t(C.Structure):
+    _fields_ = [("host_bytes", C.c_uint64), ("param_bytes", C.c_uint64), ("n_chunks", C.c_uint32),
+                ("resident", C.c_int32), ("extent_offset", C.c_uint64), ("last_use_clock", C.c_uint64)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class TorporError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+_P = C.c_void_p
+_SIGS = {
+    "tp_create": [C.POINTER(tp_config), C.POINTER(_P)],
+    "tp_destroy": [_P],
+    "tp_register_model": [_P, C.POINTER(tp_model_desc), _P, C.c_uint64, C.POINTER(C.c_int32)],
+    "tp_unregister_model": [_P, C.c_int32],
+    "tp_infer": [_P, C.c_int32, _P, C.c_int32, _P, _P],
+    "tp_swap_in": [_P, C.c_int32, _P],
+    "tp_evict": [_P, C.c_int32],
+    "tp_is_resident": [_P, C.c_int32, C.POINTER(C.c_int32)],
+    "tp_arena_stats": [_P, C.POINTER(tp_arena_stats_t)],
+    "tp_model_info": [_P, C.c_int32, C.POINTER(tp_model_info_t)],
+    "tp_model_chunks": [_P, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
+                        C.c_uint32, C.POINTER(C.c_uint32)],
+    "tp_workspace_bytes": [C.POINTER(tp_model_desc), C.c_int32, C.POINTER(C.c_uint64)],
+    "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
+    "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+                 C.POINTER(C.c_uint32), C.c_uint32, C.POINTER(C.c_uint32)],
+    "tph_arena_create": [C.c_uint64, C.c_uint64, C.POINTER(_P)],
+    "tph_arena_destroy": [_P],
+    "tph_arena_register": [_P, C.c_int32, C.c_uint64],
+    "tph_arena_unregister": [_P, C.c_int32],
+    "tph_arena_request": [_P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_uint64), C.POINTER(C.c_int32),
+                          C.c_uint32, C.POINTER(C.c_uint32)],
+    "tph_arena_evict": [_P, C.c_int32],
+    "tph_arena_stats": [_P, C.POINTER(tp_arena_stats_t)],
+}
+HOST_ONLY = [n for n in _SIGS if n.startswith("tph_")]
+
+_lib = None
+_host = None
+
+
+def _bind(lib, names):
+    for n in names:
+        f = getattr(lib, n)
+        f.argtypes = _SIGS[n]
+        f.restype = C.c_int32
+    lib.tp_last_error.argtypes = []
+    lib.tp_last_error.restype = C.c_char_p
+    return lib
+
+
+def lib():
+    """The HIP library. torch is imported first so both share torch's HIP runtime."""
+    global _lib
+    if _lib is None:
+        import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run python -m paper_2306_03622_amd.build")
+        _lib = _bind(C.CDLL(LIB_PATH), list(_SIGS))
+    return _lib
+
+
+def host_lib():
+    """The host-only planning library (same tph_* calls, built without HIP)."""
+    global _host
+    if _host is None:
+        if not os.path.exists(HOST_LIB_PATH):
+            raise ImportError(f"{HOST_LIB_PATH} is not built; run python -m paper_2306_03622_amd.build")
+        _host = _bind(C.CDLL(HOST_LIB_PATH), HOST_ONLY)
+    return _host
+
+
+def _check(L, status):
+    if status != TP_OK:
+        raise TorporError(status, L.tp_last_error().decode())
+
+
+def _ptr(x):
+    """Device or host address of a torch tensor, an int or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if hasattr(x, "cuda_stream"):
+        return x.cuda_stream
+    raise TypeError(type(x))
+
+
+# ------------------------------------------------------------------ descriptors
+
+class ModelDesc:
+    """Owns a tp_model_desc and its tensor table.
+
+    tensors: iterable of (layer, role name, offset, nbytes, shape).
+    """
+
+    def __init__(self, arch: str, dtype: str, dims, tensors):
+        self.tensors = list(tensors)
+        self._arr = (tp_tensor_desc * len(self.tensors))()
+        for i, (layer, role, off, nb, shape) in enumerate(self.tensors):
+            t = self._arr[i]
+            t.layer, t.role, t.offset, t.bytes = layer, ROLES[role], off, nb
+            for k, s in enumerate(tuple(shape)[:4]):
+                t.shape[k] = s
+        self.desc = tp_model_desc()
+        self.desc.arch = ARCHS[arch]
+        self.desc.dtype = DTYPES[dtype]
+        for k, v in enumerate(list(dims)[:8]):
+            self.desc.dims[k] = int(v)
+        self.desc.n_tensors = len(self.tensors)
+        self.desc.tensors = self._arr
+
+    @classmethod
+    def of(cls, model):
+        """From any object with arch, dtype, dims and tensors(layer, role, offset, nbytes, shape)."""
+        d = model.dims
+        if model.arch == "mlp":
+            dims = [d["layers"], d["width"], TP_ACT[d["act"]]]
+        elif model.arch == "resnet50":
+            dims = [d["classes"], d["image"]]
+        else:
+            dims = [d["layers"], d["d"], d["heads"], d["ffn"], d["seq"], d["vocab"], d["maxpos"]]
+        return cls(model.arch, model.dtype, dims,
+                   [(t.layer, t.role, t.offset, t.nbytes, t.shape) for t in model.tensors])
+
+
+# ------------------------------------------------------------------ C calls
+
+def tp_create(arena_dev, arena_bytes, work_dev, work_bytes, copy_stream=None, chunk_min_bytes=2 << 20,
+              copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0):
+    L = lib()
+    cfg = tp_config(_ptr(arena_dev), arena_bytes, _ptr(work_dev), work_bytes, _ptr(copy_stream), chunk_min_bytes,
+                    copy_method, gather_wgs, flags, throttle_us)
+    ctx = _P()
+    _check(L, L.tp_create(C.byref(cfg), C.byref(ctx)))
+    return ctx
+
+
+def tp_destroy(ctx):
+    _check(lib(), lib().tp_destroy(ctx))
+
+
+def tp_register_model(ctx, desc: ModelDesc, host_weights: np.ndarray) -> int:
+    buf = np.ascontiguousarray(host_weights).view(np.uint8)
+    mid = C.c_int32()
+    _check(lib(), lib().tp_register_model(ctx, C.byref(desc.desc), buf.ctypes.data, buf.nbytes, C.byref(mid)))
+    return mid.value
+
+
+def tp_unregister_model(ctx, model_id):
+    _check(lib(), lib().tp_unregister_model(ctx, model_id))
+
+
+def tp_infer(ctx, model_id, input_dev, batch, output_dev, stream=None):
+    _check(lib(), lib().tp_infer(ctx, model_id, _ptr(input_dev), batch, _ptr(output_dev), _ptr(stream)))
+
+
+def tp_swap_in(ctx, model_id, stream=None):
+    _check(lib(), lib().tp_swap_in(ctx, model_id, _ptr(stream)))
+
+
+def tp_evict(ctx, model_id):
+    _check(lib(), lib().tp_evict(ctx, model_id))
+
+
+def tp_is_resident(ctx, model_id) -> bool:
+    r = C.c_int32()
+    _check(lib(), lib().tp_is_resident(ctx, model_id, C.byref(r)))
+    return bool(r.value)
+
+
+def tp_arena_stats(ctx) -> dict:
+    s = tp_arena_stats_t()
+    _check(lib(), lib().tp_arena_stats(ctx, C.byref(s)))
+    return s.as_dict()
+
+
+def tp_model_info(ctx, model_id) -> dict:
+    s = tp_model_info_t()
+    _check(lib(), lib().tp_model_info(ctx, model_id, C.byref(s)))
+    return s.as_dict()
+
+
+def tp_model_chunks(ctx, model_id):
+    L = lib()
+    n = C.c_uint32()
+    _check(L, L.tp_model_chunks(ctx, model_id, None, None, None, 0, C.byref(n)))
+    b, e, f = (C.c_uint64 * n.value)(), (C.c_uint64 * n.value)(), (C.c_uint32 * n.value)()
+    _check(L, L.tp_model_chunks(ctx, model_id, b, e, f, n.value, C.byref(n)))
+    return [{"begin": b[i], "end": e[i], "first_layer": f[i]} for i in range(n.value)]
+
+
+def tp_workspace_bytes(desc: ModelDesc, batch: int) -> int:
+    out = C.c_uint64()
+    _check(lib(), lib().tp_workspace_bytes(C.byref(desc.desc), batch, C.byref(out)))
+    return out.value
+
+
+# host-only planning calls; `L` picks the library (the HIP one by default)
+
+def tph_validate(desc: ModelDesc, host_bytes: int, L=None):
+    L = L or lib()
+    _check(L, L.tph_validate(C.byref(desc.desc), host_bytes))
+
+
+def tph_plan(desc: ModelDesc, host_bytes: int, chunk_min_bytes: int, L=None):
+    L = L or lib()
+    n = C.c_uint32()
+    _check(L, L.tph_plan(C.byref(desc.desc), host_bytes, chunk_min_bytes, None, None, None, 0, C.byref(n)))
+    b, e, f = (C.c_uint64 * n.value)(), (C.c_uint64 * n.value)(), (C.c_uint32 * n.value)()
+    _check(L, L.tph_plan(C.byref(desc.desc), host_bytes, chunk_min_bytes, b, e, f, n.value, C.byref(n)))
+    return [{"begin": b[i], "end": e[i], "first_layer": f[i]} for i in range(n.value)]
+
+
+class HostArena:
+    """tph_arena_*: the arena bookkeeping without a device."""
+
+    def __init__(self, capacity: int, align: int = 256, L=None):
+        self.L = L or lib()
+        self.h = _P()
+        _check(self.L, self.L.tph_arena_create(capacity, align, C.byref(self.h)))
+
+    def __del__(self):
+        if getattr(self, "h", None):
+            self.L.tph_arena_destroy(self.h)
+            self.h = None
+
+    def register(self, mid, nbytes):
+        _check(self.L, self.L.tph_arena_register(self.h, mid, nbytes))
+
+    def unregister(self, mid):
+        _check(self.L, self.L.tph_arena_unregister(self.h, mid))
+
+    def request(self, mid):
+        hit, off, n = C.c_int32(), C.c_uint64(), C.c_uint32()
+        vict = (C.c_int32 * 1024)()
+        _check(self.L, self.L.tph_arena_request(self.h, mid, C.byref(hit), C.byref(off), vict, 1024, C.byref(n)))
+        return {"hit": bool(hit.value), "offset": off.value, "evicted": [vict[i] for i in range(n.value)]}
+
+    def evict(self, mid):
+        _check(self.L, self.L.tph_arena_evict(self.h, mid))
+
+    def stats(self):
+        s = tp_arena_stats_t()
+        _check(self.L, self.L.tph_arena_stats(self.h, C.byref(s)))
+        return s.as_dict()
+
+
+# ------------------------------------------------------------------ convenience
+
+class Runtime:
+    """A context whose arena and workspace are torch allocations made once."""
+
+    def __init__(self, arena_bytes: int, work_bytes: int, device: int = 0, chunk_min_bytes: int = 2 << 20,
+                 copy_method: int = TP_COPY_MEMCPY, gather_wgs: int = 0, flags: int = 0, throttle_us: int = 0,
+                 copy_stream=None):
+        import torch
+        if not torch.cuda.is_available():
+            raise RuntimeError("libtorpor needs a HIP device")
+        self.torch = torch
+        self.device = torch.device("cuda", device)
+        torch.cuda.set_device(self.device)
+        self.arena = torch.empty(arena_bytes, dtype=torch.uint8, device=self.device)
+        self.work = torch.empty(max(work_bytes, 256), dtype=torch.uint8, device=self.device)
+        self.copy_stream = copy_stream
+        self.ctx = tp_create(self.arena, arena_bytes, self.work, self.work.numel(), copy_stream, chunk_min_bytes,
+                             copy_method, gather_wgs, flags, throttle_us)
+        self.descs = {}
+
+    def close(self):
+        if self.ctx is not None:
+            tp_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def register(self, desc: ModelDesc, host_weights: np.ndarray) -> int:
+        mid = tp_register_model(self.ctx, desc, host_weights)
+        self.descs[mid] = desc
+        return mid
+
+    def unregister(self, mid):
+        tp_unregister_model(self.ctx, mid)
+        self.descs.pop(mid, None)
+
+    def infer(self, mid, x, out, stream=None):
+        """x, out: torch device tensors; stream: a torch stream (default: current)."""
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        tp_infer(self.ctx, mid, x, int(x.shape[0]), out, s)
+
+    def swap_in(self, mid, stream=None):
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        tp_swap_in(self.ctx, mid, s)
+
+    def evict(self, mid):
+        tp_evict(self.ctx, mid)
+
+    def resident(self, mid) -> bool:
+        return tp_is_resident(self.ctx, mid)
+
+    def stats(self) -> dict:
+        return tp_arena_stats(self.ctx)
+
+    def info(self, mid) -> dict:
+        return tp_model_info(self.ctx, mid)
+
+    def chunks(self, mid):
+        return tp_model_chunks(self.ctx, mid)
+
+    def extent(self, mid):
+        """The model's arena bytes (a view of the arena), when resident."""
+        i = self.info(mid)
+        return self.arena[i["extent_offset"]:i["extent_offset"] + i["host_bytes"]]

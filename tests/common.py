@@ -1,0 +1,64 @@
+"""Helpers shared by the GPU tests: run a synthetic model through the C ABI and compare."""
+import sys
+
+import numpy as np
+
+import synth
+from oracle import forward as oracle_forward
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def torch_dev():
+    import torch
+    return torch, torch.device("cuda", 0)
+
+
+def to_device(x: np.ndarray):
+    torch, dev = torch_dev()
+    if x.dtype == np.uint16:
+        x = x.view(np.int16)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+
+def out_shape(model, batch):
+    if model.arch == "mlp":
+        return (batch, model.dims["width"])
+    if model.arch == "resnet50":
+        return (batch, model.dims["classes"])
+    return (batch, model.dims["seq"], model.dims["d"])
+
+
+def make_runtime(models, batch_max=1, arena_bytes=None, **kw):
+    import paper_2306_03622_amd as tp
+    descs = [tp.ModelDesc.of(m) for m in models]
+    ws = max(tp.tp_workspace_bytes(d, batch_max) for d in descs)
+    if arena_bytes is None:
+        arena_bytes = sum(m.total_bytes for m in models) + (1 << 20)
+    rt = tp.Runtime(arena_bytes, ws, **kw)
+    ids = [rt.register(d, m.blob()) for d, m in zip(descs, models)]
+    return rt, ids
+
+
+def infer(rt, mid, model, x_np, stream=None):
+    """One request; returns the fp32 output on the host."""
+    torch, dev = torch_dev()
+    x = to_device(x_np)
+    out = torch.full(out_shape(model, x_np.shape[0]), float("nan"), dtype=torch.float32, device=dev)
+    s = stream or torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    rt.infer(mid, x, out, stream=s)
+    s.synchronize()
+    return out.cpu().numpy()
+
+
+def check_parity(got, model, x_np, tol):
+    ref = oracle_forward.forward(model, x_np)
+    err = oracle_forward.normwise_error(got, ref)
+    log(f"  normwise error per sample: max {err.max():.3e} (tol {tol})")
+    assert np.all(np.isfinite(got)), "non-finite output"
+    assert err.max() <= tol, (err.max(), tol)
+    return err

@@ -1,0 +1,61 @@
+"""MLP family through the C ABI on the GPU vs the oracle, plus the swap invariants.
+
+fp32 (the 4 x 256 workload): normwise error <= 1e-4. bf16: <= 2e-2.
+"""
+import numpy as np
+import pytest
+
+import synth
+from tests.common import check_parity, infer, log, make_runtime
+
+pytestmark = pytest.mark.gpu
+
+
+def test_cfg1_fp32_cold_then_warm():
+    m = synth.config_model(1)
+    x = synth.config_input(m, 1, 10101)
+    rt, (mid,) = make_runtime([m])
+    log("cfg1 cold")
+    cold = infer(rt, mid, m, x)
+    assert rt.resident(mid)
+    warm = infer(rt, mid, m, x)
+    check_parity(cold, m, x, 1e-4)
+    assert np.array_equal(cold, warm)
+    # swapped bytes are the host bytes
+    assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob())
+    st = rt.stats()
+    assert (st["hits"], st["misses"], st["bytes_swapped"]) == (1, 1, m.total_bytes)
+    rt.close()
+
+
+@pytest.mark.parametrize("batch", [1, 5, 16, 17, 32, 33, 100])
+def test_mlp_bf16_ragged(batch):
+    m = synth.mlp(3, 200, "bf16", "gelu", seed=7)
+    x = synth.mlp_input(batch, 200, "bf16", 100 + batch)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"mlp bf16 width 200 batch {batch}")
+    got = infer(rt, mid, m, x)
+    check_parity(got, m, x, 2e-2)
+    rt.close()
+
+
+@pytest.mark.parametrize("act", ["relu", "none"])
+def test_mlp_f32_acts(act):
+    m = synth.mlp(2, 264, "f32", act, seed=3, bias_std=0.1)
+    x = synth.mlp_input(3, 264, "f32", 4)
+    rt, (mid,) = make_runtime([m], batch_max=3)
+    check_parity(infer(rt, mid, m, x), m, x, 1e-4)
+    rt.close()
+
+
+@pytest.mark.parametrize("batch", [1, 8, 32])
+def test_cfg2_full(batch):
+    m = synth.config_model(2)
+    x = synth.config_input(m, batch, 10200 + batch)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"cfg2 batch {batch}: cold")
+    cold = infer(rt, mid, m, x)
+    warm = infer(rt, mid, m, x)
+    assert np.array_equal(cold, warm)
+    check_parity(cold, m, x, 2e-2)
+    rt.close()
