@@ -1,0 +1,152 @@
+"""Host-side checks of the C ABI (no GPU): exported symbols, descriptor validation, the
+chunk plan and the arena bookkeeping against the oracle's reference rules."""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import paper_2306_03622_amd as tp
+import synth
+from oracle import chunks as ref_chunks
+from oracle.arena_sim import ArenaSim, NoSpace
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    names = set()
+    for h in ("torpor.h", "torpor_plan.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        names |= set(re.findall(r"^TP_API\s+[\w\s\*]+?\b(tph?_\w+)\s*\(", src, re.M))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_symbols()
+    assert len(names) == 22, sorted(names)
+    L = tp.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", tp.torpor.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (tph?_\w+)", out))
+    assert exported == names, exported ^ names
+    host = subprocess.run(["nm", "-D", "--defined-only", tp.torpor.HOST_LIB_PATH], capture_output=True, text=True).stdout
+    assert set(re.findall(r" T (tph?_\w+)", host)) == {n for n in names if n.startswith("tph_")} | {"tp_last_error"}
+
+
+def _desc(model, mutate=None, dims=None, dtype=None):
+    tensors = [[t.layer, t.role, t.offset, t.nbytes, list(t.shape)] for t in model.tensors]
+    if mutate:
+        mutate(tensors)
+    d = tp.ModelDesc.of(model)
+    return tp.ModelDesc(model.arch, dtype or model.dtype, dims or list(d.desc.dims), [tuple(t) for t in tensors])
+
+
+@pytest.mark.parametrize("case", ["shape", "missing", "dup", "misaligned", "overlap", "order", "bounds", "bytes",
+                                  "dims", "dtype", "role"])
+def test_validation_rejects_malformed_layouts(case):
+    m = synth.bert(seed=1, layers=2, d=128, heads=2, ffn=256, seq=64, vocab=100, maxpos=64)
+    kw = {}
+    mut = None
+    if case == "shape":
+        mut = lambda t: t[3].__setitem__(4, [2, 128 * 3])
+    elif case == "missing":
+        mut = lambda t: t.pop(7)
+    elif case == "dup":
+        mut = lambda t: t[6].__setitem__(1, t[5][1])
+    elif case == "misaligned":
+        mut = lambda t: t[3].__setitem__(2, t[3][2] + 2)
+    elif case == "overlap":
+        mut = lambda t: t[3].__setitem__(2, t[2][2])
+    elif case == "order":
+        mut = lambda t: t.insert(0, t.pop(10))
+    elif case == "bounds":
+        mut = lambda t: t[-1].__setitem__(2, m.total_bytes + 256)
+    elif case == "bytes":
+        mut = lambda t: t[5].__setitem__(3, t[5][3] + 2)
+    elif case == "dims":
+        kw["dims"] = [2, 128, 3, 256, 64, 100, 64]
+    elif case == "dtype":
+        kw["dtype"] = "f32"
+    elif case == "role":
+        mut = lambda t: t[0].__setitem__(1, "w")
+    d = _desc(m, mut, **kw)
+    with pytest.raises(tp.TorporError) as e:
+        tp.tph_validate(d, m.total_bytes)
+    assert e.value.status == tp.TP_E_INVAL
+    assert tp.lib().tp_last_error().decode()
+    tp.tph_validate(tp.ModelDesc.of(m), m.total_bytes)        # the unmodified layout passes
+
+
+def test_validation_accepts_all_workloads():
+    for cfg in (1, 2, 3, 4):
+        m = synth.config_model(cfg)
+        tp.tph_validate(tp.ModelDesc.of(m), m.total_bytes)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+@pytest.mark.parametrize("g", [0, 64 << 10, 2 << 20, 16 << 20, 1 << 40])
+def test_chunk_plan_matches_reference(cfg, g):
+    m = synth.config_model(cfg)
+    want = ref_chunks.plan([(t.layer, t.offset, t.nbytes) for t in m.tensors], m.total_bytes, g)
+    for L in (tp.lib(), tp.host_lib()):
+        got = tp.tph_plan(tp.ModelDesc.of(m), m.total_bytes, g, L=L)
+        assert [(c["begin"], c["end"], c["first_layer"]) for c in got] == \
+            [(c["begin"], c["end"], c["first_layer"]) for c in want]
+
+
+def test_workspace_grows_with_batch():
+    for cfg in (1, 2, 3, 4):
+        d = tp.ModelDesc.of(synth.config_model(cfg))
+        w = [tp.tp_workspace_bytes(d, b) for b in (1, 2, 8)]
+        assert 0 < w[0] <= w[1] <= w[2]
+
+
+def _replay(trace, sizes, cap, L):
+    sim = ArenaSim(cap, align=256)
+    ha = tp.HostArena(cap, 256, L=L)
+    for i, nb in enumerate(sizes):
+        sim.register(i, nb)
+        ha.register(i, nb)
+    for op, k in trace:
+        if op == "evict":
+            sim.evict(k)
+            ha.evict(k)
+            continue
+        try:
+            want = sim.request(k)
+        except NoSpace:
+            with pytest.raises(tp.TorporError) as e:
+                ha.request(k)
+            assert e.value.status == tp.TP_E_NOSPC
+            continue
+        assert ha.request(k) == want
+    assert ha.stats() == {**sim.stats(), "registered": len(sizes)}
+
+
+@settings(max_examples=60, deadline=None)
+@given(sizes=st.lists(st.integers(1, 40) .map(lambda x: x * 1000), min_size=2, max_size=10),
+       ops=st.lists(st.tuples(st.sampled_from(["req", "req", "req", "evict"]), st.integers(0, 9)), max_size=80),
+       frac=st.floats(0.2, 1.2))
+def test_arena_matches_simulator_random_traces(sizes, ops, frac):
+    cap = max(int(sum(sizes) * frac), 256) // 256 * 256
+    trace = [(op, k % len(sizes)) for op, k in ops]
+    _replay(trace, sizes, cap, tp.lib())
+    _replay(trace, sizes, cap, tp.host_lib())
+
+
+def test_arena_unregister_and_errors():
+    ha = tp.HostArena(10_000, 256)
+    ha.register(1, 5000)
+    with pytest.raises(tp.TorporError) as e:
+        ha.register(1, 10)
+    assert e.value.status == tp.TP_E_STATE
+    with pytest.raises(tp.TorporError) as e:
+        ha.request(7)
+    assert e.value.status == tp.TP_E_NOENT
+    ha.request(1)
+    ha.unregister(1)
+    assert ha.stats()["used"] == 0 and ha.stats()["registered"] == 0

@@ -1,0 +1,63 @@
+"""BERT and ResNet families through the C ABI on the GPU vs the oracle (bf16: 2e-2)."""
+import numpy as np
+import pytest
+
+import synth
+from tests.common import check_parity, infer, log, make_runtime
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("seq,batch", [(32, 1), (64, 3), (96, 2), (256, 1)])
+def test_bert_small(seq, batch):
+    m = synth.bert(seed=41, layers=2, d=128, heads=2, ffn=264, seq=seq, vocab=1000, maxpos=256)
+    ids = synth.bert_input(batch, 42 + seq, seq=seq, vocab=1000)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"bert small seq {seq} batch {batch}")
+    check_parity(infer(rt, mid, m, ids), m, ids, 2e-2)
+    rt.close()
+
+
+def test_bert_out_of_range_ids_are_clamped():
+    m = synth.bert(seed=43, layers=1, d=64, heads=1, ffn=64, seq=32, vocab=50, maxpos=32)
+    ids = synth.bert_input(1, 44, seq=32, vocab=50)
+    bad = ids.copy()
+    bad[0, :4] = [-5, 50, 1 << 30, -(1 << 30)]
+    clamped = np.clip(bad, 0, 49).astype(np.int32)
+    rt, (mid,) = make_runtime([m], batch_max=1)
+    assert np.array_equal(infer(rt, mid, m, bad), infer(rt, mid, m, clamped))
+    rt.close()
+
+
+@pytest.mark.parametrize("batch", [1, 8])
+def test_cfg4_full(batch):
+    m = synth.config_model(4)
+    ids = synth.config_input(m, batch, 10400 + batch)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"cfg4 batch {batch}")
+    cold = infer(rt, mid, m, ids)
+    assert np.array_equal(cold, infer(rt, mid, m, ids))
+    check_parity(cold, m, ids, 2e-2)
+    rt.close()
+
+
+@pytest.mark.parametrize("image,batch", [(32, 1), (64, 3)])
+def test_resnet_small_images(image, batch):
+    m = synth.resnet50(seed=51, classes=10, image=image)
+    x = synth.resnet_input(batch, 52, image=image)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"resnet image {image} batch {batch}")
+    check_parity(infer(rt, mid, m, x), m, x, 2e-2)
+    rt.close()
+
+
+@pytest.mark.parametrize("batch", [1, 8])
+def test_cfg3_full(batch):
+    m = synth.config_model(3)
+    x = synth.config_input(m, batch, 10300 + batch)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"cfg3 batch {batch}")
+    cold = infer(rt, mid, m, x)
+    assert np.array_equal(cold, infer(rt, mid, m, x))
+    check_parity(cold, m, x, 2e-2)
+    rt.close()

@@ -1,0 +1,120 @@
+"""Swap-in invariants on the GPU (exact): swapped bytes equal the host copy for both copy
+methods; pipelined output equals preloaded output bit for bit; relocation after a
+different eviction history does not change the output; throttled copies with poisoned
+evicted extents give the same bits; arena decisions follow the reference simulator."""
+import numpy as np
+import pytest
+
+import paper_2306_03622_amd as tp
+import synth
+from oracle.arena_sim import ArenaSim
+from tests.common import infer, log, make_runtime, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _models():
+    return [synth.mlp(6, 512, "bf16", "gelu", seed=61),
+            synth.bert(seed=62, layers=2, d=128, heads=2, ffn=256, seq=64, vocab=500, maxpos=64),
+            synth.resnet50(seed=63, classes=10, image=32)]
+
+
+def _inputs(ms, batch=2):
+    return [synth.config_input(m, batch, 70 + i) for i, m in enumerate(ms)]
+
+
+@pytest.mark.parametrize("method", [tp.TP_COPY_MEMCPY, tp.TP_COPY_GATHER])
+@pytest.mark.parametrize("chunk", [0, 64 << 10, 2 << 20, 1 << 40])
+def test_swapped_bytes_identical(method, chunk):
+    ms = _models()
+    rt, ids = make_runtime(ms, batch_max=2, copy_method=method, chunk_min_bytes=chunk)
+    torch, dev = torch_dev()
+    s = torch.cuda.Stream(device=dev)
+    for mid, m in zip(ids, ms):
+        rt.swap_in(mid, stream=s)
+        s.synchronize()
+        assert rt.resident(mid)
+        assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob()), (method, chunk, m.arch)
+    rt.close()
+
+
+@pytest.mark.parametrize("method", [tp.TP_COPY_MEMCPY, tp.TP_COPY_GATHER])
+def test_pipelined_equals_preloaded(method):
+    ms, xs = _models(), None
+    xs = _inputs(ms)
+    rt, ids = make_runtime(ms, batch_max=2, copy_method=method, chunk_min_bytes=0)
+    torch, dev = torch_dev()
+    s = torch.cuda.Stream(device=dev)
+    for mid, m, x in zip(ids, ms, xs):
+        log(f"pipelined vs preloaded: {m.arch}")
+        pipelined = infer(rt, mid, m, x, stream=s)          # cold: per-layer waits
+        rt.evict(mid)
+        rt.swap_in(mid, stream=s)                           # preloaded: swap, sync, run
+        s.synchronize()
+        preloaded = infer(rt, mid, m, x, stream=s)
+        assert np.array_equal(pipelined, preloaded)
+    rt.close()
+
+
+def test_eviction_order_and_placement_do_not_change_outputs():
+    ms = _models()
+    xs = _inputs(ms)
+    small_arena = max(m.total_bytes for m in ms) + sum(sorted(m.total_bytes for m in ms)[:1]) + 4096
+    ref_rt, ref_ids = make_runtime(ms, batch_max=2)
+    ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
+    ref_rt.close()
+    rt, ids = make_runtime(ms, batch_max=2, arena_bytes=small_arena, flags=tp.TP_FLAG_POISON)
+    offsets = {i: set() for i in range(3)}
+    order = [0, 1, 2, 1, 0, 2, 2, 0, 1, 0]
+    for k in order:
+        got = infer(rt, ids[k], ms[k], xs[k])
+        offsets[k].add(rt.info(ids[k])["extent_offset"])
+        assert np.array_equal(got, ref[k]), (k, order)
+    log(f"offsets seen: {offsets}")
+    assert rt.stats()["evictions"] > 0
+    assert any(len(v) > 1 for v in offsets.values())
+    rt.close()
+
+
+def test_throttled_poisoned_swaps_are_bit_identical():
+    ms = _models()
+    xs = _inputs(ms)
+    ref_rt, ref_ids = make_runtime(ms, batch_max=2)
+    ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
+    ref_rt.close()
+    # each chunk waits ~200 us on the copy stream; a layer that did not wait for its chunk
+    # would read 0xFF bytes (NaN) left by the poisoned eviction of the previous tenant
+    arena = max(m.total_bytes for m in ms) + 4096
+    rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, chunk_min_bytes=0,
+                           flags=tp.TP_FLAG_POISON | tp.TP_FLAG_THROTTLE, throttle_us=200)
+    for rep in range(2):
+        for k in range(3):
+            got = infer(rt, ids[k], ms[k], xs[k])
+            assert np.array_equal(got, ref[k]), (rep, k)
+    assert rt.stats()["misses"] == 6
+    rt.close()
+
+
+def test_arena_decisions_match_simulator():
+    rng = np.random.default_rng(5)
+    ms = [synth.mlp(int(rng.integers(1, 5)), int(rng.choice([64, 128, 256])), "bf16", "relu", seed=80 + i)
+          for i in range(8)]
+    cap = max(int(sum(m.total_bytes for m in ms) * 0.45), max(m.total_bytes for m in ms)) // 256 * 256
+    rt, ids = make_runtime(ms, batch_max=1, arena_bytes=cap)
+    sim = ArenaSim(cap, align=256)
+    for i, m in zip(ids, ms):
+        sim.register(i, m.total_bytes)
+    xs = [synth.mlp_input(1, m.dims["width"], "bf16", 90 + i) for i, m in enumerate(ms)]
+    for step in range(60):
+        k = int(rng.integers(0, len(ms)))
+        if rng.random() < 0.1:
+            rt.evict(ids[k]); sim.evict(ids[k])
+            continue
+        want = sim.request(ids[k])
+        infer(rt, ids[k], ms[k], xs[k])
+        assert rt.info(ids[k])["extent_offset"] == want["offset"]
+        assert [rt.resident(i) for i in ids] == [i in sim.where for i in ids], step
+    got = rt.stats()
+    for key, v in sim.stats().items():
+        assert got[key] == v, (key, got[key], v)
+    rt.close()
