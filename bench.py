@@ -1,0 +1,358 @@
+"""Cold-start (swap-in + execute) latency of the 24-layer, 4096-wide bf16 MLP on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--batch B] [--method memcpy|gather|auto] [--full]
+
+A step is one cold request: the model is invalidated (metadata only), then tp_infer
+streams its 805,502,976 weight bytes from the pinned host pool into the HBM arena in
+per-layer chunks while the layer kernels run as each chunk lands, and the host waits
+for the fp32 output. The request input (activations) is already in device memory when
+the clock starts; the weights start in pinned host memory by definition of "cold".
+
+Prints one JSON line: the p50 cold latency, its lower bound
+max(weight bytes / measured host-link peak, warm compute time), the effective swap
+rate, warm latency, the HBM roofline of the dominant compute kernel (the skinny bf16
+GEMM, timed with HIP events on its stream), and the CPU oracle timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+PCIE5_X16_GBS = 63.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def p50(xs):
+    return statistics.median(xs)
+
+
+def pct(xs, q):
+    return float(np.percentile(np.asarray(xs), q))
+
+
+def to_dev(torch, x, dev):
+    if x.dtype == np.uint16:
+        x = x.view(np.int16)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+
+def out_shape(m, b):
+    if m.arch == "mlp":
+        return (b, m.dims["width"])
+    if m.arch == "resnet50":
+        return (b, m.dims["classes"])
+    return (b, m.dims["seq"], m.dims["d"])
+
+
+def link_peak(torch, dev, reps=10, nbytes=1 << 30):
+    """Best-of-`reps` single pinned host->device copy of 1 GiB (GB/s)."""
+    h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    best = 0.0
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        with torch.cuda.stream(s):
+            d.copy_(h, non_blocking=True)
+        s.synchronize()
+        best = max(best, nbytes / (time.perf_counter() - t0) / 1e9)
+    del h, d
+    return best
+
+
+class Bench:
+    def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0):
+        import paper_2306_03622_amd as tp
+        self.tp, self.torch, self.dev, self.m = tp, torch, dev, model
+        self.desc = tp.ModelDesc.of(model)
+        ws = tp.tp_workspace_bytes(self.desc, max(batches))
+        cm = tp.TP_COPY_GATHER if method == "gather" else tp.TP_COPY_MEMCPY
+        self.rt = tp.Runtime(model.total_bytes + (1 << 20), ws, chunk_min_bytes=chunk, copy_method=cm,
+                             copy_streams=copy_streams)
+        self.mid = self.rt.register(self.desc, model.blob())
+        self.stream = torch.cuda.Stream(device=dev)
+
+    def request(self, x, out, cold):
+        torch = self.torch
+        if cold:
+            self.rt.evict(self.mid)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        self.rt.infer(self.mid, x, out, stream=self.stream)
+        self.stream.synchronize()
+        return (time.perf_counter() - t0) * 1e3
+
+    def swap_only(self):
+        self.rt.evict(self.mid)
+        self.torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        self.rt.swap_in(self.mid, stream=self.stream)
+        self.stream.synchronize()
+        return (time.perf_counter() - t0) * 1e3
+
+    def io(self, batch, seed):
+        import synth
+        x = to_dev(self.torch, synth.config_input(self.m, batch, seed), self.dev)
+        out = self.torch.empty(out_shape(self.m, batch), dtype=self.torch.float32, device=self.dev)
+        return x, out
+
+    def event_time_ms(self, x, out, reps):
+        """Average warm forward time measured by HIP events on the compute stream."""
+        torch = self.torch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        self.rt.infer(self.mid, x, out, stream=self.stream)
+        torch.cuda.synchronize()
+        e0.record(self.stream)
+        for _ in range(reps):
+            self.rt.infer(self.mid, x, out, stream=self.stream)
+        e1.record(self.stream)
+        self.stream.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    def close(self):
+        self.rt.close()
+
+
+def measure(b: Bench, batch, seed, steps, warmup, warm_reps):
+    x, out = b.io(batch, seed)
+    for _ in range(warmup):
+        b.request(x, out, cold=True)
+        b.request(x, out, cold=False)
+    torch = b.torch
+    torch.cuda.synchronize()
+    t_all = time.perf_counter()
+    cold = [b.request(x, out, cold=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t_all = time.perf_counter() - t_all
+    warm = [b.request(x, out, cold=False) for _ in range(warm_reps)]
+    swap = [b.swap_only() for _ in range(max(5, steps // 2))]
+    return {"cold": cold, "warm": warm, "swap": swap, "t_all": t_all, "x": x, "out": out}
+
+
+def elbow_sweep(torch, dev, method, copy_streams=0, sizes=(256 << 10, 512 << 10, 1 << 20, 2 << 20, 4 << 20, 8 << 20, 16 << 20,
+                                             32 << 20, 1 << 40), reps=8):
+    """Transfer throughput of a chunked, event-handed-off swap versus group size G.
+
+    Runs through the library: a 512-wide bf16 MLP of 256 layers (512 KiB per layer,
+    128 MiB) is swapped in with each G (whole layers per chunk), and a cold request
+    with per-layer waits is timed too. The elbow is the smallest G whose swap
+    throughput is within 5% of the largest measured.
+    """
+    import paper_2306_03622_amd as tp
+    import synth
+    m = synth.mlp(256, 512, "bf16", "relu", seed=99)
+    m.blob()
+    rows = []
+    x, out = None, None
+    for g in sizes:
+        b = Bench(torch, dev, m, [1], method, g, copy_streams)
+        if x is None:
+            x, out = b.io(1, 5)
+        b.swap_only()
+        sw = p50([b.swap_only() for _ in range(reps)])
+        b.request(x, out, cold=True)
+        cold = p50([b.request(x, out, cold=True) for _ in range(reps)])
+        n = len(b.rt.chunks(b.mid))
+        b.close()
+        rows.append({"chunk_min_bytes": g, "chunks": n, "swap_gbs": round(m.total_bytes / (sw / 1e3) / 1e9, 2),
+                     "cold_pipelined_ms": round(cold, 3)})
+        log(f"  G={g >> 10} KiB chunks={n}: swap {rows[-1]['swap_gbs']} GB/s, cold {cold:.3f} ms")
+    best = max(r["swap_gbs"] for r in rows)
+    elbow = next(r["chunk_min_bytes"] for r in rows if r["swap_gbs"] >= 0.95 * best)
+    return {"model": "256 x 512 bf16 MLP (512 KiB per layer)", "rows": rows, "elbow_bytes": elbow}
+
+
+def cpu_baseline(model, batch, seed, budget_s=12.0, max_runs=30):
+    """The oracle (fp32 variant) on this host's cores, a bounded number of runs."""
+    import synth
+    from oracle import forward as oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"), default=0)
+    except Exception:
+        threads = 0
+    x = synth.config_input(model, batch, seed)
+    oracle.forward(model, x, np.float32)          # first touch
+    times = []
+    t_start = time.perf_counter()
+    while len(times) < max_runs and (time.perf_counter() - t_start) < budget_s:
+        t0 = time.perf_counter()
+        oracle.forward(model, x, np.float32)
+        times.append((time.perf_counter() - t0) * 1e3)
+    return {"value": round(p50(times), 3), "unit": "ms", "cores": threads or os.cpu_count(), "kind": "oracle",
+            "sample": f"{len(times)} fp32 oracle forwards of the same workload at batch {batch} "
+                      f"(p50; {os.cpu_count()} host CPUs visible, BLAS threads {threads})"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--batch", type=int, default=8)
+    ap.add_argument("--method", choices=["memcpy", "gather", "auto"], default="memcpy")
+    ap.add_argument("--chunk", default="default",
+                    help="transfer group size G in bytes, 'default' (the library's) or 'elbow' (this run's sweep)")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the group-size sweep")
+    ap.add_argument("--copy-streams", type=int, default=0, help="copy streams of the library (0: its default)")
+    ap.add_argument("--pmc-workload", action="store_true",
+                    help="run only a fixed workload for hardware-counter passes: 20 warm forwards of the "
+                         "bench model, then one 256 MiB device-to-device copy (the byte-count calibration)")
+    ap.add_argument("--full", action="store_true", help="also time the other batches and workloads")
+    ap.add_argument("--no-cpu", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: swap-in and execution of a model is a per-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    if not torch.cuda.is_available():
+        print("bench.py needs an MI355X (no HIP device visible)", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    if a.pmc_workload:
+        model = synth.config_model(2)
+        b = Bench(torch, dev, model, [a.batch], "memcpy", 8 << 20, a.copy_streams)
+        x, out = b.io(a.batch, 10200 + a.batch)
+        for _ in range(20):
+            b.request(x, out, cold=False)
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        b.close()
+        print(json.dumps({"pmc_workload": "20 warm forwards of the 24 x 4096 bf16 MLP at batch "
+                          f"{a.batch}, then one 268435456-byte device copy"}), flush=True)
+        return
+
+    log("measuring host-link peak (1 GiB pinned H2D, best of 10)")
+    link = link_peak(torch, dev)
+    log(f"  link peak {link:.1f} GB/s")
+
+    import paper_2306_03622_amd as tp
+    sweep = None
+    if not a.no_sweep:
+        log("group-size sweep")
+        sweep = elbow_sweep(torch, dev, "gather" if a.method == "gather" else "memcpy", a.copy_streams)
+    if a.chunk == "elbow" and sweep:
+        a.chunk = sweep["elbow_bytes"]
+    elif a.chunk in ("default", "elbow"):
+        a.chunk = tp.DEFAULT_CHUNK
+    else:
+        a.chunk = int(a.chunk)
+
+    model = synth.config_model(2)
+    log("generating the 24 x 4096 bf16 MLP weights")
+    model.blob()
+    batches = [1, 8, 32] if a.full else [a.batch]
+    method = a.method
+    extra = {}
+    if method == "auto":
+        rates = {}
+        for meth in ("memcpy", "gather"):
+            b = Bench(torch, dev, model, batches, meth, a.chunk, a.copy_streams)
+            b.swap_only()
+            rates[meth] = model.total_bytes / (p50([b.swap_only() for _ in range(5)]) / 1e3) / 1e9
+            b.close()
+        method = max(rates, key=rates.get)
+        extra["swap_rate_by_method_gbs"] = {k: round(v, 2) for k, v in rates.items()}
+        log(f"  swap rates {rates} -> {method}")
+
+    b = Bench(torch, dev, model, batches, method, a.chunk, a.copy_streams)
+    results = {}
+    for bt in batches:
+        log(f"cold/warm requests, batch {bt}")
+        results[bt] = measure(b, bt, 10200 + bt, a.steps, a.warmup, max(4 * a.steps, 100))
+    r = results[a.batch] if a.batch in results else results[batches[0]]
+    B = a.batch if a.batch in results else batches[0]
+
+    W = model.total_bytes
+    warm_p50 = p50(r["warm"])
+    cold_p50 = p50(r["cold"])
+    bound = max(W / (link * 1e9) * 1e3, warm_p50)
+    swap_gbs = W / (p50(r["swap"]) / 1e3) / 1e9
+
+    # dominant compute kernel: the skinny bf16 GEMM (24 launches per forward, nothing else)
+    reps = 50
+    fwd_ms = b.event_time_ms(r["x"], r["out"], reps)
+    kern_us = fwd_ms / 24 * 1e3
+    K = N = 4096
+    alg_bytes = N * K * 2 + N * 2 + B * K * 2 + B * N * 2
+    achieved = alg_bytes / (kern_us * 1e-6) / 1e9
+    flops = 2 * B * N * K
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "k_gemv<1,16> (bf16 [B x 4096] x [4096 x 4096]^T + bias, GELU)",
+                "avg_launch_us": round(kern_us, 2), "algorithmic_bytes_per_launch": alg_bytes,
+                "mfma_util": round(flops / (kern_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)}
+
+    for bt, rr in results.items():
+        wp = p50(rr["warm"])
+        extra[f"mlp24x4096_b{bt}"] = {
+            "cold_p50_ms": round(p50(rr["cold"]), 3), "cold_p10_ms": round(pct(rr["cold"], 10), 3),
+            "cold_p90_ms": round(pct(rr["cold"], 90), 3), "warm_p50_ms": round(wp, 4),
+            "bound_ms": round(max(W / (link * 1e9) * 1e3, wp), 3),
+            "cold_over_bound": round(p50(rr["cold"]) / max(W / (link * 1e9) * 1e3, wp), 4),
+            "swap_only_p50_ms": round(p50(rr["swap"]), 3)}
+    b.close()
+
+    if a.full:
+        for cfg, bts in ((1, [1]), (3, [1, 8]), (4, [1, 8])):
+            m = synth.config_model(cfg)
+            log(f"workload {cfg}")
+            bb = Bench(torch, dev, m, bts, method, a.chunk, a.copy_streams)
+            for bt in bts:
+                rr = measure(bb, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt), a.steps, a.warmup,
+                             max(4 * a.steps, 100))
+                wp = p50(rr["warm"])
+                bnd = max(m.total_bytes / (link * 1e9) * 1e3, wp)
+                extra[f"cfg{cfg}_b{bt}"] = {
+                    "weight_bytes": m.total_bytes, "cold_p50_ms": round(p50(rr["cold"]), 4),
+                    "warm_p50_ms": round(wp, 4), "bound_ms": round(bnd, 4),
+                    "cold_over_bound": round(p50(rr["cold"]) / bnd, 4),
+                    "swap_only_gbs": round(m.total_bytes / (p50(rr["swap"]) / 1e3) / 1e9, 2)}
+            bb.close()
+            m.drop_blob()
+
+    cpu = None
+    if not a.no_cpu:
+        log("CPU oracle baseline")
+        cpu = cpu_baseline(model, B, 10200 + B)
+
+    line = {
+        "metric": "cold-start p50 latency (swap+exec)",
+        "value": round(cold_p50, 3), "unit": "ms", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(r["t_all"] / a.steps * 1e3, 3), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"24-layer MLP, hidden 4096, bf16 weights (805,502,976 B) swapped cold from pinned "
+                               f"host memory, batch {B}", "batch": B, "copy_method": method,
+                   "chunk_min_bytes": a.chunk, "copy_streams": a.copy_streams or 1},
+        "bound_ms": round(bound, 3), "cold_over_bound": round(cold_p50 / bound, 4),
+        "swap_gbs": round(swap_gbs, 2), "link_peak_gbs": round(link, 2), "link_theoretical_gbs": PCIE5_X16_GBS,
+        "warm_p50_ms": round(warm_p50, 4), "roofline": roofline, "cpu_baseline": cpu, "elbow_sweep": sweep,
+        "extra": extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -90,16 +90,22 @@ typedef struct {
 enum { TP_COPY_MEMCPY = 0, TP_COPY_GATHER = 1 };
 enum {
   TP_FLAG_POISON = 1,    /* evicted extents are filled with 0xFF (NaN for fp32/bf16) */
-  TP_FLAG_THROTTLE = 2   /* a bounded delay kernel precedes every chunk on the copy stream */
+  TP_FLAG_THROTTLE = 2,  /* a bounded delay kernel precedes every chunk on the copy stream */
+  TP_FLAG_NO_GRAPH = 4   /* launch warm requests kernel by kernel instead of replaying a graph */
 };
 
 /* Context configuration. arena_dev/work_dev are caller-owned device buffers that must
- * stay valid until tp_destroy; the library never frees them. copy_stream: NULL makes
- * the library create (and later destroy) one non-blocking stream. chunk_min_bytes is
- * the transfer group size G (0 = one chunk per layer). copy_method: TP_COPY_MEMCPY uses
- * hipMemcpyAsync; TP_COPY_GATHER runs a copy kernel reading host-mapped pinned memory
- * with gather_wgs workgroups (0 = default). throttle_us: delay per chunk under
- * TP_FLAG_THROTTLE. */
+ * stay valid until tp_destroy; the library never frees them. copy_stream: the primary
+ * copy stream (NULL: the library creates and later destroys one non-blocking stream);
+ * with copy_streams == 2 the library adds a second non-blocking stream and alternates
+ * chunks between the two, forked from the primary after every ordering wait (0 or 1:
+ * one stream, so chunks arrive in first-use order at the full link rate).
+ * chunk_min_bytes is the transfer group size G (0 = one chunk per layer). copy_method:
+ * TP_COPY_MEMCPY uses hipMemcpyAsync; TP_COPY_GATHER runs a copy kernel reading
+ * host-mapped pinned memory with gather_wgs workgroups (0 = default). throttle_us:
+ * delay per chunk under TP_FLAG_THROTTLE. Warm requests replay an instantiated HIP
+ * graph of the forward pass, cached per (model, batch, input, output) unless
+ * TP_FLAG_NO_GRAPH is set. */
 typedef struct {
   void* arena_dev;
   uint64_t arena_bytes;
@@ -111,6 +117,7 @@ typedef struct {
   int32_t gather_wgs;
   int32_t flags;
   int32_t throttle_us;
+  int32_t copy_streams;
 } tp_config;
 
 typedef struct {

@@ -29,7 +29,29 @@ Model* find(tp_ctx* c, int32_t id) {
   return it == c->models.end() ? nullptr : it->second.get();
 }
 
+hipError_t sync_copies(tp_ctx* c) {
+  hipError_t e = hipSuccess;
+  for (int i = 0; i < 2; ++i)
+    if (c->copy[i] && e == hipSuccess) e = hipStreamSynchronize(c->copy[i]);
+  return e;
+}
+
+void destroy_streams(tp_ctx* c) {
+  if (c->own_copy && c->copy[0]) (void)hipStreamDestroy(c->copy[0]);
+  if (c->copy[1]) (void)hipStreamDestroy(c->copy[1]);
+  if (c->capture) (void)hipStreamDestroy(c->capture);
+  if (c->req_done) (void)hipEventDestroy(c->req_done);
+  if (c->fork) (void)hipEventDestroy(c->fork);
+}
+
+void drop_graphs(Model* m) {
+  for (auto& g : m->graphs)
+    if (g.exec) (void)hipGraphExecDestroy(g.exec);
+  m->graphs.clear();
+}
+
 void free_model(Model* m) {
+  drop_graphs(m);
   for (hipEvent_t e : m->chunk_ev)
     if (e) (void)hipEventDestroy(e);
   if (m->last_use) (void)hipEventDestroy(m->last_use);
@@ -42,8 +64,8 @@ tp_status retire(tp_ctx* c, int32_t id, uint64_t off, uint64_t len) {
   c->retired.push_back({off, len, id});
   if (c->cfg.flags & TP_FLAG_POISON) {
     Model* m = find(c, id);
-    if (m && m->used) TP_HIP(hipStreamWaitEvent(c->copy, m->last_use, 0));
-    TP_HIP(hipMemsetAsync(c->arena + off, 0xFF, len, c->copy));
+    if (m && m->used) TP_HIP(hipStreamWaitEvent(c->copy[0], m->last_use, 0));
+    TP_HIP(hipMemsetAsync(c->arena + off, 0xFF, len, c->copy[0]));
   }
   return ok();
 }
@@ -60,7 +82,7 @@ tp_status claim(tp_ctx* c, uint64_t off, uint64_t len) {
       continue;
     }
     Model* m = find(c, r.model);
-    if (m && m->used) TP_HIP(hipStreamWaitEvent(c->copy, m->last_use, 0));
+    if (m && m->used) TP_HIP(hipStreamWaitEvent(c->copy[0], m->last_use, 0));
     if (r.off < off) keep.push_back({r.off, off - r.off, r.model});
     if (rend > end) keep.push_back({end, rend - end, r.model});
   }
@@ -70,17 +92,23 @@ tp_status claim(tp_ctx* c, uint64_t off, uint64_t len) {
 
 tp_status enqueue_swap(tp_ctx* c, Model* m, uint64_t off) {
   char* dst = c->arena + off;
-  for (size_t i = 0; i < m->chunks.size(); ++i) {
+  const size_t n = m->chunks.size();
+  const int ns = (c->ncopy == 2 && n > 1) ? 2 : 1;
+  if (ns == 2) {
+    // everything ordered on copy[0] so far (victim waits, poison) precedes copy[1]'s chunks
+    TP_HIP(hipEventRecord(c->fork, c->copy[0]));
+    TP_HIP(hipStreamWaitEvent(c->copy[1], c->fork, 0));
+  }
+  for (size_t i = 0; i < n; ++i) {
     const Chunk& ch = m->chunks[i];
-    const uint64_t n = ch.end - ch.begin;
-    if (c->cfg.flags & TP_FLAG_THROTTLE) TP_HIP(k::delay(c->cfg.throttle_us, c->copy));
+    const uint64_t nb = ch.end - ch.begin;
+    hipStream_t s = c->copy[i % ns];
+    if (c->cfg.flags & TP_FLAG_THROTTLE) TP_HIP(k::delay(c->cfg.throttle_us, s));
     if (c->cfg.copy_method == TP_COPY_GATHER)
-      TP_HIP(k::gather_copy(static_cast<char*>(m->host_dev) + ch.begin, dst + ch.begin, n, c->cfg.gather_wgs,
-                            c->copy));
+      TP_HIP(k::gather_copy(static_cast<char*>(m->host_dev) + ch.begin, dst + ch.begin, nb, c->cfg.gather_wgs, s));
     else
-      TP_HIP(hipMemcpyAsync(dst + ch.begin, static_cast<char*>(m->host) + ch.begin, n, hipMemcpyHostToDevice,
-                            c->copy));
-    TP_HIP(hipEventRecord(m->chunk_ev[i], c->copy));
+      TP_HIP(hipMemcpyAsync(dst + ch.begin, static_cast<char*>(m->host) + ch.begin, nb, hipMemcpyHostToDevice, s));
+    TP_HIP(hipEventRecord(m->chunk_ev[i], s));
   }
   return ok();
 }
@@ -103,6 +131,61 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
     return fail(s, msg);
   }
   return ok();
+}
+
+hipError_t run_forward(ExecCtx& x) {
+  switch (x.m->spec.arch) {
+    case TP_ARCH_MLP: return run_mlp(x);
+    case TP_ARCH_RESNET50: return run_resnet(x);
+    case TP_ARCH_BERT: return run_bert(x);
+  }
+  return hipErrorInvalidValue;
+}
+
+// Warm request: replay the model's forward pass as one graph launch. The graph is
+// captured from the same kernel sequence (on a private stream, nothing executes) the
+// first time a (batch, input, output, extent) combination is seen; up to kGraphs
+// combinations stay instantiated per model. If capture fails the model falls back to
+// launching its kernels one by one, which computes the same bits.
+constexpr size_t kGraphs = 4;
+
+hipError_t launch_graph(tp_ctx* c, Model* m, char* base, const void* in, int batch, void* out, hipStream_t stream) {
+  GraphEntry* hit = nullptr;
+  for (auto& g : m->graphs)
+    if (g.batch == batch && g.in == in && g.out == out && g.base == base) hit = &g;
+  if (!hit) {
+    Waiter w;
+    w.m = m;
+    ExecCtx x{m, base, c->work, in, out, batch, c->capture, &w};
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    hipError_t e = hipStreamBeginCapture(c->capture, hipStreamCaptureModeThreadLocal);
+    if (e == hipSuccess) {
+      hipError_t er = run_forward(x);
+      e = hipStreamEndCapture(c->capture, &graph);
+      if (er != hipSuccess) e = er;
+    }
+    if (e == hipSuccess) e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    if (graph) (void)hipGraphDestroy(graph);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      m->graph_failed = true;
+      Waiter w2;
+      w2.m = m;
+      ExecCtx x2{m, base, c->work, in, out, batch, stream, &w2};
+      return run_forward(x2);
+    }
+    if (m->graphs.size() >= kGraphs) {
+      auto oldest = std::min_element(m->graphs.begin(), m->graphs.end(),
+                                     [](const GraphEntry& a, const GraphEntry& b) { return a.stamp < b.stamp; });
+      (void)hipGraphExecDestroy(oldest->exec);
+      m->graphs.erase(oldest);
+    }
+    m->graphs.push_back({batch, in, out, base, exec, 0});
+    hit = &m->graphs.back();
+  }
+  hit->stamp = ++c->graph_clock;
+  return hipGraphLaunch(hit->exec, stream);
 }
 
 tp_status begin_request(tp_ctx* c, hipStream_t stream) {
@@ -144,6 +227,7 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
     return fail(TP_E_INVAL, "tp_create: unknown copy_method");
   if (cfg->gather_wgs < 0 || cfg->gather_wgs > 4096 || cfg->throttle_us < 0 || cfg->throttle_us > 100000)
     return fail(TP_E_INVAL, "tp_create: gather_wgs or throttle_us out of range");
+  if (cfg->copy_streams < 0 || cfg->copy_streams > 2) return fail(TP_E_INVAL, "tp_create: copy_streams must be 0, 1 or 2");
   std::unique_ptr<tp_ctx> c(new (std::nothrow) tp_ctx);
   if (!c) return fail(TP_E_NOSPC, "out of host memory");
   c->cfg = *cfg;
@@ -152,16 +236,21 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   c->work = static_cast<char*>(cfg->work_dev);
   c->policy.reset(new Arena(cfg->arena_bytes, 256));
   TP_HIP(hipGetDevice(&c->device));
+  c->ncopy = cfg->copy_streams == 2 ? 2 : 1;
+  hipError_t e = hipSuccess;
   if (cfg->copy_stream) {
-    c->copy = static_cast<hipStream_t>(cfg->copy_stream);
+    c->copy[0] = static_cast<hipStream_t>(cfg->copy_stream);
   } else {
-    TP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
-    c->own_copy = true;
+    e = hipStreamCreateWithFlags(&c->copy[0], hipStreamNonBlocking);
+    c->own_copy = e == hipSuccess;
   }
-  hipError_t e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
+  if (e == hipSuccess && c->ncopy == 2) e = hipStreamCreateWithFlags(&c->copy[1], hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming);
   if (e != hipSuccess) {
-    if (c->own_copy) (void)hipStreamDestroy(c->copy);
-    return hip_fail(e, "hipEventCreateWithFlags");
+    destroy_streams(c.get());
+    return hip_fail(e, "tp_create: stream or event creation");
   }
   *out = c.release();
   return ok();
@@ -169,14 +258,13 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
 
 tp_status tp_destroy(tp_ctx* c) {
   if (!c) return fail(TP_E_INVAL, "NULL context");
-  hipError_t e = hipStreamSynchronize(c->copy);
+  hipError_t e = sync_copies(c);
   if (e == hipSuccess && c->any_request) e = hipEventSynchronize(c->req_done);
   for (auto& kv : c->models) {
     if (kv.second->used) (void)hipEventSynchronize(kv.second->last_use);
     free_model(kv.second.get());
   }
-  (void)hipEventDestroy(c->req_done);
-  if (c->own_copy) (void)hipStreamDestroy(c->copy);
+  destroy_streams(c);
   delete c;
   return e == hipSuccess ? ok() : hip_fail(e, "tp_destroy synchronisation");
 }
@@ -222,8 +310,8 @@ tp_status tp_unregister_model(tp_ctx* c, int32_t id) {
   if (!c) return fail(TP_E_INVAL, "NULL context");
   Model* m = find(c, id);
   if (!m) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
-  // the copy stream may still read the host copy; the last use may still read the extent
-  TP_HIP(hipStreamSynchronize(c->copy));
+  // the copy streams may still read the host copy; the last use may still read the extent
+  TP_HIP(sync_copies(c));
   if (m->used) TP_HIP(hipEventSynchronize(m->last_use));
   if (c->policy->resident(id)) c->policy->evict(id);
   c->retired.erase(std::remove_if(c->retired.begin(), c->retired.end(),
@@ -249,16 +337,16 @@ tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, 
   bool swapped = false;
   if ((s = admit(c, m, &swapped)) != TP_OK) return s;
   const uint64_t off = c->policy->offset(id);
-  Waiter w;
-  w.m = m;
-  w.stream = stream;
-  w.swapping = swapped;
-  ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w};
-  hipError_t e = hipErrorInvalidValue;
-  switch (m->spec.arch) {
-    case TP_ARCH_MLP: e = run_mlp(x); break;
-    case TP_ARCH_RESNET50: e = run_resnet(x); break;
-    case TP_ARCH_BERT: e = run_bert(x); break;
+  hipError_t e = hipSuccess;
+  if (!swapped && !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed) {
+    e = launch_graph(c, m, c->arena + off, input_dev, batch, output_dev, stream);
+  } else {
+    Waiter w;
+    w.m = m;
+    w.stream = stream;
+    w.swapping = swapped;
+    ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w};
+    e = run_forward(x);
   }
   if (e != hipSuccess) {
     // keep the ordering intact, then leave the model non-resident
@@ -278,7 +366,11 @@ tp_status tp_swap_in(tp_ctx* c, int32_t id, void* stream_) {
   if ((s = begin_request(c, stream)) != TP_OK) return s;
   bool swapped = false;
   if ((s = admit(c, m, &swapped)) != TP_OK) return s;
-  if (swapped) TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev.back(), 0));
+  if (swapped) {
+    const size_t n = m->chunk_ev.size();
+    TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev[n - 1], 0));
+    if (c->ncopy == 2 && n > 1) TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev[n - 2], 0));
+  }
   return end_request(c, m, stream);
 }
 

@@ -14,6 +14,17 @@
 
 namespace tp {
 
+// An instantiated graph of one warm forward pass: kernel arguments (weight, workspace,
+// input and output addresses, batch) are baked in, so it is keyed by all of them.
+struct GraphEntry {
+  int batch = 0;
+  const void* in = nullptr;
+  void* out = nullptr;
+  const char* base = nullptr;
+  hipGraphExec_t exec = nullptr;
+  uint64_t stamp = 0;
+};
+
 struct Model {
   int32_t id = 0;
   ModelSpec spec;
@@ -24,11 +35,13 @@ struct Model {
   std::vector<hipEvent_t> chunk_ev;
   hipEvent_t last_use = nullptr;
   bool used = false;             // last_use has been recorded at least once
+  std::vector<GraphEntry> graphs;
+  bool graph_failed = false;     // capture failed once: launch this model kernel by kernel
 };
 
-// Makes `stream` wait for the chunk holding a layer, once per chunk, in first-use order.
-// Chunks complete in order on the single copy stream, so waiting for chunk c covers all
-// earlier chunks.
+// Makes `stream` wait for the chunks holding a layer's weights before its first kernel.
+// Chunks alternate between copy streams, so each chunk's event is waited for itself,
+// once, in first-use order.
 struct Waiter {
   const Model* m = nullptr;
   hipStream_t stream = nullptr;
@@ -37,9 +50,12 @@ struct Waiter {
   hipError_t need(uint32_t layer) {
     if (!swapping) return hipSuccess;
     const int c = (int)m->chunk_of_layer[layer];
-    if (c <= waited) return hipSuccess;
-    waited = c;
-    return hipStreamWaitEvent(stream, m->chunk_ev[c], 0);
+    while (waited < c) {
+      ++waited;
+      hipError_t e = hipStreamWaitEvent(stream, m->chunk_ev[waited], 0);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
   }
 };
 
@@ -70,8 +86,12 @@ struct tp_ctx {
   tp_config cfg{};
   char* arena = nullptr;
   char* work = nullptr;
-  hipStream_t copy = nullptr;
+  hipStream_t copy[2] = {nullptr, nullptr};   // copy[0] carries all ordering waits
+  int ncopy = 1;
   bool own_copy = false;
+  hipEvent_t fork = nullptr;                   // copy[1] starts a swap after copy[0]
+  hipStream_t capture = nullptr;               // private stream for graph capture
+  uint64_t graph_clock = 0;
   std::unique_ptr<tp::Arena> policy;
   std::unordered_map<int32_t, std::unique_ptr<tp::Model>> models;
   int32_t next_id = 1;

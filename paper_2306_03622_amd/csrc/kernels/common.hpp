@@ -30,6 +30,12 @@ __device__ __forceinline__ float act_apply(float v, int act) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// branch-free zeroing of a loaded vector (the load itself is always in bounds)
+__device__ __forceinline__ uint4 mask_u4(uint4 v, bool ok) {
+  const uint32_t m = ok ? 0xffffffffu : 0u;
+  return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+}
+
 // butterfly sum over the 64 lanes of a wave (fixed order: bit-identical across runs)
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -89,33 +89,44 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
   const int n0 = blockIdx.x * 16;
   const bool nvalid = n0 + r < a.N;
   const uint16_t* wrow = a.w + (size_t)(nvalid ? n0 + r : 0) * a.K;
-  const uint4 zero = make_uint4(0, 0, 0, 0);
+  const uint16_t* xrow[MT];
+  bool mvalid[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    const int m = (t << 4) + r;
+    mvalid[t] = m < a.M;
+    xrow[t] = a.x + (size_t)(mvalid[t] ? m : 0) * a.K;
+  }
   f32x4 acc[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // k-block of 128: load j of lane (r, q) covers k = kb*128 + 32 j + 8 q .. +8, so one
+  // load instruction reads 64 contiguous bytes of each of the 16 weight rows
   const int nkb = (a.K + 127) >> 7;
-  for (int kb = wave; kb < nkb; kb += NW) {
-    const int kbase = (kb << 7) + (q << 5);
-    uint4 av[4], bv[MT][4];
+  for (int kb0 = wave; kb0 < nkb; kb0 += 2 * NW) {
+    uint4 av[2][4], bv[2][MT][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int kk = kbase + (j << 3);
-      av[j] = (nvalid && kk < a.K) ? *reinterpret_cast<const uint4*>(wrow + kk) : zero;
-    }
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      const int m = (t << 4) + r;
+    for (int u = 0; u < 2; ++u) {
+      const int kb = kb0 + u * NW;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int kk = kbase + (j << 3);
-        bv[t][j] = (m < a.M && kk < a.K) ? *reinterpret_cast<const uint4*>(a.x + (size_t)m * a.K + kk) : zero;
+        const int kk = (kb << 7) + (j << 5) + (q << 3);
+        const bool kin = kb < nkb && kk < a.K;
+        const int ks = kin ? kk : 0;
+        av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + ks), nvalid && kin);
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+          bv[u][t][j] = mask_u4(*reinterpret_cast<const uint4*>(xrow[t] + ks), mvalid[t] && kin);
       }
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int t = 0; t < MT; ++t)
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[j]), as_bf16x8(bv[t][j]), acc[t], 0, 0, 0);
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[u][j]), as_bf16x8(bv[u][t][j]), acc[t], 0, 0,
+                                                           0);
   }
   __shared__ f32x4 red[NW][MT][64];
 #pragma unroll
@@ -155,42 +166,47 @@ __device__ __forceinline__ RowInfo row_info(const GemmArgs& a, int m) {
 
 template <int MODE>
 __device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, int k) {
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  if (!ri.valid || k >= a.K) return zero;
-  if (MODE == X_ROWS) return *reinterpret_cast<const uint4*>(a.x + (size_t)ri.b * a.K + k);
+  if (MODE == X_ROWS) {
+    const bool ok = ri.valid && k < a.K;
+    return mask_u4(*reinterpret_cast<const uint4*>(a.x + (size_t)ri.b * a.K + (ok ? k : 0)), ok);
+  }
   if (MODE == X_CONV8) {
     const int tap = k / a.C, c = k - tap * a.C;
     const int kh = tap / a.KW, kw = tap - kh * a.KW;
     const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
-    if (ih < 0 || ih >= a.H || iw < 0 || iw >= a.W) return zero;
-    return *reinterpret_cast<const uint4*>(a.x + (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c);
+    const bool ok = ri.valid && k < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+    const size_t off = ok ? (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c : 0;
+    return mask_u4(*reinterpret_cast<const uint4*>(a.x + off), ok);
   }
-  uint16_t v[8];
+  uint32_t v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int kk = k + e;
-    v[e] = 0;
-    if (kk < a.K) {
-      const int tap = kk / a.C, c = kk - tap * a.C;
-      const int kh = tap / a.KW, kw = tap - kh * a.KW;
-      const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
-      if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) v[e] = a.x[(((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c];
-    }
+    const int tap = kk / a.C, c = kk - tap * a.C;
+    const int kh = tap / a.KW, kw = tap - kh * a.KW;
+    const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
+    const bool ok = ri.valid && kk < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+    const size_t off = ok ? (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c : 0;
+    v[e] = ok ? (uint32_t)a.x[off] : 0u;
   }
-  return make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16), v[4] | ((uint32_t)v[5] << 16),
-                    v[6] | ((uint32_t)v[7] << 16));
+  return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
 template <bool WVEC>
 __device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
-  if (n >= a.N || k >= a.K) return make_uint4(0, 0, 0, 0);
-  const uint16_t* p = a.w + (size_t)n * a.K + k;
-  if (WVEC) return *reinterpret_cast<const uint4*>(p);
-  uint16_t v[8];
+  const bool row_ok = n < a.N;
+  const uint16_t* p = a.w + (size_t)(row_ok ? n : 0) * a.K;
+  if (WVEC) {
+    const bool ok = row_ok && k < a.K;
+    return mask_u4(*reinterpret_cast<const uint4*>(p + (ok ? k : 0)), ok);
+  }
+  uint32_t v[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) v[e] = (k + e < a.K) ? p[e] : (uint16_t)0;
-  return make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16), v[4] | ((uint32_t)v[5] << 16),
-                    v[6] | ((uint32_t)v[7] << 16));
+  for (int e = 0; e < 8; ++e) {
+    const bool ok = row_ok && k + e < a.K;
+    v[e] = ok ? (uint32_t)p[ok ? k + e : 0] : 0u;
+  }
+  return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
 template <int BN, int BM, int MODE, bool WVEC>

@@ -24,13 +24,15 @@ TP_F32, TP_BF16 = 0, 1
 TP_ARCH_MLP, TP_ARCH_RESNET50, TP_ARCH_BERT = 0, 1, 2
 TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
 TP_COPY_MEMCPY, TP_COPY_GATHER = 0, 1
-TP_FLAG_POISON, TP_FLAG_THROTTLE = 1, 2
+TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH = 1, 2, 4
 ROLES = {
     "w": 0, "b": 1,
     "tok_emb": 10, "pos_emb": 11, "type_emb": 12, "emb_ln_g": 13, "emb_ln_b": 14,
     "qkv_w": 20, "qkv_b": 21, "o_w": 22, "o_b": 23, "ln1_g": 24, "ln1_b": 25,
     "ffn1_w": 26, "ffn1_b": 27, "ffn2_w": 28, "ffn2_b": 29, "ln2_g": 30, "ln2_b": 31,
 }
+# transfer group size G (whole layers per chunk, closed once a chunk holds >= G bytes)
+DEFAULT_CHUNK = 8 << 20
 ARCHS = {"mlp": TP_ARCH_MLP, "resnet50": TP_ARCH_RESNET50, "bert": TP_ARCH_BERT}
 DTYPES = {"f32": TP_F32, "bf16": TP_BF16}
 
@@ -49,7 +51,7 @@ class tp_config(C.Structure):
     _fields_ = [("arena_dev", C.c_void_p), ("arena_bytes", C.c_uint64), ("work_dev", C.c_void_p),
                 ("work_bytes", C.c_uint64), ("copy_stream", C.c_void_p), ("chunk_min_bytes", C.c_uint64),
                 ("copy_method", C.c_int32), ("gather_wgs", C.c_int32), ("flags", C.c_int32),
-                ("throttle_us", C.c_int32)]
+                ("throttle_us", C.c_int32), ("copy_streams", C.c_int32)]
 
 
 class tp_arena_stats_t(C.Structure):
@@ -198,11 +200,11 @@ class ModelDesc:
 
 # ------------------------------------------------------------------ C calls
 
-def tp_create(arena_dev, arena_bytes, work_dev, work_bytes, copy_stream=None, chunk_min_bytes=2 << 20,
-              copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0):
+def tp_create(arena_dev, arena_bytes, work_dev, work_bytes, copy_stream=None, chunk_min_bytes=DEFAULT_CHUNK,
+              copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0, copy_streams=0):
     L = lib()
     cfg = tp_config(_ptr(arena_dev), arena_bytes, _ptr(work_dev), work_bytes, _ptr(copy_stream), chunk_min_bytes,
-                    copy_method, gather_wgs, flags, throttle_us)
+                    copy_method, gather_wgs, flags, throttle_us, copy_streams)
     ctx = _P()
     _check(L, L.tp_create(C.byref(cfg), C.byref(ctx)))
     return ctx
@@ -323,9 +325,9 @@ class HostArena:
 class Runtime:
     """A context whose arena and workspace are torch allocations made once."""
 
-    def __init__(self, arena_bytes: int, work_bytes: int, device: int = 0, chunk_min_bytes: int = 2 << 20,
+    def __init__(self, arena_bytes: int, work_bytes: int, device: int = 0, chunk_min_bytes: int = DEFAULT_CHUNK,
                  copy_method: int = TP_COPY_MEMCPY, gather_wgs: int = 0, flags: int = 0, throttle_us: int = 0,
-                 copy_stream=None):
+                 copy_stream=None, copy_streams: int = 0):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("libtorpor needs a HIP device")
@@ -336,7 +338,7 @@ class Runtime:
         self.work = torch.empty(max(work_bytes, 256), dtype=torch.uint8, device=self.device)
         self.copy_stream = copy_stream
         self.ctx = tp_create(self.arena, arena_bytes, self.work, self.work.numel(), copy_stream, chunk_min_bytes,
-                             copy_method, gather_wgs, flags, throttle_us)
+                             copy_method, gather_wgs, flags, throttle_us, copy_streams)
         self.descs = {}
 
     def close(self):

@@ -8,7 +8,11 @@ import pytest
 import paper_2306_03622_amd as tp
 import synth
 from oracle.arena_sim import ArenaSim
-from tests.common import infer, log, make_runtime, torch_dev
+from tests.common import infer, log, make_runtime, out_shape, to_device, torch_dev
+
+
+def infer_shape(m):
+    return out_shape(m, 1)[1:]
 
 pytestmark = pytest.mark.gpu
 
@@ -39,10 +43,12 @@ def test_swapped_bytes_identical(method, chunk):
 
 
 @pytest.mark.parametrize("method", [tp.TP_COPY_MEMCPY, tp.TP_COPY_GATHER])
-def test_pipelined_equals_preloaded(method):
+@pytest.mark.parametrize("streams", [1, 2])
+def test_pipelined_equals_preloaded(method, streams):
     ms, xs = _models(), None
     xs = _inputs(ms)
-    rt, ids = make_runtime(ms, batch_max=2, copy_method=method, chunk_min_bytes=0)
+    rt, ids = make_runtime(ms, batch_max=2, copy_method=method, chunk_min_bytes=0, copy_streams=streams,
+                           flags=tp.TP_FLAG_NO_GRAPH)
     torch, dev = torch_dev()
     s = torch.cuda.Stream(device=dev)
     for mid, m, x in zip(ids, ms, xs):
@@ -53,6 +59,33 @@ def test_pipelined_equals_preloaded(method):
         s.synchronize()
         preloaded = infer(rt, mid, m, x, stream=s)
         assert np.array_equal(pipelined, preloaded)
+    rt.close()
+
+
+def test_warm_graph_replay_equals_kernel_by_kernel():
+    ms = _models()
+    torch, dev = torch_dev()
+    eager_rt, eager_ids = make_runtime(ms, batch_max=3, flags=tp.TP_FLAG_NO_GRAPH)
+    rt, ids = make_runtime(ms, batch_max=3)
+    s = torch.cuda.Stream(device=dev)
+    for k, m in enumerate(ms):
+        # same buffers, new contents each request; then a different output buffer and batch
+        x_np = synth.config_input(m, 3, 200 + k)
+        x = torch.empty_like(to_device(x_np))
+        outs = [torch.empty((3,) + tuple(infer_shape(m)), dtype=torch.float32, device=dev) for _ in range(2)]
+        for rep in range(5):
+            x_np = synth.config_input(m, 3, 300 + 10 * k + rep)
+            x.copy_(to_device(x_np))
+            want = infer(eager_rt, eager_ids[k], m, x_np)
+            out = outs[rep % 2]
+            torch.cuda.synchronize()
+            rt.infer(ids[k], x, out, stream=s)
+            s.synchronize()
+            assert np.array_equal(out.cpu().numpy(), want), (m.arch, rep)
+        # a smaller batch through a sliced input makes a new graph
+        got = infer(rt, ids[k], m, x_np[:1])
+        assert np.array_equal(got, infer(eager_rt, eager_ids[k], m, x_np[:1]))
+    eager_rt.close()
     rt.close()
 
 
