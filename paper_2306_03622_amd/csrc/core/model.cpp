@@ -219,6 +219,10 @@ std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes) {
 }
 
 uint64_t workspace_bytes(const ModelSpec& m, int32_t batch) {
+  return activation_bytes(m, batch) + (m.dtype == TP_BF16 ? kSplitScratch : 0);
+}
+
+uint64_t activation_bytes(const ModelSpec& m, int32_t batch) {
   const uint64_t B = (uint64_t)std::max(batch, 1);
   switch (m.arch) {
     case TP_ARCH_MLP: {

@@ -53,7 +53,14 @@ tp_status validate_model(const tp_model_desc* d, uint64_t host_bytes, ModelSpec*
 // layer boundary where it holds >= min_bytes. Chunks tile [0, host_bytes).
 std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes);
 
-// Workspace needed by the executors for `batch` samples (each buffer 256-aligned).
+// Activation buffers of the executors for `batch` samples (each buffer 256-aligned).
+uint64_t activation_bytes(const ModelSpec& m, int32_t batch);
+
+// fp32 partial tiles for contractions split over k (bf16 families only); placed after
+// the activation buffers.
+constexpr uint64_t kSplitScratch = 8ull << 20;
+
+// Workspace needed by tp_infer: activations, then the split scratch.
 uint64_t workspace_bytes(const ModelSpec& m, int32_t batch);
 
 inline uint64_t round_up(uint64_t n, uint64_t a) { return (n + a - 1) / a * a; }

@@ -37,7 +37,8 @@ hipError_t run_mlp(ExecCtx& x) {
       ep.act = a;
       ep.out = dst;
       ep.out_f32 = last;
-      TP_TRY(k::linear_bf16(static_cast<const uint16_t*>(cur), B, W, x.t<uint16_t>(l, TP_ROLE_W), W, ep, x.stream));
+      TP_TRY(k::linear_bf16(static_cast<const uint16_t*>(cur), B, W, x.t<uint16_t>(l, TP_ROLE_W), W, ep, x.split,
+                             x.stream));
     }
     cur = dst;
   }
@@ -64,7 +65,7 @@ hipError_t run_resnet(ExecCtx& x) {
     ep.act = act;
     ep.out = out;
     return k::conv_bf16(in, B, c.hin, c.hin, c.c.cin, x.t<uint16_t>(layer, TP_ROLE_W), c.c.cout, c.c.k, c.c.k,
-                        c.c.stride, c.c.pad, ep, x.stream);
+                        c.c.stride, c.c.pad, ep, x.split, x.stream);
   };
 
   TP_TRY(conv(0, static_cast<const uint16_t*>(x.in), buf[0], nullptr, k::ACT_RELU));
@@ -98,7 +99,7 @@ hipError_t run_resnet(ExecCtx& x) {
   ep.bias = x.t<uint16_t>(li, TP_ROLE_B);
   ep.out = x.out;
   ep.out_f32 = 1;
-  return k::linear_bf16(pooled, B, 2048, x.t<uint16_t>(li, TP_ROLE_W), classes, ep, x.stream);
+  return k::linear_bf16(pooled, B, 2048, x.t<uint16_t>(li, TP_ROLE_W), classes, ep, x.split, x.stream);
 }
 
 hipError_t run_bert(ExecCtx& x) {
@@ -127,27 +128,27 @@ hipError_t run_bert(ExecCtx& x) {
     k::Epilogue e1;
     e1.bias = x.t<uint16_t>(l, TP_ROLE_QKV_B);
     e1.out = qkv;
-    TP_TRY(k::linear_bf16(h, M, d, x.t<uint16_t>(l, TP_ROLE_QKV_W), 3 * d, e1, x.stream));
+    TP_TRY(k::linear_bf16(h, M, d, x.t<uint16_t>(l, TP_ROLE_QKV_W), 3 * d, e1, x.split, x.stream));
     TP_TRY(k::attention(qkv, B, S, H, att, x.stream));
     k::Epilogue e2;
     e2.bias = x.t<uint16_t>(l, TP_ROLE_O_B);
     e2.res = h;
     e2.out = pre;
     e2.out_f32 = 1;
-    TP_TRY(k::linear_bf16(att, M, d, x.t<uint16_t>(l, TP_ROLE_O_W), d, e2, x.stream));
+    TP_TRY(k::linear_bf16(att, M, d, x.t<uint16_t>(l, TP_ROLE_O_W), d, e2, x.split, x.stream));
     TP_TRY(k::layernorm(pre, M, d, x.t<uint16_t>(l, TP_ROLE_LN1_G), x.t<uint16_t>(l, TP_ROLE_LN1_B), eps, h, 0,
                         x.stream));
     k::Epilogue e3;
     e3.bias = x.t<uint16_t>(l, TP_ROLE_FFN1_B);
     e3.act = k::ACT_GELU;
     e3.out = ff;
-    TP_TRY(k::linear_bf16(h, M, d, x.t<uint16_t>(l, TP_ROLE_FFN1_W), F, e3, x.stream));
+    TP_TRY(k::linear_bf16(h, M, d, x.t<uint16_t>(l, TP_ROLE_FFN1_W), F, e3, x.split, x.stream));
     k::Epilogue e4;
     e4.bias = x.t<uint16_t>(l, TP_ROLE_FFN2_B);
     e4.res = h;
     e4.out = pre;
     e4.out_f32 = 1;
-    TP_TRY(k::linear_bf16(ff, M, F, x.t<uint16_t>(l, TP_ROLE_FFN2_W), d, e4, x.stream));
+    TP_TRY(k::linear_bf16(ff, M, F, x.t<uint16_t>(l, TP_ROLE_FFN2_W), d, e4, x.split, x.stream));
     const bool last = l == L;
     TP_TRY(k::layernorm(pre, M, d, x.t<uint16_t>(l, TP_ROLE_LN2_G), x.t<uint16_t>(l, TP_ROLE_LN2_B), eps,
                         last ? x.out : static_cast<void*>(h), last ? 1 : 0, x.stream));

@@ -44,6 +44,14 @@ void destroy_streams(tp_ctx* c) {
   if (c->fork) (void)hipEventDestroy(c->fork);
 }
 
+k::Split make_split(tp_ctx* c, const Model* m, int batch) {
+  k::Split sp;
+  if (m->spec.dtype != TP_BF16) return sp;
+  sp.partials = reinterpret_cast<float*>(c->work + activation_bytes(m->spec, batch));
+  sp.partial_bytes = kSplitScratch;
+  return sp;
+}
+
 void drop_graphs(Model* m) {
   for (auto& g : m->graphs)
     if (g.exec) (void)hipGraphExecDestroy(g.exec);
@@ -90,31 +98,34 @@ tp_status claim(tp_ctx* c, uint64_t off, uint64_t len) {
   return ok();
 }
 
-tp_status enqueue_swap(tp_ctx* c, Model* m, uint64_t off) {
-  char* dst = c->arena + off;
+// Enqueues the copy of chunk i of `m` into the extent at arena offset `off`, then its event.
+hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
   const size_t n = m->chunks.size();
   const int ns = (c->ncopy == 2 && n > 1) ? 2 : 1;
-  if (ns == 2) {
+  hipError_t e = hipSuccess;
+  if (i == 0 && ns == 2) {
     // everything ordered on copy[0] so far (victim waits, poison) precedes copy[1]'s chunks
-    TP_HIP(hipEventRecord(c->fork, c->copy[0]));
-    TP_HIP(hipStreamWaitEvent(c->copy[1], c->fork, 0));
+    e = hipEventRecord(c->fork, c->copy[0]);
+    if (e == hipSuccess) e = hipStreamWaitEvent(c->copy[1], c->fork, 0);
   }
-  for (size_t i = 0; i < n; ++i) {
-    const Chunk& ch = m->chunks[i];
-    const uint64_t nb = ch.end - ch.begin;
-    hipStream_t s = c->copy[i % ns];
-    if (c->cfg.flags & TP_FLAG_THROTTLE) TP_HIP(k::delay(c->cfg.throttle_us, s));
+  const Chunk& ch = m->chunks[i];
+  const uint64_t nb = ch.end - ch.begin;
+  char* dst = c->arena + off + ch.begin;
+  hipStream_t s = c->copy[i % ns];
+  if (e == hipSuccess && (c->cfg.flags & TP_FLAG_THROTTLE)) e = k::delay(c->cfg.throttle_us, s);
+  if (e == hipSuccess) {
     if (c->cfg.copy_method == TP_COPY_GATHER)
-      TP_HIP(k::gather_copy(static_cast<char*>(m->host_dev) + ch.begin, dst + ch.begin, nb, c->cfg.gather_wgs, s));
+      e = k::gather_copy(static_cast<char*>(m->host_dev) + ch.begin, dst, nb, c->cfg.gather_wgs, s);
     else
-      TP_HIP(hipMemcpyAsync(dst + ch.begin, static_cast<char*>(m->host) + ch.begin, nb, hipMemcpyHostToDevice, s));
-    TP_HIP(hipEventRecord(m->chunk_ev[i], s));
+      e = hipMemcpyAsync(dst, static_cast<char*>(m->host) + ch.begin, nb, hipMemcpyHostToDevice, s);
   }
-  return ok();
+  if (e == hipSuccess) e = hipEventRecord(m->chunk_ev[i], s);
+  return e;
 }
 
-// One request's admission: a hit, or victims invalidated, their readers waited for, and
-// the model's chunks enqueued. On failure the model is left non-resident.
+// One request's admission: a hit, or victims invalidated and their readers waited for on
+// the primary copy stream; the chunk copies are then issued by the request's Waiter. On
+// failure the model is left non-resident.
 tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   Arena::Decision d = c->policy->request(m->id);
   *swapped = !d.hit;
@@ -123,7 +134,6 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   for (int32_t v : d.victims)
     if (s == TP_OK) s = retire(c, v, c->policy->offset(v), c->policy->bytes(v));
   if (s == TP_OK) s = claim(c, d.offset, m->spec.host_bytes);
-  if (s == TP_OK) s = enqueue_swap(c, m, d.offset);
   if (s != TP_OK) {
     const std::string msg = last_error();
     c->policy->evict(m->id);
@@ -132,6 +142,16 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   }
   return ok();
 }
+
+}  // namespace
+
+hipError_t tp::Waiter::issue_through(int c) {
+  hipError_t e = hipSuccess;
+  while (e == hipSuccess && issued <= c && issued < (int)m->chunks.size()) e = enqueue_chunk(ctx, m, base_off, issued++);
+  return e;
+}
+
+namespace {
 
 hipError_t run_forward(ExecCtx& x) {
   switch (x.m->spec.arch) {
@@ -156,7 +176,7 @@ hipError_t launch_graph(tp_ctx* c, Model* m, char* base, const void* in, int bat
   if (!hit) {
     Waiter w;
     w.m = m;
-    ExecCtx x{m, base, c->work, in, out, batch, c->capture, &w};
+    ExecCtx x{m, base, c->work, in, out, batch, c->capture, &w, make_split(c, m, batch)};
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
     hipError_t e = hipStreamBeginCapture(c->capture, hipStreamCaptureModeThreadLocal);
@@ -172,7 +192,7 @@ hipError_t launch_graph(tp_ctx* c, Model* m, char* base, const void* in, int bat
       m->graph_failed = true;
       Waiter w2;
       w2.m = m;
-      ExecCtx x2{m, base, c->work, in, out, batch, stream, &w2};
+      ExecCtx x2{m, base, c->work, in, out, batch, stream, &w2, make_split(c, m, batch)};
       return run_forward(x2);
     }
     if (m->graphs.size() >= kGraphs) {
@@ -345,8 +365,12 @@ tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, 
     w.m = m;
     w.stream = stream;
     w.swapping = swapped;
-    ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w};
+    w.ctx = c;
+    w.base_off = off;
+    ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w, make_split(c, m, batch)};
     e = run_forward(x);
+    // every layer asks for its chunk; issue any the forward pass did not reach
+    if (e == hipSuccess && swapped) e = w.issue_through((int)m->chunks.size() - 1);
   }
   if (e != hipSuccess) {
     // keep the ordering intact, then leave the model non-resident
@@ -367,6 +391,16 @@ tp_status tp_swap_in(tp_ctx* c, int32_t id, void* stream_) {
   bool swapped = false;
   if ((s = admit(c, m, &swapped)) != TP_OK) return s;
   if (swapped) {
+    Waiter w;
+    w.m = m;
+    w.ctx = c;
+    w.base_off = c->policy->offset(id);
+    hipError_t e = w.issue_through((int)m->chunks.size() - 1);
+    if (e != hipSuccess) {
+      c->policy->evict(id);
+      (void)retire(c, id, w.base_off, m->spec.host_bytes);
+      return hip_fail(e, "tp_swap_in: copy enqueue");
+    }
     const size_t n = m->chunk_ev.size();
     TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev[n - 1], 0));
     if (c->ncopy == 2 && n > 1) TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev[n - 2], 0));

@@ -10,6 +10,7 @@
 
 #include "../core/arena.hpp"
 #include "../core/model.hpp"
+#include "../kernels/kernels.hpp"
 #include "torpor.h"
 
 namespace tp {
@@ -39,23 +40,31 @@ struct Model {
   bool graph_failed = false;     // capture failed once: launch this model kernel by kernel
 };
 
-// Makes `stream` wait for the chunks holding a layer's weights before its first kernel.
-// Chunks alternate between copy streams, so each chunk's event is waited for itself,
-// once, in first-use order.
+// Drives a cold request's swap from the layer loop. Before the first kernel of a layer,
+// need() issues the copies of every chunk up to the one holding that layer (each copy
+// followed by its event on a copy stream) and makes `stream` wait for those events.
+// Copies are thus issued interleaved with the layer kernels: copy c+1 is enqueued after
+// the kernels of chunk c. When the runtime maps the copy stream onto the same hardware
+// queue as the compute stream, this order keeps each chunk's event packet behind the
+// kernels that precede it instead of ahead of all of them.
 struct Waiter {
   const Model* m = nullptr;
   hipStream_t stream = nullptr;
   bool swapping = false;
   int waited = -1;
+  tp_ctx* ctx = nullptr;
+  uint64_t base_off = 0;
+  int issued = 0;                // chunks whose copies are enqueued
+  hipError_t issue_through(int c);
   hipError_t need(uint32_t layer) {
     if (!swapping) return hipSuccess;
     const int c = (int)m->chunk_of_layer[layer];
-    while (waited < c) {
+    hipError_t e = issue_through(c);
+    while (e == hipSuccess && waited < c) {
       ++waited;
-      hipError_t e = hipStreamWaitEvent(stream, m->chunk_ev[waited], 0);
-      if (e != hipSuccess) return e;
+      e = hipStreamWaitEvent(stream, m->chunk_ev[waited], 0);
     }
-    return hipSuccess;
+    return e;
   }
 };
 
@@ -69,6 +78,7 @@ struct ExecCtx {
   int batch;
   hipStream_t stream;
   Waiter* wait;
+  k::Split split;    // scratch for contractions split over k
   template <typename T>
   const T* t(uint32_t layer, uint32_t role) const {
     return reinterpret_cast<const T*>(base + m->spec.t(layer, role).offset);

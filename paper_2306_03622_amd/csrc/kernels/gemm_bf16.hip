@@ -13,10 +13,12 @@
 //     workgroup owns 16 weight rows and its 16 waves stream disjoint 128-wide k-blocks
 //     with 4 x 16-byte loads per lane in flight, then reduce across waves through LDS in
 //     a fixed order.
-//   * k_gemm: LDS-tiled BN x BM x 32 tiles, 4 waves in a 2 x 2 arrangement, global loads
-//     of the next k-stage issued before the MFMAs of the current one. The activation
-//     loader is either a plain row-major matrix or an NHWC implicit-GEMM (im2col) gather
-//     for convolutions, k = (kh * KW + kw) * C + c, matching OHWI weight rows.
+//   * k_gemm: LDS-tiled BN x BM x BK tiles, 4 waves in a 2 x 2 arrangement, global loads
+//     of the next k-stage issued before the MFMAs of the current one, double-buffered LDS,
+//     and a deterministic split over k when the tile grid alone cannot fill the chip. The
+//     activation loader is either a plain row-major matrix or an NHWC implicit-GEMM
+//     (im2col) gather for convolutions, k = (kh * KW + kw) * C + c, matching OHWI weight
+//     rows.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -33,6 +35,8 @@ struct GemmArgs {
   int M, N, K;
   int H, W, C, KW, stride, pad, Ho, Wo;   // convolution geometry (X_CONV*)
   Epilogue ep;
+  int kst, splits;                        // k-stages per split, number of splits
+  float* partials;                        // [splits][M][N] fp32 when splits > 1
 };
 
 __device__ __forceinline__ void store_row4(const GemmArgs& a, int m, int n0, f32x4 acc) {
@@ -209,22 +213,29 @@ __device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
   return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
-template <int BN, int BM, int MODE, bool WVEC>
+// One BN x BM output tile over the k-stages [s0, s1) of this split (blockIdx.z). Global
+// loads of stage s+1 are issued before the MFMAs of stage s; LDS is double-buffered so
+// one barrier per stage suffices. With a.splits > 1 every split stores its fp32 partial
+// to a.partials and k_split_reduce (the next launch on the stream) sums the partials in
+// split order, which is fixed, so results are bit-reproducible.
+template <int BN, int BM, int BK, int MODE, bool WVEC>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-  constexpr int BK = 32, LDK = BK + 8;
-  constexpr int VA = BN / 64, VB = BM / 64;      // 16-byte vectors per thread per stage
-  constexpr int NB = BN / 32, MB = BM / 32;      // 16 x 16 MFMA blocks per wave
-  __shared__ __attribute__((aligned(16))) uint16_t As[BN * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BM * LDK];
+  constexpr int LDK = BK + 8;
+  constexpr int KV = BK / 8;                    // 16-byte vectors per row and stage
+  constexpr int RSTEP = 256 / KV;               // rows covered by one pass of 256 threads
+  constexpr int VA = BN / RSTEP, VB = BM / RSTEP;
+  constexpr int NB = BN / 32, MB = BM / 32;     // 16 x 16 blocks per wave (wave tile BN/2 x BM/2)
+  static_assert(VA >= 1 && VB >= 1 && BK % 32 == 0, "tile shape");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * (BN + BM) * LDK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn = wave & 1, wm = wave >> 1;
   const int n_base = blockIdx.x * BN, m_base = blockIdx.y * BM;
-  const int kq = (tid & 3) << 3;
+  const int row0 = tid / KV, kq = (tid % KV) * 8;
 
   RowInfo ri[VB];
 #pragma unroll
-  for (int p = 0; p < VB; ++p) ri[p] = row_info<MODE>(a, m_base + (tid >> 2) + 64 * p);
+  for (int p = 0; p < VB; ++p) ri[p] = row_info<MODE>(a, m_base + row0 + RSTEP * p);
 
   f32x4 acc[NB][MB];
 #pragma unroll
@@ -232,36 +243,73 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < MB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  uint4 ra[VA], rb[VB];
   const int nst = (a.K + BK - 1) / BK;
-  auto load_stage = [&](int s) {
+  const int s0 = blockIdx.z * a.kst;
+  const int s1 = min(s0 + a.kst, nst);
+  uint4 ra[VA], rb[VB];
+  auto load = [&](int s) {
     const int k = s * BK + kq;
 #pragma unroll
-    for (int p = 0; p < VA; ++p) ra[p] = load_w8<WVEC>(a, n_base + (tid >> 2) + 64 * p, k);
+    for (int p = 0; p < VA; ++p) ra[p] = load_w8<WVEC>(a, n_base + row0 + RSTEP * p, k);
 #pragma unroll
     for (int p = 0; p < VB; ++p) rb[p] = load_x8<MODE>(a, ri[p], k);
   };
-  load_stage(0);
-  for (int s = 0; s < nst; ++s) {
+  auto store = [&](int buf) {
+    uint16_t* As = lds + buf * (BN + BM) * LDK;
+    uint16_t* Bs = As + BN * LDK;
 #pragma unroll
-    for (int p = 0; p < VA; ++p) *reinterpret_cast<uint4*>(&As[((tid >> 2) + 64 * p) * LDK + kq]) = ra[p];
+    for (int p = 0; p < VA; ++p) *reinterpret_cast<uint4*>(&As[(row0 + RSTEP * p) * LDK + kq]) = ra[p];
 #pragma unroll
-    for (int p = 0; p < VB; ++p) *reinterpret_cast<uint4*>(&Bs[((tid >> 2) + 64 * p) * LDK + kq]) = rb[p];
-    __syncthreads();
-    if (s + 1 < nst) load_stage(s + 1);
-    uint4 fa[NB], fb[MB];
+    for (int p = 0; p < VB; ++p) *reinterpret_cast<uint4*>(&Bs[(row0 + RSTEP * p) * LDK + kq]) = rb[p];
+  };
+  if (s0 < s1) {
+    load(s0);
+    store(0);
+  }
+  __syncthreads();
+  for (int s = s0; s < s1; ++s) {
+    const int cur = (s - s0) & 1;
+    if (s + 1 < s1) load(s + 1);
+    const uint16_t* As = lds + cur * (BN + BM) * LDK;
+    const uint16_t* Bs = As + BN * LDK;
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
-      fa[i] = *reinterpret_cast<const uint4*>(&As[(wn * (BN / 2) + i * 16 + (lane & 15)) * LDK + ((lane >> 4) << 3)]);
+    for (int kk = 0; kk < BK; kk += 32) {
+      uint4 fa[NB], fb[MB];
 #pragma unroll
-    for (int j = 0; j < MB; ++j)
-      fb[j] = *reinterpret_cast<const uint4*>(&Bs[(wm * (BM / 2) + j * 16 + (lane & 15)) * LDK + ((lane >> 4) << 3)]);
-#pragma unroll
-    for (int i = 0; i < NB; ++i)
+      for (int i = 0; i < NB; ++i)
+        fa[i] = *reinterpret_cast<const uint4*>(&As[(wn * (BN / 2) + i * 16 + (lane & 15)) * LDK + kk + ((lane >> 4) << 3)]);
 #pragma unroll
       for (int j = 0; j < MB; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[i]), as_bf16x8(fb[j]), acc[i][j], 0, 0, 0);
+        fb[j] = *reinterpret_cast<const uint4*>(&Bs[(wm * (BM / 2) + j * 16 + (lane & 15)) * LDK + kk + ((lane >> 4) << 3)]);
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[i]), as_bf16x8(fb[j]), acc[i][j], 0, 0, 0);
+    }
+    if (s + 1 < s1) store(cur ^ 1);
     __syncthreads();
+  }
+
+  if (a.splits > 1) {
+    // fp32 partial of this split: P[split][m][n], four consecutive n per lane
+    float* part = a.partials + (size_t)blockIdx.z * a.M * a.N;
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+#pragma unroll
+      for (int j = 0; j < MB; ++j) {
+        const int m = m_base + wm * (BM / 2) + j * 16 + (lane & 15);
+        const int n = n_base + wn * (BN / 2) + i * 16 + ((lane >> 4) << 2);
+        if (m < a.M && n < a.N) {
+          const f32x4 v = acc[i][j];
+          if (n + 3 < a.N && (a.N & 3) == 0) {
+            *reinterpret_cast<float4*>(part + (size_t)m * a.N + n) = make_float4(v[0], v[1], v[2], v[3]);
+          } else {
+            for (int e = 0; e < 4 && n + e < a.N; ++e) part[(size_t)m * a.N + n + e] = v[e];
+          }
+        }
+      }
+    return;
   }
 #pragma unroll
   for (int i = 0; i < NB; ++i)
@@ -271,18 +319,60 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
                  n_base + wn * (BN / 2) + i * 16 + ((lane >> 4) << 2), acc[i][j]);
 }
 
-template <int BN, int BM, int MODE, bool WVEC>
-hipError_t launch_tiled(const GemmArgs& a, hipStream_t s) {
-  dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM);
-  hipLaunchKernelGGL((k_gemm<BN, BM, MODE, WVEC>), grid, dim3(256), 0, s, a);
+// y = epilogue(sum over splits z = 0, 1, ... of P[z]) for four consecutive outputs per thread
+__global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
+  const long q = (long)blockIdx.x * 256 + threadIdx.x;       // index of a group of 4 outputs
+  const int groups_per_row = (a.N + 3) >> 2;
+  const long total = (long)a.M * groups_per_row;
+  if (q >= total) return;
+  const int m = (int)(q / groups_per_row), n0 = (int)(q - (long)m * groups_per_row) * 4;
+  const size_t plane = (size_t)a.M * a.N;
+  f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int z = 0; z < a.splits; ++z) {
+    const float* p = a.partials + z * plane + (size_t)m * a.N + n0;
+    if (n0 + 3 < a.N && (a.N & 3) == 0) {
+      const float4 v = *reinterpret_cast<const float4*>(p);
+      sum += f32x4{v.x, v.y, v.z, v.w};
+    } else {
+      for (int e = 0; e < 4 && n0 + e < a.N; ++e) sum[e] += p[e];
+    }
+  }
+  store_row4(a, m, n0, sum);
+}
+
+template <int BN, int BM, int BK, int MODE, bool WVEC>
+hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
+  const int tn = (a.N + BN - 1) / BN, tm = (a.M + BM - 1) / BM, tiles = tn * tm;
+  const int nst = (a.K + BK - 1) / BK;
+  int splits = 1;
+  if (sp.partials && tiles < 128) {
+    // aim for about 512 workgroups, at least 4 k-stages per split, within the scratch
+    const size_t per_split = (size_t)a.M * a.N * 4;
+    int want = (512 + tiles - 1) / tiles;
+    want = min(want, max(nst / 4, 1));
+    want = min(want, 16);
+    while (want > 1 && per_split * want > sp.partial_bytes) --want;
+    splits = max(want, 1);
+  }
+  a.kst = (nst + splits - 1) / splits;
+  a.splits = (nst + a.kst - 1) / a.kst;        // no empty split
+  a.partials = sp.partials;
+  dim3 grid(tn, tm, a.splits);
+  hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC>), grid, dim3(256), 0, s, a);
+  if (a.splits > 1) {
+    const long groups = (long)a.M * ((a.N + 3) / 4);
+    hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
 template <int MODE, bool WVEC>
-hipError_t pick_tiled(const GemmArgs& a, hipStream_t s) {
+hipError_t pick_tiled(const GemmArgs& a, const Split& sp, hipStream_t s) {
+  // 64 x 64 tiles keep several workgroups per CU resident (latency hiding by occupancy);
+  // 128 x 128 only once the grid has well over a few tiles per CU
   const long tiles128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
-  if (tiles128 >= 240) return launch_tiled<128, 128, MODE, WVEC>(a, s);
-  return launch_tiled<64, 64, MODE, WVEC>(a, s);
+  if (tiles128 >= 1024) return launch_tiled<128, 128, 64, MODE, WVEC>(a, sp, s);
+  return launch_tiled<64, 64, 64, MODE, WVEC>(a, sp, s);
 }
 
 bool ep_ok(const Epilogue& ep) { return ep.out != nullptr && ep.act >= 0 && ep.act <= 2; }
@@ -290,7 +380,7 @@ bool ep_ok(const Epilogue& ep) { return ep.out != nullptr && ep.act >= 0 && ep.a
 }  // namespace
 
 hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N, const Epilogue& ep,
-                       hipStream_t s) {
+                       const Split& sp, hipStream_t s) {
   if (!x || !w || M < 1 || N < 1 || K < 8 || (K & 7) || !ep_ok(ep)) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = x; a.w = w; a.M = M; a.N = N; a.K = K; a.ep = ep;
@@ -302,25 +392,25 @@ hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N
     hipLaunchKernelGGL((k_gemv<2, 16>), dim3((N + 15) / 16), dim3(1024), 0, s, a);
     return hipGetLastError();
   }
-  return pick_tiled<X_ROWS, true>(a, s);
+  return pick_tiled<X_ROWS, true>(a, sp, s);
 }
 
 hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16_t* w, int O, int KH, int KW,
-                     int stride, int pad, const Epilogue& ep, hipStream_t s) {
+                     int stride, int pad, const Epilogue& ep, const Split& sp, hipStream_t s) {
   if (!x || !w || B < 1 || H < 1 || W < 1 || C < 1 || O < 1 || KH < 1 || KW < 1 || stride < 1 || pad < 0 ||
       !ep_ok(ep))
     return hipErrorInvalidValue;
   const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
   if (Ho < 1 || Wo < 1) return hipErrorInvalidValue;
   if (KH == 1 && KW == 1 && stride == 1 && pad == 0 && (C & 7) == 0)
-    return linear_bf16(x, B * H * W, C, w, O, ep, s);
+    return linear_bf16(x, B * H * W, C, w, O, ep, sp, s);
   GemmArgs a{};
   a.x = x; a.w = w; a.M = B * Ho * Wo; a.N = O; a.K = KH * KW * C;
   a.H = H; a.W = W; a.C = C; a.KW = KW; a.stride = stride; a.pad = pad; a.Ho = Ho; a.Wo = Wo;
   a.ep = ep;
-  if ((C & 7) == 0) return pick_tiled<X_CONV8, true>(a, s);
-  if ((a.K & 7) == 0) return pick_tiled<X_CONV1, true>(a, s);
-  return pick_tiled<X_CONV1, false>(a, s);
+  if ((C & 7) == 0) return pick_tiled<X_CONV8, true>(a, sp, s);
+  if ((a.K & 7) == 0) return pick_tiled<X_CONV1, true>(a, sp, s);
+  return pick_tiled<X_CONV1, false>(a, sp, s);
 }
 
 }  // namespace k

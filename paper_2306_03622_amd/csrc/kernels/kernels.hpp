@@ -21,14 +21,20 @@ struct Epilogue {
   int out_f32 = 0;                  // out dtype: 0 bf16, 1 fp32
 };
 
+// Scratch for splitting a contraction over k into fp32 partials (null disables splitting).
+struct Split {
+  float* partials = nullptr;
+  size_t partial_bytes = 0;
+};
+
 // y[M][N] = x[M][K] * w[N][K]^T with the epilogue; bf16 in, fp32 accumulate. K % 8 == 0.
 hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N, const Epilogue& ep,
-                       hipStream_t s);
+                       const Split& sp, hipStream_t s);
 
 // Implicit-GEMM convolution: x NHWC [B][H][W][C] bf16, w OHWI [O][KH][KW][C] bf16,
 // y NHWC [B][Ho][Wo][O] via the epilogue (M = B*Ho*Wo rows of N = O).
 hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16_t* w, int O, int KH, int KW,
-                     int stride, int pad, const Epilogue& ep, hipStream_t s);
+                     int stride, int pad, const Epilogue& ep, const Split& sp, hipStream_t s);
 
 // fp32 linear: y[M][N] = act(x[M][K] * w[N][K]^T + bias). K % 4 == 0.
 hipError_t linear_f32(const float* x, int M, int K, const float* w, int N, const float* bias, int act, float* y,
