@@ -177,6 +177,78 @@ def elbow_sweep(torch, dev, method, copy_streams=0, sizes=(256 << 10, 512 << 10,
     return {"model": "256 x 512 bf16 MLP (512 KiB per layer)", "rows": rows, "elbow_bytes": elbow}
 
 
+def tenants(torch, dev, n_requests, n_models, arena_gib, workers):
+    """Open-loop multi-tenant run: n_models registered models of the three families, an
+    arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU."""
+    import paper_2306_03622_amd as tp
+    import synth
+    specs = synth.tenant_models(n_models)
+    trace = synth.tenant_trace(n_requests, n_models=n_models)
+    ws = 0
+    descs, kinds, host_bytes = {}, {}, {}
+    for cfg in (2, 3, 4):
+        ws = max(ws, tp.tp_workspace_bytes(tp.ModelDesc.of(synth.config_model(cfg)), 1))
+    rt = tp.Runtime(arena_gib << 30, ws)
+    t0 = time.perf_counter()
+    ids = []
+    for i, m in synth.build_models(specs, workers):
+        d = tp.ModelDesc.of(m)
+        mid = rt.register(d, m.blob())
+        ids.append(mid)
+        kinds[mid] = m.arch
+        host_bytes[mid] = m.total_bytes
+        if i % 10 == 9:
+            log(f"  registered {i + 1} models ({(time.perf_counter() - t0):.0f} s)")
+        m.drop_blob()
+    reg_s = time.perf_counter() - t0
+    protos = {cfg: synth.config_model(cfg, 0) for cfg in (2, 3, 4)}      # shapes only
+    xs, outs, reqs = [], [], []
+    for r in range(n_requests):
+        mid = ids[int(trace.model[r])]
+        proto = protos[specs[int(trace.model[r])][0]]
+        x = to_dev(torch, synth.request_input(proto, int(trace.input_seed[r])), dev)
+        y = torch.empty(out_shape(proto, 1), dtype=torch.float32, device=dev)
+        xs.append(x)
+        outs.append(y)
+        reqs.append((mid, 1, x, y, int(trace.arrival_s[r] * 1e9)))
+    stream = torch.cuda.Stream(device=dev)
+    # warm every family's kernels once, then start from an empty arena
+    for cfg in (2, 3, 4):
+        k = next(i for i, sp in enumerate(specs) if sp[0] == cfg)
+        r0 = next(r for r in range(n_requests) if int(trace.model[r]) == k) if k in set(trace.model.tolist()) else None
+        x = xs[r0] if r0 is not None else to_dev(torch, synth.request_input(protos[cfg], 1), dev)
+        y = torch.empty(out_shape(protos[cfg], 1), dtype=torch.float32, device=dev)
+        rt.infer(ids[k], x, y, stream=stream)
+    stream.synchronize()
+    for mid in ids:
+        rt.evict(mid)
+    st0 = rt.stats()
+    torch.cuda.synchronize()
+    log(f"running {n_requests} requests over {trace.arrival_s[-1]:.1f} s")
+    res = rt.run_trace(reqs, stream=stream)
+    st1 = rt.stats()
+    rt.close()
+    lat = np.array([(r["done_ns"] - q[4]) / 1e6 for r, q in zip(res, reqs)])
+    hit = np.array([r["hit"] for r in res])
+    arch = np.array([kinds[q[0]] for q in reqs])
+    per = {}
+    for a in ("mlp", "resnet50", "bert"):
+        sel = arch == a
+        if sel.any():
+            per[a] = {"requests": int(sel.sum()), "p50_ms": round(float(np.percentile(lat[sel], 50)), 3),
+                      "p99_ms": round(float(np.percentile(lat[sel], 99)), 3),
+                      "hit_rate": round(float(hit[sel].mean()), 4)}
+    delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped")}
+    return {"metric": "multi-tenant request latency (open loop, LRU)", "unit": "ms",
+            "p50_ms": round(float(np.percentile(lat, 50)), 3), "p99_ms": round(float(np.percentile(lat, 99)), 3),
+            "hit_rate": round(float(hit.mean()), 4), "requests": n_requests, "models": n_models,
+            "arena_gib": arena_gib, "registered_host_bytes": int(sum(host_bytes.values())),
+            "register_s": round(reg_s, 1), "trace_s": round(float(trace.arrival_s[-1]), 2),
+            "per_family": per, "arena": delta,
+            "config": {"workload": f"{n_models} models (24x4096 MLP / ResNet-50 / BERT-base by index mod 3), "
+                                   f"Poisson 50 req/s, Zipf(1.1), {arena_gib} GiB arena, batch 1"}}
+
+
 def kernel_fingerprint():
     """First 16 hex digits of sha256 over the skinny-GEMM kernel sources."""
     import hashlib
@@ -236,6 +308,10 @@ def main():
                     help="transfer group size G in bytes, 'default' (the library's) or 'elbow' (this run's sweep)")
     ap.add_argument("--no-sweep", action="store_true", help="skip the group-size sweep")
     ap.add_argument("--copy-streams", type=int, default=0, help="copy streams of the library (0: its default)")
+    ap.add_argument("--tenants", type=int, default=0, metavar="N_REQUESTS",
+                    help="run the multi-tenant open-loop workload with this many requests instead")
+    ap.add_argument("--tenant-models", type=int, default=100)
+    ap.add_argument("--tenant-arena-gib", type=int, default=8)
     ap.add_argument("--pmc-workload", action="store_true",
                     help="run only a fixed workload for hardware-counter passes: 20 warm forwards of the "
                          "bench model, then one 256 MiB device-to-device copy (the byte-count calibration)")
@@ -254,6 +330,10 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+
+    if a.tenants:
+        print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16)), flush=True)
+        return
 
     if a.pmc_workload:
         model = synth.config_model(2)

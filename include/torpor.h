@@ -196,6 +196,32 @@ TP_API tp_status tp_model_chunks(struct tp_ctx* ctx, int32_t model_id, uint64_t*
 /* Workspace bytes tp_infer needs for this model at this batch size (host-only). */
 TP_API tp_status tp_workspace_bytes(const tp_model_desc* desc, int32_t batch, uint64_t* bytes);
 
+/* One request of an open-loop trace (tp_run_trace). */
+typedef struct {
+  int32_t model_id;
+  int32_t batch;
+  const void* input_dev;
+  void* output_dev;
+  uint64_t arrival_ns;      /* arrival time, nanoseconds after the start of the trace */
+} tp_request;
+
+typedef struct {
+  uint64_t issue_ns;        /* when tp_infer was called (ns after the start) */
+  uint64_t done_ns;         /* when the host observed the request's completion */
+  int32_t hit;              /* the model was resident when the request was issued */
+  int32_t status;           /* tp_infer's status for this request */
+} tp_request_result;
+
+/* Replays an open-loop request trace (the paper's serving setting, Sec. 3 and Sec. 7: requests
+ * arrive independently of completions). The calling thread sleeps until each request's arrival
+ * time and issues tp_infer on `stream`; a second thread waits for the requests' completions in
+ * issue order and stamps the time the host sees each one, so latency = done - arrival includes
+ * queueing behind earlier requests. At most 256 requests are in flight (a fixed ring of events
+ * created once per context); the dispatcher waits for a free slot beyond that. Requests whose
+ * tp_infer fails carry the status and are not waited for. Returns after the last completion. */
+TP_API tp_status tp_run_trace(struct tp_ctx* ctx, const tp_request* requests, uint32_t n, void* stream,
+                              tp_request_result* results);
+
 /* Thread-local message describing the last non-OK status ("" if none). */
 TP_API const char* tp_last_error(void);
 

@@ -23,7 +23,7 @@ HOST_LIB = os.path.join(PKG, "libtorpor_host.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 CORE = ["core/model.cpp", "core/arena.cpp", "core/plan_api.cpp", "core/errors.cpp"]
-HIP_HOST = ["hip/runtime.cpp", "hip/executors.cpp"]
+HIP_HOST = ["hip/runtime.cpp", "hip/executors.cpp", "hip/trace.cpp"]
 KERNELS = ["kernels/gemm_bf16.hip", "kernels/linear_f32.hip", "kernels/norm.hip", "kernels/attention.hip",
            "kernels/pool_copy.hip"]
 
@@ -60,7 +60,7 @@ def build(jobs: int = 8, sanitize: bool = False, verbose: bool = False) -> str:
                 print(msg, file=sys.stderr)
     objs = [_obj(s) for s in CORE + HIP_HOST + KERNELS]
     tmp = LIB + ".tmp"
-    _run([HIPCC, "-shared", "-fPIC", *DEVICE, "-o", tmp, *objs])
+    _run([HIPCC, "-shared", "-fPIC", *DEVICE, "-o", tmp, *objs, "-lpthread"])
     os.replace(tmp, LIB)
     # host-only planning library
     san = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer"] if sanitize else []

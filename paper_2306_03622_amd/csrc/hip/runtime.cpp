@@ -42,6 +42,8 @@ void destroy_streams(tp_ctx* c) {
   if (c->capture) (void)hipStreamDestroy(c->capture);
   if (c->req_done) (void)hipEventDestroy(c->req_done);
   if (c->fork) (void)hipEventDestroy(c->fork);
+  for (hipEvent_t e : c->trace_ev)
+    if (e) (void)hipEventDestroy(e);
 }
 
 k::Split make_split(tp_ctx* c, const Model* m, int batch) {

@@ -109,6 +109,7 @@ struct tp_ctx {
   hipEvent_t req_done = nullptr;
   hipStream_t last_stream = nullptr;
   bool any_request = false;
+  std::vector<hipEvent_t> trace_ev;            // completion ring of tp_run_trace
   // extents invalidated but possibly still read by enqueued work of their old owner
   struct Retired {
     uint64_t off, len;

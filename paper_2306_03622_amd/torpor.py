@@ -72,6 +72,15 @@ class tp_model_info_t(C.Structure):
         return {k: getattr(self, k) for k, _ in self._fields_}
 
 
+class tp_request(C.Structure):
+    _fields_ = [("model_id", C.c_int32), ("batch", C.c_int32), ("input_dev", C.c_void_p),
+                ("output_dev", C.c_void_p), ("arrival_ns", C.c_uint64)]
+
+
+class tp_request_result(C.Structure):
+    _fields_ = [("issue_ns", C.c_uint64), ("done_ns", C.c_uint64), ("hit", C.c_int32), ("status", C.c_int32)]
+
+
 class TorporError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"status {status}: {msg}")
@@ -93,6 +102,7 @@ _SIGS = {
     "tp_model_chunks": [_P, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
                         C.c_uint32, C.POINTER(C.c_uint32)],
     "tp_workspace_bytes": [C.POINTER(tp_model_desc), C.c_int32, C.POINTER(C.c_uint64)],
+    "tp_run_trace": [_P, C.POINTER(tp_request), C.c_uint32, _P, C.POINTER(tp_request_result)],
     "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
     "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                  C.POINTER(C.c_uint32), C.c_uint32, C.POINTER(C.c_uint32)],
@@ -270,6 +280,22 @@ def tp_workspace_bytes(desc: ModelDesc, batch: int) -> int:
     return out.value
 
 
+def tp_run_trace(ctx, requests, stream=None):
+    """requests: iterable of (model_id, batch, input_dev, output_dev, arrival_ns).
+
+    Returns a list of dicts (issue_ns, done_ns, hit, status). Raises if any request failed
+    (after the whole trace ran)."""
+    reqs = list(requests)
+    arr = (tp_request * len(reqs))()
+    for i, (mid, b, x, y, t) in enumerate(reqs):
+        arr[i] = tp_request(mid, b, _ptr(x), _ptr(y), int(t))
+    res = (tp_request_result * len(reqs))()
+    st = lib().tp_run_trace(ctx, arr, len(reqs), _ptr(stream), res)
+    out = [{"issue_ns": r.issue_ns, "done_ns": r.done_ns, "hit": bool(r.hit), "status": r.status} for r in res]
+    _check(lib(), st)
+    return out
+
+
 # host-only planning calls; `L` picks the library (the HIP one by default)
 
 def tph_validate(desc: ModelDesc, host_bytes: int, L=None):
@@ -384,6 +410,10 @@ class Runtime:
 
     def chunks(self, mid):
         return tp_model_chunks(self.ctx, mid)
+
+    def run_trace(self, requests, stream=None):
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        return tp_run_trace(self.ctx, requests, s)
 
     def extent(self, mid):
         """The model's arena bytes (a view of the arena), when resident."""

@@ -8,3 +8,4 @@ from .models import (  # noqa: F401
     ALIGN, Tensor, Model, mlp, resnet50, bert, config_model, CONFIG_SEEDS,
     bf16_round, bf16_to_f32, mlp_input, resnet_input, bert_input, config_input,
 )
+from .tenants import tenant_models, tenant_trace, build_models, request_input  # noqa: F401,E402

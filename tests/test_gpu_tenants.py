@@ -1,0 +1,62 @@
+"""Multi-tenant open-loop replay (tp_run_trace) on the GPU, scaled down: 9 models of the
+three families, an arena that holds about a third of them, Poisson/Zipf arrivals.
+
+Checks: every request's hit flag and the arena's counters equal the reference simulator
+replayed on the same request sequence; every model's first output matches the oracle."""
+import numpy as np
+import pytest
+
+import paper_2306_03622_amd as tp
+import synth
+from oracle import forward as oracle
+from oracle.arena_sim import ArenaSim
+from tests.common import log, out_shape, to_device, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def test_tenant_trace_lru_and_first_outputs():
+    torch, dev = torch_dev()
+    specs = synth.tenant_models(9)
+    models = [m for _, m in synth.build_models(specs, workers=9)]
+    trace = synth.tenant_trace(120, n_models=9)
+    cap = (models[0].total_bytes + models[1].total_bytes + models[2].total_bytes) // 256 * 256 + (64 << 20)
+    ws = max(tp.tp_workspace_bytes(tp.ModelDesc.of(m), 1) for m in models)
+    rt = tp.Runtime(cap, ws)
+    ids = [rt.register(tp.ModelDesc.of(m), m.blob()) for m in models]
+    xs_np, reqs, outs = [], [], []
+    for r in range(len(trace.model)):
+        m = models[int(trace.model[r])]
+        x_np = synth.request_input(m, int(trace.input_seed[r]))
+        xs_np.append(x_np)
+        y = torch.full(out_shape(m, 1), float("nan"), dtype=torch.float32, device=dev)
+        outs.append(y)
+        reqs.append((ids[int(trace.model[r])], 1, to_device(x_np), y, int(trace.arrival_s[r] * 1e9)))
+    torch.cuda.synchronize()
+    log(f"replaying {len(reqs)} requests over {trace.arrival_s[-1]:.2f} s")
+    res = rt.run_trace(reqs)
+    torch.cuda.synchronize()
+    assert all(r["status"] == 0 for r in res)
+    assert all(r["done_ns"] >= r["issue_ns"] for r in res)
+
+    sim = ArenaSim(cap, align=256)
+    for i, m in zip(ids, models):
+        sim.register(i, m.total_bytes)
+    want_hits = [sim.request(q[0])["hit"] for q in reqs]
+    assert [r["hit"] for r in res] == want_hits
+    got = rt.stats()
+    for k, v in sim.stats().items():
+        assert got[k] == v, (k, got[k], v)
+    log(f"hit rate {np.mean(want_hits):.3f}, evictions {got['evictions']}")
+
+    seen = set()
+    for r, q in enumerate(reqs):
+        k = int(trace.model[r])
+        if k in seen:
+            continue
+        seen.add(k)
+        y = outs[r].cpu().numpy()
+        err = oracle.normwise_error(y, oracle.forward(models[k], xs_np[r])).max()
+        log(f"  model {k} ({models[k].arch}) first request {r}: error {err:.2e}")
+        assert np.all(np.isfinite(y)) and err <= 2e-2
+    rt.close()
