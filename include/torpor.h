@@ -188,6 +188,13 @@ TP_API tp_status tp_is_resident(struct tp_ctx* ctx, int32_t model_id, int32_t* r
 TP_API tp_status tp_arena_stats(struct tp_ctx* ctx, tp_arena_stats_t* out);
 TP_API tp_status tp_model_info(struct tp_ctx* ctx, int32_t model_id, tp_model_info_t* out);
 
+/* The library's pinned host image of a registered model (what a swap copies, byte for byte).
+ * It equals the registered bytes except that bf16 MLP weight matrices whose width is a
+ * multiple of 128 are stored blocked for the skinny-batch kernel: each block of 16 rows x
+ * 128 columns is contiguous, ordered [32-column group][8-column slot][row][8 elements].
+ * *ptr stays valid until the model is unregistered; read-only. */
+TP_API tp_status tp_model_host_image(struct tp_ctx* ctx, int32_t model_id, const void** ptr, uint64_t* bytes);
+
 /* Chunk plan of a registered model: fills up to `cap` entries of [begin, end) host
  * byte ranges and the first layer each chunk holds; *n receives the chunk count. */
 TP_API tp_status tp_model_chunks(struct tp_ctx* ctx, int32_t model_id, uint64_t* begin, uint64_t* end,

@@ -187,8 +187,23 @@ tp_status validate_model(const tp_model_desc* d, uint64_t host_bytes, ModelSpec*
     }
   }
   m.host_bytes = round_up(host_bytes, 256);
+  m.packed_mlp = m.arch == TP_ARCH_MLP && m.dtype == TP_BF16 && m.dims[1] % 128 == 0;
   *out = std::move(m);
   return TP_OK;
+}
+
+void pack_rows16x128(const uint16_t* src, uint16_t* dst, int64_t N, int64_t K) {
+  const int64_t nkb = K / 128;
+  for (int64_t t = 0; t < N / 16; ++t)
+    for (int64_t kb = 0; kb < nkb; ++kb) {
+      uint16_t* blk = dst + (t * nkb + kb) * 2048;
+      for (int j = 0; j < 4; ++j)
+        for (int q = 0; q < 4; ++q)
+          for (int r = 0; r < 16; ++r) {
+            const uint16_t* s8 = src + (t * 16 + r) * K + kb * 128 + j * 32 + q * 8;
+            std::copy(s8, s8 + 8, blk + j * 512 + (q * 16 + r) * 8);
+          }
+    }
 }
 
 std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes) {

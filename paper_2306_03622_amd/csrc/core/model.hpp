@@ -39,6 +39,7 @@ struct ModelSpec {
   uint32_t n_layers = 0;
   std::vector<int32_t> lookup;  // (layer * kRoles + role) -> tensor index, -1 if absent
   static constexpr int kRoles = 32;
+  bool packed_mlp = false;      // bf16 MLP weights stored in 16 x 128 blocks (see pack_rows16x128)
 
   const tp_tensor_desc& t(uint32_t layer, uint32_t role) const {
     return tensors[lookup[layer * kRoles + role]];
@@ -58,11 +59,16 @@ uint64_t activation_bytes(const ModelSpec& m, int32_t batch);
 
 // fp32 partial tiles for contractions split over k (bf16 families only); placed after
 // the activation buffers.
-constexpr uint64_t kSplitScratch = 8ull << 20;
+constexpr uint64_t kSplitScratch = 32ull << 20;
 
 // Workspace needed by tp_infer: activations, then the split scratch.
 uint64_t workspace_bytes(const ModelSpec& m, int32_t batch);
 
 inline uint64_t round_up(uint64_t n, uint64_t a) { return (n + a - 1) / a * a; }
+
+// Blocked copy of a bf16 [N][K] matrix (N % 16 == 0, K % 128 == 0): block (n/16, k/128) is
+// 2048 contiguous elements ordered [(k%128)/32][(k%32)/8][n%16][k%8], so that one 16-byte load
+// per lane of a 64-lane wave reads a whole 1 KB run of a skinny-GEMM operand.
+void pack_rows16x128(const uint16_t* src, uint16_t* dst, int64_t N, int64_t K);
 
 }  // namespace tp

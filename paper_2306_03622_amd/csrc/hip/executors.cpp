@@ -37,6 +37,7 @@ hipError_t run_mlp(ExecCtx& x) {
       ep.act = a;
       ep.out = dst;
       ep.out_f32 = last;
+      ep.w_packed = s.packed_mlp;
       TP_TRY(k::linear_bf16(static_cast<const uint16_t*>(cur), B, W, x.t<uint16_t>(l, TP_ROLE_W), W, ep, x.split,
                              x.stream));
     }

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cstring>
 #include <new>
+#include <thread>
 
 #include "../core/errors.hpp"
 #include "../kernels/kernels.hpp"
@@ -309,6 +310,21 @@ tp_status tp_register_model(tp_ctx* c, const tp_model_desc* desc, const void* ho
   if (e != hipSuccess) { m->host = nullptr; return hip_fail(e, "hipHostMalloc (pinned model copy)"); }
   std::memcpy(m->host, host_weights, host_bytes);
   if (nb > host_bytes) std::memset(static_cast<char*>(m->host) + host_bytes, 0, nb - host_bytes);
+  if (m->spec.packed_mlp) {
+    // weight matrices in the skinny-GEMM block order, one thread per group of layers
+    std::vector<std::thread> th;
+    const int L = m->spec.dims[0], W = m->spec.dims[1];
+    const int nt = std::max(1, std::min(8, L));
+    for (int w = 0; w < nt; ++w)
+      th.emplace_back([&, w] {
+        for (int l = w; l < L; l += nt) {
+          const tp_tensor_desc& t = m->spec.t(l, TP_ROLE_W);
+          pack_rows16x128(reinterpret_cast<const uint16_t*>(static_cast<const char*>(host_weights) + t.offset),
+                          reinterpret_cast<uint16_t*>(static_cast<char*>(m->host) + t.offset), W, W);
+        }
+      });
+    for (auto& t : th) t.join();
+  }
   e = hipHostGetDevicePointer(&m->host_dev, m->host, 0);
   m->chunk_ev.assign(m->chunks.size(), nullptr);
   for (size_t i = 0; e == hipSuccess && i < m->chunks.size(); ++i)
@@ -442,6 +458,15 @@ tp_status tp_model_info(tp_ctx* c, int32_t id, tp_model_info_t* out) {
   out->resident = c->policy->resident(id) ? 1 : 0;
   out->extent_offset = c->policy->offset(id);
   out->last_use_clock = c->policy->last_use(id);
+  return ok();
+}
+
+tp_status tp_model_host_image(tp_ctx* c, int32_t id, const void** ptr, uint64_t* bytes) {
+  if (!c || !ptr || !bytes) return fail(TP_E_INVAL, "NULL argument");
+  Model* m = find(c, id);
+  if (!m) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  *ptr = m->host;
+  *bytes = m->spec.host_bytes;
   return ok();
 }
 

@@ -27,7 +27,9 @@ namespace k {
 
 namespace {
 
-enum { X_ROWS = 0, X_CONV8 = 1, X_CONV1 = 2 };
+// activation loaders: row-major matrix; NHWC im2col with C % 64 == 0 (a 64-deep k-stage
+// then lies inside one filter tap); NHWC im2col with C % 8 == 0; element-wise im2col
+enum { X_ROWS = 0, X_CONV8 = 1, X_CONV1 = 2, X_CONV64 = 3 };
 
 struct GemmArgs {
   const uint16_t* x;
@@ -86,13 +88,19 @@ __device__ __forceinline__ void store_row4(const GemmArgs& a, int m, int n0, f32
 
 // ------------------------------------------------------------------ skinny M
 
-template <int MT, int NW>
+// PK: weights in 16 x 128 blocks (see pack_rows16x128 in the host code), so load j of
+// lane (r, q) in k-block kb reads 16 bytes at block offset j*512 + (q*16 + r)*8 and one
+// load instruction covers a contiguous 1 KB; otherwise rows are [N][K] and an instruction
+// reads 64 contiguous bytes of each of 16 rows. Activation rows beyond M issue no load.
+template <int MT, int NW, bool PK>
 __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, q = lane >> 4;
   const int n0 = blockIdx.x * 16;
   const bool nvalid = n0 + r < a.N;
-  const uint16_t* wrow = a.w + (size_t)(nvalid ? n0 + r : 0) * a.K;
+  const int nkb = (a.K + 127) >> 7;
+  const uint16_t* wrow = PK ? a.w + (size_t)blockIdx.x * nkb * 2048 + lane * 8
+                            : a.w + (size_t)(nvalid ? n0 + r : 0) * a.K;
   const uint16_t* xrow[MT];
   bool mvalid[MT];
 #pragma unroll
@@ -104,9 +112,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
   f32x4 acc[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // k-block of 128: load j of lane (r, q) covers k = kb*128 + 32 j + 8 q .. +8, so one
-  // load instruction reads 64 contiguous bytes of each of the 16 weight rows
-  const int nkb = (a.K + 127) >> 7;
+  // k-block of 128: load j of lane (r, q) covers k = kb*128 + 32 j + 8 q .. +8
   for (int kb0 = wave; kb0 < nkb; kb0 += 2 * NW) {
     uint4 av[2][4], bv[2][MT][4];
 #pragma unroll
@@ -117,10 +123,16 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
         const int kk = (kb << 7) + (j << 5) + (q << 3);
         const bool kin = kb < nkb && kk < a.K;
         const int ks = kin ? kk : 0;
-        av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + ks), nvalid && kin);
+        if (PK)
+          av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + (size_t)(kin ? kb : 0) * 2048 + j * 512), kin);
+        else
+          av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + ks), nvalid && kin);
 #pragma unroll
-        for (int t = 0; t < MT; ++t)
-          bv[u][t][j] = mask_u4(*reinterpret_cast<const uint4*>(xrow[t] + ks), mvalid[t] && kin);
+        for (int t = 0; t < MT; ++t) {
+          uint4 v = make_uint4(0, 0, 0, 0);
+          if (mvalid[t] && kin) v = *reinterpret_cast<const uint4*>(xrow[t] + ks);
+          bv[u][t][j] = v;
+        }
       }
     }
 #pragma unroll
@@ -148,6 +160,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
 struct RowInfo {
   int b, ih0, iw0;   // conv: sample and top-left input corner; rows: b = m
   bool valid;
+  size_t base;       // X_CONV64: element offset of (b, ih0, iw0, 0)
 };
 
 template <int MODE>
@@ -164,8 +177,38 @@ __device__ __forceinline__ RowInfo row_info(const GemmArgs& a, int m) {
     const int oh = rem / a.Wo, ow = rem - (rem / a.Wo) * a.Wo;
     ri.ih0 = oh * a.stride - a.pad;
     ri.iw0 = ow * a.stride - a.pad;
+    ri.base = (((size_t)ri.b * a.H + ri.ih0) * a.W + ri.iw0) * (size_t)a.C;
   }
   return ri;
+}
+
+// k-stage position of an X_CONV64 contraction: filter tap (kh, kw) and channel offset c0,
+// identical for every thread of the workgroup
+struct TapPos {
+  int kh, kw, c0;
+  __device__ void init(const GemmArgs& a, int k0) {
+    const int tap = k0 / a.C;
+    c0 = k0 - tap * a.C;
+    kh = tap / a.KW;
+    kw = tap - kh * a.KW;
+  }
+  __device__ void advance(const GemmArgs& a, int bk) {
+    c0 += bk;
+    if (c0 >= a.C) {
+      c0 = 0;
+      if (++kw == a.KW) {
+        kw = 0;
+        ++kh;
+      }
+    }
+  }
+};
+
+__device__ __forceinline__ uint4 load_x_tap(const GemmArgs& a, const RowInfo& ri, const TapPos& tp, int kq) {
+  const int ih = ri.ih0 + tp.kh, iw = ri.iw0 + tp.kw;
+  const bool ok = ri.valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+  const size_t off = ri.base + ((size_t)tp.kh * a.W + tp.kw) * a.C + tp.c0 + kq;
+  return mask_u4(*reinterpret_cast<const uint4*>(a.x + (ok ? off : 0)), ok);
 }
 
 template <int MODE>
@@ -196,8 +239,18 @@ __device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, i
   return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
+// weights in 16 x 128 blocks (N % 16 == 0, K % 128 == 0): element (n, k) of an 8-run
+__device__ __forceinline__ uint4 load_w8_packed(const GemmArgs& a, int n, int k) {
+  const bool ok = n < a.N && k < a.K;
+  const int nn = ok ? n : 0, kk = ok ? k : 0;
+  const size_t off = ((((size_t)(nn >> 4) * (a.K >> 7) + (kk >> 7)) * 4 + ((kk >> 5) & 3)) * 512) +
+                     ((((kk >> 3) & 3) << 4) + (nn & 15)) * 8;
+  return mask_u4(*reinterpret_cast<const uint4*>(a.w + off), ok);
+}
+
 template <bool WVEC>
 __device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
+  if (a.ep.w_packed) return load_w8_packed(a, n, k);
   const bool row_ok = n < a.N;
   const uint16_t* p = a.w + (size_t)(row_ok ? n : 0) * a.K;
   if (WVEC) {
@@ -226,6 +279,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int VA = BN / RSTEP, VB = BM / RSTEP;
   constexpr int NB = BN / 32, MB = BM / 32;     // 16 x 16 blocks per wave (wave tile BN/2 x BM/2)
   static_assert(VA >= 1 && VB >= 1 && BK % 32 == 0, "tile shape");
+  static_assert(MODE != X_CONV64 || BK == 64, "X_CONV64 steps one 64-deep stage per tap position");
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * (BN + BM) * LDK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -247,12 +301,20 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const int s0 = blockIdx.z * a.kst;
   const int s1 = min(s0 + a.kst, nst);
   uint4 ra[VA], rb[VB];
+  TapPos tap;
+  if (MODE == X_CONV64) tap.init(a, s0 * BK);
   auto load = [&](int s) {
     const int k = s * BK + kq;
 #pragma unroll
     for (int p = 0; p < VA; ++p) ra[p] = load_w8<WVEC>(a, n_base + row0 + RSTEP * p, k);
+    if (MODE == X_CONV64) {
 #pragma unroll
-    for (int p = 0; p < VB; ++p) rb[p] = load_x8<MODE>(a, ri[p], k);
+      for (int p = 0; p < VB; ++p) rb[p] = load_x_tap(a, ri[p], tap, kq);
+      tap.advance(a, BK);
+    } else {
+#pragma unroll
+      for (int p = 0; p < VB; ++p) rb[p] = load_x8<MODE>(a, ri[p], k);
+    }
   };
   auto store = [&](int buf) {
     uint16_t* As = lds + buf * (BN + BM) * LDK;
@@ -345,11 +407,12 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   const int tn = (a.N + BN - 1) / BN, tm = (a.M + BM - 1) / BM, tiles = tn * tm;
   const int nst = (a.K + BK - 1) / BK;
   int splits = 1;
-  if (sp.partials && tiles < 128) {
-    // aim for about 512 workgroups, at least 4 k-stages per split, within the scratch
+  if (sp.partials && tiles < 512) {
+    // aim for about 512 workgroups (two per CU), at least 8 k-stages per split, within
+    // the scratch
     const size_t per_split = (size_t)a.M * a.N * 4;
     int want = (512 + tiles - 1) / tiles;
-    want = min(want, max(nst / 4, 1));
+    want = min(want, max(nst / 8, 1));
     want = min(want, 16);
     while (want > 1 && per_split * want > sp.partial_bytes) --want;
     splits = max(want, 1);
@@ -382,14 +445,18 @@ bool ep_ok(const Epilogue& ep) { return ep.out != nullptr && ep.act >= 0 && ep.a
 hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N, const Epilogue& ep,
                        const Split& sp, hipStream_t s) {
   if (!x || !w || M < 1 || N < 1 || K < 8 || (K & 7) || !ep_ok(ep)) return hipErrorInvalidValue;
+  if (ep.w_packed && ((N & 15) || (K & 127))) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = x; a.w = w; a.M = M; a.N = N; a.K = K; a.ep = ep;
-  if (M <= 16) {
-    hipLaunchKernelGGL((k_gemv<1, 16>), dim3((N + 15) / 16), dim3(1024), 0, s, a);
-    return hipGetLastError();
-  }
   if (M <= 32) {
-    hipLaunchKernelGGL((k_gemv<2, 16>), dim3((N + 15) / 16), dim3(1024), 0, s, a);
+    const dim3 grid((N + 15) / 16), block(1024);
+    if (M <= 16) {
+      if (ep.w_packed) hipLaunchKernelGGL((k_gemv<1, 16, true>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((k_gemv<1, 16, false>), grid, block, 0, s, a);
+    } else {
+      if (ep.w_packed) hipLaunchKernelGGL((k_gemv<2, 16, true>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((k_gemv<2, 16, false>), grid, block, 0, s, a);
+    }
     return hipGetLastError();
   }
   return pick_tiled<X_ROWS, true>(a, sp, s);
@@ -408,6 +475,8 @@ hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16
   a.x = x; a.w = w; a.M = B * Ho * Wo; a.N = O; a.K = KH * KW * C;
   a.H = H; a.W = W; a.C = C; a.KW = KW; a.stride = stride; a.pad = pad; a.Ho = Ho; a.Wo = Wo;
   a.ep = ep;
+  a.ep.w_packed = 0;
+  if ((C & 63) == 0) return pick_tiled<X_CONV64, true>(a, sp, s);
   if ((C & 7) == 0) return pick_tiled<X_CONV8, true>(a, sp, s);
   if ((a.K & 7) == 0) return pick_tiled<X_CONV1, true>(a, sp, s);
   return pick_tiled<X_CONV1, false>(a, sp, s);

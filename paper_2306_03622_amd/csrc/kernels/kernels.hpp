@@ -19,6 +19,7 @@ struct Epilogue {
   int act = 0;                      // ACT_*
   void* out = nullptr;
   int out_f32 = 0;                  // out dtype: 0 bf16, 1 fp32
+  int w_packed = 0;                 // weights in 16 x 128 blocks (N % 16 == 0, K % 128 == 0)
 };
 
 // Scratch for splitting a contraction over k into fp32 partials (null disables splitting).

@@ -102,6 +102,7 @@ _SIGS = {
     "tp_model_chunks": [_P, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
                         C.c_uint32, C.POINTER(C.c_uint32)],
     "tp_workspace_bytes": [C.POINTER(tp_model_desc), C.c_int32, C.POINTER(C.c_uint64)],
+    "tp_model_host_image": [_P, C.c_int32, C.POINTER(_P), C.POINTER(C.c_uint64)],
     "tp_run_trace": [_P, C.POINTER(tp_request), C.c_uint32, _P, C.POINTER(tp_request_result)],
     "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
     "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
@@ -274,6 +275,15 @@ def tp_model_chunks(ctx, model_id):
     return [{"begin": b[i], "end": e[i], "first_layer": f[i]} for i in range(n.value)]
 
 
+def tp_model_host_image(ctx, model_id) -> np.ndarray:
+    """Read-only uint8 view of the library's pinned host image of a model."""
+    p, n = _P(), C.c_uint64()
+    _check(lib(), lib().tp_model_host_image(ctx, model_id, C.byref(p), C.byref(n)))
+    arr = np.ctypeslib.as_array(C.cast(p, C.POINTER(C.c_uint8)), shape=(n.value,))
+    arr.flags.writeable = False
+    return arr
+
+
 def tp_workspace_bytes(desc: ModelDesc, batch: int) -> int:
     out = C.c_uint64()
     _check(lib(), lib().tp_workspace_bytes(C.byref(desc.desc), batch, C.byref(out)))
@@ -410,6 +420,9 @@ class Runtime:
 
     def chunks(self, mid):
         return tp_model_chunks(self.ctx, mid)
+
+    def host_image(self, mid) -> np.ndarray:
+        return tp_model_host_image(self.ctx, mid)
 
     def run_trace(self, requests, stream=None):
         s = stream if stream is not None else self.torch.cuda.current_stream(self.device)

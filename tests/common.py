@@ -62,3 +62,21 @@ def check_parity(got, model, x_np, tol):
     assert np.all(np.isfinite(got)), "non-finite output"
     assert err.max() <= tol, (err.max(), tol)
     return err
+
+
+def pack_rows16x128(w: np.ndarray) -> np.ndarray:
+    """Blocked order of a bf16 [N][K] matrix used for skinny-batch MLP weights: blocks of 16
+    rows x 128 columns, each ordered [32-column group][8-column slot][row][8 elements]."""
+    n, k = w.shape
+    return w.reshape(n // 16, 16, k // 128, 4, 4, 8).transpose(0, 2, 3, 4, 1, 5).reshape(-1)
+
+
+def expected_host_image(model) -> np.ndarray:
+    """The library's pinned host image of `model` (bf16 MLPs with width % 128 == 0 are blocked)."""
+    img = model.blob().copy()
+    if model.arch == "mlp" and model.dtype == "bf16" and model.dims["width"] % 128 == 0:
+        for t in model.tensors:
+            if t.role == "w":
+                w = img[t.offset:t.offset + t.nbytes].view(np.uint16).reshape(t.shape)
+                img[t.offset:t.offset + t.nbytes] = pack_rows16x128(w).view(np.uint8)
+    return img

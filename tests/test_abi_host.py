@@ -26,7 +26,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 23, sorted(names)
+    assert len(names) == 24, sorted(names)
     L = tp.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -150,3 +150,17 @@ def test_arena_unregister_and_errors():
     ha.request(1)
     ha.unregister(1)
     assert ha.stats()["used"] == 0 and ha.stats()["registered"] == 0
+
+
+def test_blocked_layout_definition():
+    # the test-side definition of the blocked order, pinned on a small matrix by hand
+    from tests.common import pack_rows16x128
+    w = np.arange(16 * 128, dtype=np.uint16).reshape(16, 128)
+    p = pack_rows16x128(w)
+    # first 8 elements: row 0, columns 0..7; next 8: row 1, columns 0..7
+    assert p[:8].tolist() == list(range(8)) and p[8:16].tolist() == list(range(128, 136))
+    # slot q = 1 starts after 16 rows: row 0, columns 8..15
+    assert p[128:136].tolist() == list(range(8, 16))
+    # group j = 1 starts at 512: row 0, columns 32..39
+    assert p[512:520].tolist() == list(range(32, 40))
+    assert sorted(p.tolist()) == list(range(16 * 128))

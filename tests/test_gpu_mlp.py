@@ -21,7 +21,8 @@ def test_cfg1_fp32_cold_then_warm():
     warm = infer(rt, mid, m, x)
     check_parity(cold, m, x, 1e-4)
     assert np.array_equal(cold, warm)
-    # swapped bytes are the host bytes
+    # swapped bytes are the host bytes (fp32 weights are stored as registered)
+    assert np.array_equal(rt.host_image(mid), m.blob())
     assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob())
     st = rt.stats()
     assert (st["hits"], st["misses"], st["bytes_swapped"]) == (1, 1, m.total_bytes)
@@ -36,6 +37,17 @@ def test_mlp_bf16_ragged(batch):
     log(f"mlp bf16 width 200 batch {batch}")
     got = infer(rt, mid, m, x)
     check_parity(got, m, x, 2e-2)
+    rt.close()
+
+
+@pytest.mark.parametrize("batch", [1, 16, 17, 32, 33, 100])
+def test_mlp_bf16_blocked_weights(batch):
+    # width % 128 == 0: weights stored blocked; batches up to 32 take the skinny kernel,
+    # larger ones the tiled kernel, both reading the blocked layout
+    m = synth.mlp(3, 384, "bf16", "gelu", seed=17)
+    x = synth.mlp_input(batch, 384, "bf16", 300 + batch)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    check_parity(infer(rt, mid, m, x), m, x, 2e-2)
     rt.close()
 
 

@@ -8,7 +8,7 @@ import pytest
 import paper_2306_03622_amd as tp
 import synth
 from oracle.arena_sim import ArenaSim
-from tests.common import infer, log, make_runtime, out_shape, to_device, torch_dev
+from tests.common import expected_host_image, infer, log, make_runtime, out_shape, to_device, torch_dev
 
 
 def infer_shape(m):
@@ -38,7 +38,9 @@ def test_swapped_bytes_identical(method, chunk):
         rt.swap_in(mid, stream=s)
         s.synchronize()
         assert rt.resident(mid)
-        assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob()), (method, chunk, m.arch)
+        image = rt.host_image(mid)
+        assert np.array_equal(image, expected_host_image(m)), m.arch
+        assert np.array_equal(rt.extent(mid).cpu().numpy(), image), (method, chunk, m.arch)
     rt.close()
 
 
