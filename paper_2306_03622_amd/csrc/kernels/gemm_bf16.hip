@@ -86,6 +86,77 @@ __device__ __forceinline__ void store_row4(const GemmArgs& a, int m, int n0, f32
   }
 }
 
+// Epilogue of 16 consecutive outputs n0 .. n0+15 of row m (contiguous loads and stores)
+__device__ __forceinline__ void store_row16(const GemmArgs& a, int m, int n0, const float (&v_in)[16]) {
+  const Epilogue& ep = a.ep;
+  const size_t base = (size_t)m * a.N + n0;
+  if (n0 + 15 < a.N && (a.N & 7) == 0) {
+    float v[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) v[e] = v_in[e];
+    if (ep.bias) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint4 b = *reinterpret_cast<const uint4*>(ep.bias + n0 + 8 * h);
+        const uint32_t w[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[8 * h + 2 * e] += bf2f(w[e] & 0xffff);
+          v[8 * h + 2 * e + 1] += bf2f(w[e] >> 16);
+        }
+      }
+    }
+    if (ep.res) {
+      if (ep.res_f32) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(ep.res) + base + 4 * h);
+          v[4 * h] += r.x; v[4 * h + 1] += r.y; v[4 * h + 2] += r.z; v[4 * h + 3] += r.w;
+        }
+      } else {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint4 r = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(ep.res) + base + 8 * h);
+          const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[8 * h + 2 * e] += bf2f(w[e] & 0xffff);
+            v[8 * h + 2 * e + 1] += bf2f(w[e] >> 16);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) v[e] = act_apply(v[e], ep.act);
+    if (ep.out_f32) {
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        *reinterpret_cast<float4*>(static_cast<float*>(ep.out) + base + 4 * h) =
+            make_float4(v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]);
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        uint4 o;
+        o.x = (uint32_t)f2bf(v[8 * h]) | ((uint32_t)f2bf(v[8 * h + 1]) << 16);
+        o.y = (uint32_t)f2bf(v[8 * h + 2]) | ((uint32_t)f2bf(v[8 * h + 3]) << 16);
+        o.z = (uint32_t)f2bf(v[8 * h + 4]) | ((uint32_t)f2bf(v[8 * h + 5]) << 16);
+        o.w = (uint32_t)f2bf(v[8 * h + 6]) | ((uint32_t)f2bf(v[8 * h + 7]) << 16);
+        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(ep.out) + base + 8 * h) = o;
+      }
+    }
+    return;
+  }
+  for (int e = 0; e < 16 && n0 + e < a.N; ++e) {
+    float t = v_in[e];
+    if (ep.bias) t += bf2f(ep.bias[n0 + e]);
+    if (ep.res) t += ep.res_f32 ? static_cast<const float*>(ep.res)[base + e]
+                                : bf2f(static_cast<const uint16_t*>(ep.res)[base + e]);
+    t = act_apply(t, ep.act);
+    if (ep.out_f32) static_cast<float*>(ep.out)[base + e] = t;
+    else static_cast<uint16_t*>(ep.out)[base + e] = f2bf(t);
+  }
+}
+
 // ------------------------------------------------------------------ skinny M
 
 // PK: weights in 16 x 128 blocks (see pack_rows16x128 in the host code), so load j of
@@ -353,32 +424,49 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     __syncthreads();
   }
 
-  if (a.splits > 1) {
-    // fp32 partial of this split: P[split][m][n], four consecutive n per lane
-    float* part = a.partials + (size_t)blockIdx.z * a.M * a.N;
-#pragma unroll
-    for (int i = 0; i < NB; ++i)
-#pragma unroll
-      for (int j = 0; j < MB; ++j) {
-        const int m = m_base + wm * (BM / 2) + j * 16 + (lane & 15);
-        const int n = n_base + wn * (BN / 2) + i * 16 + ((lane >> 4) << 2);
-        if (m < a.M && n < a.N) {
-          const f32x4 v = acc[i][j];
-          if (n + 3 < a.N && (a.N & 3) == 0) {
-            *reinterpret_cast<float4*>(part + (size_t)m * a.N + n) = make_float4(v[0], v[1], v[2], v[3]);
-          } else {
-            for (int e = 0; e < 4 && n + e < a.N; ++e) part[(size_t)m * a.N + n + e] = v[e];
-          }
-        }
-      }
-    return;
-  }
+  // Output: the fp32 tile is staged in LDS (row-major [m][n], padded) so that each thread then
+  // handles a 16-wide run of one row with contiguous loads and stores (the accumulator layout
+  // would otherwise give 16 rows x 8 bytes per store instruction). The main loop ended with a
+  // barrier, so the LDS is free.
+  constexpr int TS = BN + 4;
+  static_assert((size_t)BM * TS * 4 <= sizeof(lds), "output tile must fit the operand buffers");
+  float* T = reinterpret_cast<float*>(lds);
 #pragma unroll
   for (int i = 0; i < NB; ++i)
 #pragma unroll
-    for (int j = 0; j < MB; ++j)
-      store_row4(a, m_base + wm * (BM / 2) + j * 16 + (lane & 15),
-                 n_base + wn * (BN / 2) + i * 16 + ((lane >> 4) << 2), acc[i][j]);
+    for (int j = 0; j < MB; ++j) {
+      const int ml = wm * (BM / 2) + j * 16 + (lane & 15);
+      const int nl = wn * (BN / 2) + i * 16 + ((lane >> 4) << 2);
+      const f32x4 v = acc[i][j];
+      *reinterpret_cast<float4*>(&T[ml * TS + nl]) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  __syncthreads();
+  constexpr int TPR = BN / 16, RPI = 256 / TPR;
+  const int nl = (tid % TPR) * 16;
+  const int n0 = n_base + nl;
+  for (int ml = tid / TPR; ml < BM; ml += RPI) {
+    const int m = m_base + ml;
+    if (m >= a.M || n0 >= a.N) continue;
+    float v[16];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const float4 t = *reinterpret_cast<const float4*>(&T[ml * TS + nl + 4 * h]);
+      v[4 * h] = t.x; v[4 * h + 1] = t.y; v[4 * h + 2] = t.z; v[4 * h + 3] = t.w;
+    }
+    if (a.splits > 1) {
+      // fp32 partial of this split: P[split][m][n]
+      float* p = a.partials + (size_t)blockIdx.z * a.M * a.N + (size_t)m * a.N + n0;
+      if (n0 + 15 < a.N && (a.N & 3) == 0) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+          *reinterpret_cast<float4*>(p + 4 * h) = make_float4(v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]);
+      } else {
+        for (int e = 0; e < 16 && n0 + e < a.N; ++e) p[e] = v[e];
+      }
+    } else {
+      store_row16(a, m, n0, v);
+    }
+  }
 }
 
 // y = epilogue(sum over splits z = 0, 1, ... of P[z]) for four consecutive outputs per thread
