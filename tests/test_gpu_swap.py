@@ -153,3 +153,25 @@ def test_arena_decisions_match_simulator():
     for key, v in sim.stats().items():
         assert got[key] == v, (key, got[key], v)
     rt.close()
+
+
+def test_single_chunk_swaps_over_previous_tenant():
+    # one chunk per model and an arena that holds one model at a time: every request swaps
+    # over the extent the previous tenant was still reading
+    ms = _models()
+    xs = _inputs(ms)
+    ref_rt, ref_ids = make_runtime(ms, batch_max=2, flags=tp.TP_FLAG_NO_GRAPH)
+    ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
+    ref_rt.close()
+    arena = max(m.total_bytes for m in ms) + 4096
+    rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, chunk_min_bytes=1 << 40)
+    torch, dev = torch_dev()
+    s = torch.cuda.Stream(device=dev)
+    for rep in range(3):
+        for k in range(3):
+            assert len(rt.chunks(ids[k])) == 1
+            got = infer(rt, ids[k], ms[k], xs[k], stream=s)
+            assert np.array_equal(got, ref[k]), (rep, k)
+            assert np.array_equal(rt.extent(ids[k]).cpu().numpy(), expected_host_image(ms[k])), (rep, k)
+    assert rt.stats()["misses"] == 9
+    rt.close()
