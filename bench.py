@@ -76,14 +76,15 @@ def link_peak(torch, dev, reps=10, nbytes=1 << 30):
 
 
 class Bench:
-    def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0):
+    def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0, flags=0):
         import paper_2306_03622_amd as tp
         self.tp, self.torch, self.dev, self.m = tp, torch, dev, model
         self.desc = tp.ModelDesc.of(model)
         ws = tp.tp_workspace_bytes(self.desc, max(batches))
-        cm = tp.TP_COPY_GATHER if method == "gather" else tp.TP_COPY_MEMCPY
+        cm = {"memcpy": tp.TP_COPY_MEMCPY, "gather": tp.TP_COPY_GATHER, "pageable": tp.TP_COPY_PAGEABLE,
+              "zero": tp.TP_COPY_ZERO}[method]
         self.rt = tp.Runtime(model.total_bytes + (1 << 20), ws, chunk_min_bytes=chunk, copy_method=cm,
-                             copy_streams=copy_streams)
+                             copy_streams=copy_streams, flags=flags)
         self.mid = self.rt.register(self.desc, model.blob())
         self.stream = torch.cuda.Stream(device=dev)
 
@@ -175,6 +176,55 @@ def elbow_sweep(torch, dev, method, copy_streams=0, sizes=(256 << 10, 512 << 10,
     best = max(r["swap_gbs"] for r in rows)
     elbow = next(r["chunk_min_bytes"] for r in rows if r["swap_gbs"] >= 0.95 * best)
     return {"model": "256 x 512 bf16 MLP (512 KiB per layer)", "rows": rows, "elbow_bytes": elbow}
+
+
+# Swap designs of the breakdown (Sec. 6.1, "Performance breakdown of model swapping"), each
+# changing one thing from the row above, then the alternatives the library also offers.
+# (name, copy method, group size or None for the default, flags, copy streams)
+ABLATION = (
+    ("baseline: pageable copy per tensor, then execute", "pageable", 0, "serial|per_tensor", 1),
+    ("pinned: pinned copy per tensor, then execute", "memcpy", 0, "serial|per_tensor", 1),
+    ("pipeline: per-tensor transfers overlapped with execution", "memcpy", 0, "per_tensor", 1),
+    ("group: tensors grouped to >= G, overlapped", "memcpy", None, "per_tensor", 1),
+    ("group by layer: whole layers grouped to >= G (library default)", "memcpy", None, "", 1),
+    ("gather kernel instead of the copy engine, grouped by layer", "gather", None, "", 1),
+    ("two copy streams, grouped by layer", "memcpy", None, "", 2),
+    ("direct host access: kernels read the pinned host copy", "zero", None, "", 1),
+)
+
+
+def ablation(torch, dev, chunk, budget_s=2.5, max_reps=20):
+    """Cold p50 of every swap design on the single-GPU workloads (batch 8, and batch 1 for
+    the 1 MB MLP). A design is timed until max_reps cold requests or budget_s seconds."""
+    import synth
+    import paper_2306_03622_amd as tp
+    bits = {"serial": tp.TP_FLAG_SERIAL, "per_tensor": tp.TP_FLAG_PER_TENSOR}
+    out = {}
+    for cfg, bt in ((1, 1), (2, 8), (3, 8), (4, 8)):
+        m = synth.config_model(cfg)
+        m.blob()
+        rows = []
+        ref = None
+        for name, method, g, fl, ns in ABLATION:
+            flags = 0
+            for f in filter(None, fl.split("|")):
+                flags |= bits[f]
+            log(f"ablation cfg{cfg} b{bt}: {name}")
+            b = Bench(torch, dev, m, [bt], method, chunk if g is None else g, ns, flags)
+            x, y = b.io(bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt))
+            b.request(x, y, cold=True)
+            got = y.cpu()
+            same = bool(torch.equal(got, ref)) if ref is not None else True
+            ref = got if ref is None else ref
+            times, t_start = [], time.perf_counter()
+            while len(times) < max_reps and time.perf_counter() - t_start < budget_s:
+                times.append(b.request(x, y, cold=True))
+            rows.append({"design": name, "cold_p50_ms": round(p50(times), 3), "runs": len(times),
+                         "chunks": len(b.rt.chunks(b.mid)), "bitwise_equal_to_first": same})
+            b.close()
+        out[f"cfg{cfg}_b{bt}"] = {"weight_bytes": m.total_bytes, "designs": rows}
+        m.drop_blob()
+    return out
 
 
 def tenants(torch, dev, n_requests, n_models, arena_gib, workers):
@@ -316,6 +366,8 @@ def main():
                     help="run only a fixed workload for hardware-counter passes: 20 warm forwards of the "
                          "bench model, then one 256 MiB device-to-device copy (the byte-count calibration)")
     ap.add_argument("--full", action="store_true", help="also time the other batches and workloads")
+    ap.add_argument("--ablation", action="store_true",
+                    help="time the cold request under every swap design instead (breakdown table)")
     ap.add_argument("--no-cpu", action="store_true")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -333,6 +385,13 @@ def main():
 
     if a.tenants:
         print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16)), flush=True)
+        return
+
+    if a.ablation:
+        import paper_2306_03622_amd as tp
+        link = link_peak(torch, dev)
+        print(json.dumps({"ablation": ablation(torch, dev, tp.DEFAULT_CHUNK), "link_peak_gbs": round(link, 2),
+                          "group_bytes": tp.DEFAULT_CHUNK}), flush=True)
         return
 
     if a.pmc_workload:

@@ -87,11 +87,24 @@ typedef struct {
   const tp_tensor_desc* tensors;
 } tp_model_desc;
 
-enum { TP_COPY_MEMCPY = 0, TP_COPY_GATHER = 1 };
+/* How a chunk reaches the arena. MEMCPY and GATHER are the swap engines of the pipelined
+ * path. PAGEABLE and ZERO exist for the swap-design breakdown of Sec. 6.1 ("Performance
+ * breakdown of model swapping") and the direct-host-access alternative of Sec. 8 (related
+ * work): PAGEABLE copies from an ordinary pageable copy of the weights that the library
+ * keeps beside the pinned one (the baseline that the pinned pool improves on); ZERO
+ * never copies: a request for a non-resident model runs its kernels on the weights in
+ * the pinned host copy, read over the host link, and leaves the model non-resident
+ * (tp_swap_in still makes it resident; the arena's counters see no ZERO request). */
+enum { TP_COPY_MEMCPY = 0, TP_COPY_GATHER = 1, TP_COPY_PAGEABLE = 2, TP_COPY_ZERO = 3 };
 enum {
-  TP_FLAG_POISON = 1,    /* evicted extents are filled with 0xFF (NaN for fp32/bf16) */
-  TP_FLAG_THROTTLE = 2,  /* a bounded delay kernel precedes every chunk on the copy stream */
-  TP_FLAG_NO_GRAPH = 4   /* launch warm requests kernel by kernel instead of replaying a graph */
+  TP_FLAG_POISON = 1,     /* evicted extents are filled with 0xFF (NaN for fp32/bf16) */
+  TP_FLAG_THROTTLE = 2,   /* a bounded delay kernel precedes every chunk on the copy stream */
+  TP_FLAG_NO_GRAPH = 4,   /* launch warm requests kernel by kernel instead of replaying a graph */
+  TP_FLAG_SERIAL = 8,     /* a cold request waits for its whole model before its first kernel
+                           * (swap, then execute: no pipelining) */
+  TP_FLAG_PER_TENSOR = 16 /* transfer groups close at tensor boundaries, not layer boundaries;
+                           * with chunk_min_bytes = 0 every tensor is its own transfer (the
+                           * parameter-level pipeline of Sec. 6.1) */
 };
 
 /* Context configuration. arena_dev/work_dev are caller-owned device buffers that must

@@ -25,8 +25,9 @@ extern "C" {
 /* Validates a descriptor exactly as tp_register_model does. */
 TP_API tp_status tph_validate(const tp_model_desc* desc, uint64_t host_bytes);
 
-/* Chunk plan for group size chunk_min_bytes; same outputs as tp_model_chunks. */
-TP_API tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes,
+/* Chunk plan for group size chunk_min_bytes under context flags `flags` (only
+ * TP_FLAG_PER_TENSOR matters); same outputs as tp_model_chunks. */
+TP_API tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes, int32_t flags,
                    uint64_t* begin, uint64_t* end, uint32_t* first_layer, uint32_t cap, uint32_t* n);
 
 struct tph_arena;

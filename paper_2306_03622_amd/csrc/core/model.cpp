@@ -206,12 +206,12 @@ void pack_rows16x128(const uint16_t* src, uint16_t* dst, int64_t N, int64_t K) {
     }
 }
 
-std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes) {
-  // per-layer byte spans in first-use order
+std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes, bool per_tensor) {
+  // byte spans in first-use order: one per layer, or one per tensor
   struct Span { uint32_t layer; uint64_t begin, end; };
   std::vector<Span> spans;
   for (const auto& t : m.tensors) {
-    if (!spans.empty() && spans.back().layer == t.layer) spans.back().end = t.offset + t.bytes;
+    if (!per_tensor && !spans.empty() && spans.back().layer == t.layer) spans.back().end = t.offset + t.bytes;
     else spans.push_back({t.layer, t.offset, t.offset + t.bytes});
   }
   std::vector<Chunk> out;

@@ -50,9 +50,11 @@ struct ModelSpec {
 // TP_E_INVAL with a message in *err.
 tp_status validate_model(const tp_model_desc* d, uint64_t host_bytes, ModelSpec* out, std::string* err);
 
-// Greedy grouping in first-use order: whole layers only; a chunk is closed at the first
-// layer boundary where it holds >= min_bytes. Chunks tile [0, host_bytes).
-std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes);
+// Greedy grouping in first-use order: whole layers (or, with per_tensor, whole tensors); a
+// chunk is closed at the first layer (tensor) boundary where it holds >= min_bytes. Chunks
+// tile [0, host_bytes). With per_tensor a layer may span several chunks: first_layer and
+// last_layer are the layers of a chunk's first and last tensor.
+std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes, bool per_tensor = false);
 
 // Activation buffers of the executors for `batch` samples (each buffer 256-aligned).
 uint64_t activation_bytes(const ModelSpec& m, int32_t batch);

@@ -22,14 +22,14 @@ tp_status tph_validate(const tp_model_desc* desc, uint64_t host_bytes) {
   return s == TP_OK ? ok() : fail(s, err);
 }
 
-tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes, uint64_t* begin,
-                   uint64_t* end, uint32_t* first_layer, uint32_t cap, uint32_t* n) {
+tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes, int32_t flags,
+                   uint64_t* begin, uint64_t* end, uint32_t* first_layer, uint32_t cap, uint32_t* n) {
   ModelSpec m;
   std::string err;
   tp_status s = validate_model(desc, host_bytes, &m, &err);
   if (s != TP_OK) return fail(s, err);
   if (!n) return fail(TP_E_INVAL, "tph_plan: n is NULL");
-  const auto plan = plan_chunks(m, chunk_min_bytes);
+  const auto plan = plan_chunks(m, chunk_min_bytes, (flags & TP_FLAG_PER_TENSOR) != 0);
   *n = (uint32_t)plan.size();
   for (uint32_t i = 0; i < plan.size() && i < cap; ++i) {
     if (begin) begin[i] = plan[i].begin;

@@ -119,6 +119,8 @@ hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
   if (e == hipSuccess) {
     if (c->cfg.copy_method == TP_COPY_GATHER)
       e = k::gather_copy(static_cast<char*>(m->host_dev) + ch.begin, dst, nb, c->cfg.gather_wgs, s);
+    else if (c->cfg.copy_method == TP_COPY_PAGEABLE)
+      e = hipMemcpyAsync(dst, m->pageable.get() + ch.begin, nb, hipMemcpyHostToDevice, s);
     else
       e = hipMemcpyAsync(dst, static_cast<char*>(m->host) + ch.begin, nb, hipMemcpyHostToDevice, s);
   }
@@ -246,7 +248,7 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   if ((uintptr_t)cfg->arena_dev % 256) return fail(TP_E_INVAL, "tp_create: arena must be 256-byte aligned");
   if (cfg->work_bytes && (!cfg->work_dev || (uintptr_t)cfg->work_dev % 256))
     return fail(TP_E_INVAL, "tp_create: workspace must be non-NULL and 256-byte aligned");
-  if (cfg->copy_method != TP_COPY_MEMCPY && cfg->copy_method != TP_COPY_GATHER)
+  if (cfg->copy_method < TP_COPY_MEMCPY || cfg->copy_method > TP_COPY_ZERO)
     return fail(TP_E_INVAL, "tp_create: unknown copy_method");
   if (cfg->gather_wgs < 0 || cfg->gather_wgs > 4096 || cfg->throttle_us < 0 || cfg->throttle_us > 100000)
     return fail(TP_E_INVAL, "tp_create: gather_wgs or throttle_us out of range");
@@ -301,7 +303,7 @@ tp_status tp_register_model(tp_ctx* c, const tp_model_desc* desc, const void* ho
   tp_status s = validate_model(desc, host_bytes, &m->spec, &err);
   if (s != TP_OK) return fail(s, err);
   m->id = c->next_id;
-  m->chunks = plan_chunks(m->spec, c->cfg.chunk_min_bytes);
+  m->chunks = plan_chunks(m->spec, c->cfg.chunk_min_bytes, (c->cfg.flags & TP_FLAG_PER_TENSOR) != 0);
   m->chunk_of_layer.assign(m->spec.n_layers, 0);
   for (size_t i = 0; i < m->chunks.size(); ++i)
     for (uint32_t l = m->chunks[i].first_layer; l <= m->chunks[i].last_layer; ++l) m->chunk_of_layer[l] = (uint32_t)i;
@@ -324,6 +326,14 @@ tp_status tp_register_model(tp_ctx* c, const tp_model_desc* desc, const void* ho
         }
       });
     for (auto& t : th) t.join();
+  }
+  if (c->cfg.copy_method == TP_COPY_PAGEABLE) {
+    m->pageable.reset(new (std::nothrow) char[nb]);
+    if (!m->pageable) {
+      free_model(m.get());
+      return fail(TP_E_NOSPC, "out of host memory (pageable model copy)");
+    }
+    std::memcpy(m->pageable.get(), m->host, nb);
   }
   e = hipHostGetDevicePointer(&m->host_dev, m->host, 0);
   m->chunk_ev.assign(m->chunks.size(), nullptr);
@@ -372,6 +382,19 @@ tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, 
                                 std::to_string(need));
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   if ((s = begin_request(c, stream)) != TP_OK) return s;
+  if (c->cfg.copy_method == TP_COPY_ZERO && !c->policy->resident(id)) {
+    // direct host access: the kernels read the weights from the pinned host copy
+    Waiter w;
+    w.m = m;
+    ExecCtx x{m, static_cast<char*>(m->host_dev), c->work, input_dev, output_dev, batch, stream, &w,
+              make_split(c, m, batch)};
+    hipError_t e = run_forward(x);
+    if (e != hipSuccess) {
+      (void)end_request(c, m, stream);
+      return hip_fail(e, "tp_infer: kernel launch");
+    }
+    return end_request(c, m, stream);
+  }
   bool swapped = false;
   if ((s = admit(c, m, &swapped)) != TP_OK) return s;
   const uint64_t off = c->policy->offset(id);
@@ -386,7 +409,9 @@ tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, 
     w.ctx = c;
     w.base_off = off;
     ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w, make_split(c, m, batch)};
-    e = run_forward(x);
+    // swap, then execute: every chunk is waited for before the first kernel
+    if (swapped && (c->cfg.flags & TP_FLAG_SERIAL)) e = w.need(m->spec.n_layers - 1);
+    if (e == hipSuccess) e = run_forward(x);
     // every layer asks for its chunk; issue any the forward pass did not reach
     if (e == hipSuccess && swapped) e = w.issue_through((int)m->chunks.size() - 1);
   }

@@ -33,6 +33,7 @@ struct Model {
   std::vector<uint32_t> chunk_of_layer;
   void* host = nullptr;          // pinned, device-mapped copy of the weights
   void* host_dev = nullptr;      // its device-visible address
+  std::unique_ptr<char[]> pageable;  // ordinary host copy (TP_COPY_PAGEABLE contexts only)
   std::vector<hipEvent_t> chunk_ev;
   hipEvent_t last_use = nullptr;
   bool used = false;             // last_use has been recorded at least once

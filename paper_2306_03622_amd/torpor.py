@@ -23,8 +23,8 @@ TP_OK, TP_E_INVAL, TP_E_NOENT, TP_E_NOSPC, TP_E_HIP, TP_E_STATE = 0, -1, -2, -3,
 TP_F32, TP_BF16 = 0, 1
 TP_ARCH_MLP, TP_ARCH_RESNET50, TP_ARCH_BERT = 0, 1, 2
 TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
-TP_COPY_MEMCPY, TP_COPY_GATHER = 0, 1
-TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH = 1, 2, 4
+TP_COPY_MEMCPY, TP_COPY_GATHER, TP_COPY_PAGEABLE, TP_COPY_ZERO = 0, 1, 2, 3
+TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR = 1, 2, 4, 8, 16
 ROLES = {
     "w": 0, "b": 1,
     "tok_emb": 10, "pos_emb": 11, "type_emb": 12, "emb_ln_g": 13, "emb_ln_b": 14,
@@ -105,7 +105,7 @@ _SIGS = {
     "tp_model_host_image": [_P, C.c_int32, C.POINTER(_P), C.POINTER(C.c_uint64)],
     "tp_run_trace": [_P, C.POINTER(tp_request), C.c_uint32, _P, C.POINTER(tp_request_result)],
     "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
-    "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+    "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                  C.POINTER(C.c_uint32), C.c_uint32, C.POINTER(C.c_uint32)],
     "tph_arena_create": [C.c_uint64, C.c_uint64, C.POINTER(_P)],
     "tph_arena_destroy": [_P],
@@ -313,12 +313,12 @@ def tph_validate(desc: ModelDesc, host_bytes: int, L=None):
     _check(L, L.tph_validate(C.byref(desc.desc), host_bytes))
 
 
-def tph_plan(desc: ModelDesc, host_bytes: int, chunk_min_bytes: int, L=None):
+def tph_plan(desc: ModelDesc, host_bytes: int, chunk_min_bytes: int, flags: int = 0, L=None):
     L = L or lib()
     n = C.c_uint32()
-    _check(L, L.tph_plan(C.byref(desc.desc), host_bytes, chunk_min_bytes, None, None, None, 0, C.byref(n)))
+    _check(L, L.tph_plan(C.byref(desc.desc), host_bytes, chunk_min_bytes, flags, None, None, None, 0, C.byref(n)))
     b, e, f = (C.c_uint64 * n.value)(), (C.c_uint64 * n.value)(), (C.c_uint32 * n.value)()
-    _check(L, L.tph_plan(C.byref(desc.desc), host_bytes, chunk_min_bytes, b, e, f, n.value, C.byref(n)))
+    _check(L, L.tph_plan(C.byref(desc.desc), host_bytes, chunk_min_bytes, flags, b, e, f, n.value, C.byref(n)))
     return [{"begin": b[i], "end": e[i], "first_layer": f[i]} for i in range(n.value)]
 
 

@@ -89,11 +89,13 @@ def test_validation_accepts_all_workloads():
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
 @pytest.mark.parametrize("g", [0, 64 << 10, 2 << 20, 16 << 20, 1 << 40])
-def test_chunk_plan_matches_reference(cfg, g):
+@pytest.mark.parametrize("per_tensor", [False, True])
+def test_chunk_plan_matches_reference(cfg, g, per_tensor):
     m = synth.config_model(cfg)
-    want = ref_chunks.plan([(t.layer, t.offset, t.nbytes) for t in m.tensors], m.total_bytes, g)
+    want = ref_chunks.plan([(t.layer, t.offset, t.nbytes) for t in m.tensors], m.total_bytes, g, per_tensor)
+    flags = tp.TP_FLAG_PER_TENSOR if per_tensor else 0
     for L in (tp.lib(), tp.host_lib()):
-        got = tp.tph_plan(tp.ModelDesc.of(m), m.total_bytes, g, L=L)
+        got = tp.tph_plan(tp.ModelDesc.of(m), m.total_bytes, g, flags, L=L)
         assert [(c["begin"], c["end"], c["first_layer"]) for c in got] == \
             [(c["begin"], c["end"], c["first_layer"]) for c in want]
 

@@ -175,3 +175,44 @@ def test_single_chunk_swaps_over_previous_tenant():
             assert np.array_equal(rt.extent(ids[k]).cpu().numpy(), expected_host_image(ms[k])), (rep, k)
     assert rt.stats()["misses"] == 9
     rt.close()
+
+
+# the swap designs of the breakdown: every one computes the same bits as the default
+ABLATION = {
+    "pageable-serial-per-tensor": dict(copy_method=tp.TP_COPY_PAGEABLE, chunk_min_bytes=0,
+                                       flags=tp.TP_FLAG_SERIAL | tp.TP_FLAG_PER_TENSOR),
+    "pinned-serial-per-tensor": dict(chunk_min_bytes=0, flags=tp.TP_FLAG_SERIAL | tp.TP_FLAG_PER_TENSOR),
+    "pipelined-per-tensor": dict(chunk_min_bytes=0, flags=tp.TP_FLAG_PER_TENSOR),
+    "grouped-by-tensor": dict(chunk_min_bytes=96 << 10, flags=tp.TP_FLAG_PER_TENSOR),
+    "pageable-pipelined": dict(copy_method=tp.TP_COPY_PAGEABLE, chunk_min_bytes=96 << 10),
+    "zero-copy": dict(copy_method=tp.TP_COPY_ZERO),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ABLATION))
+def test_swap_designs_compute_the_same_bits(name):
+    ms = _models()
+    xs = _inputs(ms)
+    ref_rt, ref_ids = make_runtime(ms, batch_max=2, flags=tp.TP_FLAG_NO_GRAPH)
+    ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
+    ref_rt.close()
+    arena = max(m.total_bytes for m in ms) + 4096       # one model at a time
+    rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, **ABLATION[name])
+    zero = ABLATION[name].get("copy_method") == tp.TP_COPY_ZERO
+    for rep in range(2):
+        for k in range(3):
+            log(f"{name}: rep {rep} {ms[k].arch}")
+            got = infer(rt, ids[k], ms[k], xs[k])
+            assert np.array_equal(got, ref[k]), (name, rep, k)
+            if zero:
+                assert not rt.resident(ids[k])
+            else:
+                assert np.array_equal(rt.extent(ids[k]).cpu().numpy(), expected_host_image(ms[k])), (name, rep, k)
+    st = rt.stats()
+    assert st["misses"] == (0 if zero else 6) and st["hits"] == 0
+    if zero:
+        # an explicit swap-in still makes the model resident; the request then hits
+        rt.swap_in(ids[0])
+        got = infer(rt, ids[0], ms[0], xs[0])
+        assert np.array_equal(got, ref[0]) and rt.stats()["hits"] == 1
+    rt.close()

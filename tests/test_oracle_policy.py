@@ -74,6 +74,18 @@ def test_chunk_plan_hand_worked():
     assert one == [{"begin": 0, "end": 1024, "first_layer": 0, "last_layer": 3}]
     per_layer = chunks.plan(t, 1024, 0)
     assert [c["first_layer"] for c in per_layer] == [0, 1, 2, 3]
+    # tensor granularity: layer 0's two tensors become separate transfers at G = 0, and
+    # at G = 120 the first group closes inside layer 1's predecessor boundary rules
+    per_tensor = chunks.plan(t, 1024, 0, per_tensor=True)
+    assert [(c["begin"], c["end"], c["first_layer"], c["last_layer"]) for c in per_tensor] == [
+        (0, 64, 0, 0), (64, 128, 0, 0), (128, 256, 1, 1), (256, 768, 2, 2), (768, 1024, 3, 3)]
+    # G = 90: 60 + 36 closes after layer 0's second tensor; 50 B of layer 1 alone stays
+    # open until layer 2's 300 B join it
+    assert [(c["begin"], c["end"], c["first_layer"], c["last_layer"]) for c in chunks.plan(t, 1024, 90, per_tensor=True)] == [
+        (0, 128, 0, 0), (128, 768, 1, 2), (768, 1024, 3, 3)]
+    # G = 50: the 60 B tensor closes a group by itself, so layer 0 spans two transfers
+    assert [(c["begin"], c["end"], c["first_layer"], c["last_layer"]) for c in chunks.plan(t, 1024, 50, per_tensor=True)] == [
+        (0, 64, 0, 0), (64, 256, 0, 1), (256, 768, 2, 2), (768, 1024, 3, 3)]
 
 
 def test_chunk_plans_of_workloads():
@@ -87,3 +99,8 @@ def test_chunk_plans_of_workloads():
     assert len(p4) == 13 and p4[0]["end"] == 47_674_368
     p3 = plan(3, 2 << 20)
     assert p3[-1]["first_layer"] <= 53 and sum(c["end"] - c["begin"] for c in p3) == synth.config_model(3).total_bytes
+    # one transfer per tensor: 53 conv weights + 53 biases + FC weight and bias
+    m3 = synth.config_model(3)
+    pt = chunks.plan([(x.layer, x.offset, x.nbytes) for x in m3.tensors], m3.total_bytes, 0, per_tensor=True)
+    assert len(pt) == len(m3.tensors) == 108
+    assert [c["begin"] for c in pt[1:]] == [x.offset for x in m3.tensors[1:]]
