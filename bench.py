@@ -76,7 +76,7 @@ def link_peak(torch, dev, reps=10, nbytes=1 << 30):
 
 
 class Bench:
-    def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0, flags=0):
+    def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0, flags=0, direct=None):
         import paper_2306_03622_amd as tp
         self.tp, self.torch, self.dev, self.m = tp, torch, dev, model
         self.desc = tp.ModelDesc.of(model)
@@ -84,7 +84,8 @@ class Bench:
         cm = {"memcpy": tp.TP_COPY_MEMCPY, "gather": tp.TP_COPY_GATHER, "pageable": tp.TP_COPY_PAGEABLE,
               "zero": tp.TP_COPY_ZERO}[method]
         self.rt = tp.Runtime(model.total_bytes + (1 << 20), ws, chunk_min_bytes=chunk, copy_method=cm,
-                             copy_streams=copy_streams, flags=flags)
+                             copy_streams=copy_streams, flags=flags,
+                             direct_max_bytes=tp.DEFAULT_DIRECT if direct is None else direct)
         self.mid = self.rt.register(self.desc, model.blob())
         self.stream = torch.cuda.Stream(device=dev)
 
@@ -180,16 +181,18 @@ def elbow_sweep(torch, dev, method, copy_streams=0, sizes=(256 << 10, 512 << 10,
 
 # Swap designs of the breakdown (Sec. 6.1, "Performance breakdown of model swapping"), each
 # changing one thing from the row above, then the alternatives the library also offers.
-# (name, copy method, group size or None for the default, flags, copy streams)
+# (name, copy method, group size or None for the default, flags, copy streams, direct-access
+# size limit)
 ABLATION = (
-    ("baseline: pageable copy per tensor, then execute", "pageable", 0, "serial|per_tensor", 1),
-    ("pinned: pinned copy per tensor, then execute", "memcpy", 0, "serial|per_tensor", 1),
-    ("pipeline: per-tensor transfers overlapped with execution", "memcpy", 0, "per_tensor", 1),
-    ("group: tensors grouped to >= G, overlapped", "memcpy", None, "per_tensor", 1),
-    ("group by layer: whole layers grouped to >= G (library default)", "memcpy", None, "", 1),
-    ("gather kernel instead of the copy engine, grouped by layer", "gather", None, "", 1),
-    ("two copy streams, grouped by layer", "memcpy", None, "", 2),
-    ("direct host access: kernels read the pinned host copy", "zero", None, "", 1),
+    ("baseline: pageable copy per tensor, then execute", "pageable", 0, "serial|per_tensor", 1, 0),
+    ("pinned: pinned copy per tensor, then execute", "memcpy", 0, "serial|per_tensor", 1, 0),
+    ("pipeline: per-tensor transfers overlapped with execution", "memcpy", 0, "per_tensor", 1, 0),
+    ("group: tensors grouped to >= G, overlapped", "memcpy", None, "per_tensor", 1, 0),
+    ("group by layer: whole layers grouped to >= G", "memcpy", None, "", 1, 0),
+    ("gather kernel instead of the copy engine, grouped by layer", "gather", None, "", 1, 0),
+    ("two copy streams, grouped by layer", "memcpy", None, "", 2, 0),
+    ("zero-copy: kernels read the pinned host copy, never resident", "zero", None, "", 1, 0),
+    ("direct access first, swap behind it (default for models <= 2 MiB)", "memcpy", None, "", 1, 1 << 62),
 )
 
 
@@ -205,12 +208,12 @@ def ablation(torch, dev, chunk, budget_s=2.5, max_reps=20):
         m.blob()
         rows = []
         ref = None
-        for name, method, g, fl, ns in ABLATION:
+        for name, method, g, fl, ns, direct in ABLATION:
             flags = 0
             for f in filter(None, fl.split("|")):
                 flags |= bits[f]
             log(f"ablation cfg{cfg} b{bt}: {name}")
-            b = Bench(torch, dev, m, [bt], method, chunk if g is None else g, ns, flags)
+            b = Bench(torch, dev, m, [bt], method, chunk if g is None else g, ns, flags, direct)
             x, y = b.io(bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt))
             b.request(x, y, cold=True)
             got = y.cpu()
@@ -510,7 +513,8 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"24-layer MLP, hidden 4096, bf16 weights (805,502,976 B) swapped cold from pinned "
                                f"host memory, batch {B}", "batch": B, "copy_method": method,
-                   "chunk_min_bytes": a.chunk, "copy_streams": a.copy_streams or 1},
+                   "chunk_min_bytes": a.chunk, "copy_streams": a.copy_streams or 1,
+                   "direct_max_bytes": tp.DEFAULT_DIRECT},
         "bound_ms": round(bound, 3), "cold_over_bound": round(cold_p50 / bound, 4),
         "swap_gbs": round(swap_gbs, 2), "link_peak_gbs": round(link, 2), "link_theoretical_gbs": PCIE5_X16_GBS,
         "warm_p50_ms": round(warm_p50, 4), "roofline": roofline, "cpu_baseline": cpu, "elbow_sweep": sweep,

@@ -116,9 +116,16 @@ enum {
  * chunk_min_bytes is the transfer group size G (0 = one chunk per layer). copy_method:
  * TP_COPY_MEMCPY uses hipMemcpyAsync; TP_COPY_GATHER runs a copy kernel reading
  * host-mapped pinned memory with gather_wgs workgroups (0 = default). throttle_us:
- * delay per chunk under TP_FLAG_THROTTLE. Warm requests replay an instantiated HIP
- * graph of the forward pass, cached per (model, batch, input, output) unless
- * TP_FLAG_NO_GRAPH is set. */
+ * delay per chunk under TP_FLAG_THROTTLE. Warm requests of models whose forward pass
+ * launches at least 16 kernels replay an instantiated HIP graph of it, cached per (model,
+ * batch, input, output), unless TP_FLAG_NO_GRAPH is set; shorter forward passes are
+ * launched kernel by kernel, which is faster for them. direct_max_bytes (0 = never): a cold request for a model of
+ * at most this many bytes runs its kernels on the pinned host copy over the host link
+ * (direct host access, the alternative to swapping that Sec. 8 cites) instead of waiting
+ * for its first chunk, and the copy stream swaps the model in behind it; the next request
+ * for the model waits for that swap. This removes the copy engine's start-up and hand-off
+ * latency from the cold path of models small enough that it dominates. It applies with
+ * one copy stream and copy_method TP_COPY_MEMCPY or TP_COPY_GATHER only. */
 typedef struct {
   void* arena_dev;
   uint64_t arena_bytes;
@@ -131,6 +138,7 @@ typedef struct {
   int32_t flags;
   int32_t throttle_us;
   int32_t copy_streams;
+  uint64_t direct_max_bytes;
 } tp_config;
 
 typedef struct {

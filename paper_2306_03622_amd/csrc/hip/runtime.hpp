@@ -37,6 +37,8 @@ struct Model {
   std::vector<hipEvent_t> chunk_ev;
   hipEvent_t last_use = nullptr;
   bool used = false;             // last_use has been recorded at least once
+  bool bg_pending = false;       // swapped in behind a direct-access request: the next
+                                 // request must wait for the last chunk's event
   std::vector<GraphEntry> graphs;
   bool graph_failed = false;     // capture failed once: launch this model kernel by kernel
 };

@@ -33,6 +33,10 @@ ROLES = {
 }
 # transfer group size G (whole layers per chunk, closed once a chunk holds >= G bytes)
 DEFAULT_CHUNK = 8 << 20
+# cold requests of models up to this size read their weights over the host link directly
+# (the swap runs behind them): below it the copy engine's fixed start-up and hand-off
+# latency costs more than direct reads
+DEFAULT_DIRECT = 2 << 20
 ARCHS = {"mlp": TP_ARCH_MLP, "resnet50": TP_ARCH_RESNET50, "bert": TP_ARCH_BERT}
 DTYPES = {"f32": TP_F32, "bf16": TP_BF16}
 
@@ -51,7 +55,7 @@ class tp_config(C.Structure):
     _fields_ = [("arena_dev", C.c_void_p), ("arena_bytes", C.c_uint64), ("work_dev", C.c_void_p),
                 ("work_bytes", C.c_uint64), ("copy_stream", C.c_void_p), ("chunk_min_bytes", C.c_uint64),
                 ("copy_method", C.c_int32), ("gather_wgs", C.c_int32), ("flags", C.c_int32),
-                ("throttle_us", C.c_int32), ("copy_streams", C.c_int32)]
+                ("throttle_us", C.c_int32), ("copy_streams", C.c_int32), ("direct_max_bytes", C.c_uint64)]
 
 
 class tp_arena_stats_t(C.Structure):
@@ -212,10 +216,10 @@ class ModelDesc:
 # ------------------------------------------------------------------ C calls
 
 def tp_create(arena_dev, arena_bytes, work_dev, work_bytes, copy_stream=None, chunk_min_bytes=DEFAULT_CHUNK,
-              copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0, copy_streams=0):
+              copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0, copy_streams=0, direct_max_bytes=0):
     L = lib()
     cfg = tp_config(_ptr(arena_dev), arena_bytes, _ptr(work_dev), work_bytes, _ptr(copy_stream), chunk_min_bytes,
-                    copy_method, gather_wgs, flags, throttle_us, copy_streams)
+                    copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes)
     ctx = _P()
     _check(L, L.tp_create(C.byref(cfg), C.byref(ctx)))
     return ctx
@@ -363,7 +367,7 @@ class Runtime:
 
     def __init__(self, arena_bytes: int, work_bytes: int, device: int = 0, chunk_min_bytes: int = DEFAULT_CHUNK,
                  copy_method: int = TP_COPY_MEMCPY, gather_wgs: int = 0, flags: int = 0, throttle_us: int = 0,
-                 copy_stream=None, copy_streams: int = 0):
+                 copy_stream=None, copy_streams: int = 0, direct_max_bytes: int = DEFAULT_DIRECT):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("libtorpor needs a HIP device")
@@ -374,7 +378,7 @@ class Runtime:
         self.work = torch.empty(max(work_bytes, 256), dtype=torch.uint8, device=self.device)
         self.copy_stream = copy_stream
         self.ctx = tp_create(self.arena, arena_bytes, self.work, self.work.numel(), copy_stream, chunk_min_bytes,
-                             copy_method, gather_wgs, flags, throttle_us, copy_streams)
+                             copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes)
         self.descs = {}
 
     def close(self):

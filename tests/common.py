@@ -38,6 +38,7 @@ def make_runtime(models, batch_max=1, arena_bytes=None, **kw):
     ws = max(tp.tp_workspace_bytes(d, batch_max) for d in descs)
     if arena_bytes is None:
         arena_bytes = sum(m.total_bytes for m in models) + (1 << 20)
+    kw.setdefault("direct_max_bytes", 0)        # cold requests take the swap path unless a test asks
     rt = tp.Runtime(arena_bytes, ws, **kw)
     ids = [rt.register(d, m.blob()) for d, m in zip(descs, models)]
     return rt, ids

@@ -65,7 +65,10 @@ def test_pipelined_equals_preloaded(method, streams):
 
 
 def test_warm_graph_replay_equals_kernel_by_kernel():
-    ms = _models()
+    # every family with a forward pass long enough (>= 16 launches) to be replayed as a graph
+    ms = [synth.mlp(18, 256, "bf16", "gelu", seed=61),
+          synth.bert(seed=62, layers=3, d=128, heads=2, ffn=256, seq=64, vocab=500, maxpos=64),
+          synth.resnet50(seed=63, classes=10, image=32)]
     torch, dev = torch_dev()
     eager_rt, eager_ids = make_runtime(ms, batch_max=3, flags=tp.TP_FLAG_NO_GRAPH)
     rt, ids = make_runtime(ms, batch_max=3)
@@ -215,4 +218,31 @@ def test_swap_designs_compute_the_same_bits(name):
         rt.swap_in(ids[0])
         got = infer(rt, ids[0], ms[0], xs[0])
         assert np.array_equal(got, ref[0]) and rt.stats()["hits"] == 1
+    rt.close()
+
+
+@pytest.mark.parametrize("flags", [0, tp.TP_FLAG_NO_GRAPH])
+def test_direct_access_then_background_swap(flags):
+    # cold requests read the pinned host copy; the swap runs behind them with a ~200 us
+    # delay per chunk and evicted extents poisoned, so a later request that did not wait
+    # for the swap would read NaN bytes
+    ms = _models()
+    xs = _inputs(ms)
+    ref_rt, ref_ids = make_runtime(ms, batch_max=2, flags=tp.TP_FLAG_NO_GRAPH)
+    ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
+    ref_rt.close()
+    arena = max(m.total_bytes for m in ms) + 4096
+    rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, chunk_min_bytes=0, direct_max_bytes=1 << 40,
+                           flags=flags | tp.TP_FLAG_POISON | tp.TP_FLAG_THROTTLE, throttle_us=200)
+    torch, dev = torch_dev()
+    s = torch.cuda.Stream(device=dev)
+    for rep in range(2):
+        for k in range(3):
+            log(f"direct access: rep {rep} {ms[k].arch}")
+            cold = infer(rt, ids[k], ms[k], xs[k], stream=s)
+            warm = infer(rt, ids[k], ms[k], xs[k], stream=s)
+            assert np.array_equal(cold, ref[k]) and np.array_equal(warm, ref[k]), (rep, k)
+            assert np.array_equal(rt.extent(ids[k]).cpu().numpy(), expected_host_image(ms[k])), (rep, k)
+    st = rt.stats()
+    assert st["misses"] == 6 and st["hits"] == 6
     rt.close()
