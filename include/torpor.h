@@ -102,9 +102,10 @@ enum {
   TP_FLAG_NO_GRAPH = 4,   /* launch warm requests kernel by kernel instead of replaying a graph */
   TP_FLAG_SERIAL = 8,     /* a cold request waits for its whole model before its first kernel
                            * (swap, then execute: no pipelining) */
-  TP_FLAG_PER_TENSOR = 16 /* transfer groups close at tensor boundaries, not layer boundaries;
+  TP_FLAG_PER_TENSOR = 16,/* transfer groups close at tensor boundaries, not layer boundaries;
                            * with chunk_min_bytes = 0 every tensor is its own transfer (the
                            * parameter-level pipeline of Sec. 6.1) */
+  TP_FLAG_TRACE = 32      /* cold requests record timing events per chunk (tp_last_timeline) */
 };
 
 /* Context configuration. arena_dev/work_dev are caller-owned device buffers that must
@@ -220,6 +221,16 @@ TP_API tp_status tp_model_host_image(struct tp_ctx* ctx, int32_t model_id, const
  * byte ranges and the first layer each chunk holds; *n receives the chunk count. */
 TP_API tp_status tp_model_chunks(struct tp_ctx* ctx, int32_t model_id, uint64_t* begin, uint64_t* end,
                           uint32_t* first_layer, uint32_t cap, uint32_t* n);
+
+/* Timeline of the last cold tp_infer of a TP_FLAG_TRACE context (the pipelined path,
+ * Sec. 4.3: chunk c's copy overlaps the layers of earlier chunks), in milliseconds from
+ * that request's start event on the caller's stream: for each of the first `cap` chunks,
+ * when its copy began and ended on the copy stream and when the caller's stream passed
+ * its wait for the chunk (the first kernel that reads it starts after that); *n receives
+ * the chunk count and *total_ms the time until the request's last kernel ended. Blocks
+ * until that request has completed. TP_E_STATE if no cold request has been traced. */
+TP_API tp_status tp_last_timeline(struct tp_ctx* ctx, float* copy_begin_ms, float* copy_end_ms, float* exec_begin_ms,
+                           uint32_t cap, uint32_t* n, float* total_ms);
 
 /* Workspace bytes tp_infer needs for this model at this batch size (host-only). */
 TP_API tp_status tp_workspace_bytes(const tp_model_desc* desc, int32_t batch, uint64_t* bytes);

@@ -42,6 +42,11 @@ void destroy_streams(tp_ctx* c) {
   if (c->copy[1]) (void)hipStreamDestroy(c->copy[1]);
   if (c->capture) (void)hipStreamDestroy(c->capture);
   if (c->req_done) (void)hipEventDestroy(c->req_done);
+  for (auto* v : {&c->tl.copy_begin, &c->tl.copy_end, &c->tl.exec_begin})
+    for (hipEvent_t e : *v)
+      if (e) (void)hipEventDestroy(e);
+  if (c->tl.start) (void)hipEventDestroy(c->tl.start);
+  if (c->tl.done) (void)hipEventDestroy(c->tl.done);
   if (c->fork) (void)hipEventDestroy(c->fork);
   for (hipEvent_t e : c->trace_ev)
     if (e) (void)hipEventDestroy(e);
@@ -116,6 +121,8 @@ hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
   char* dst = c->arena + off + ch.begin;
   hipStream_t s = c->copy[i % ns];
   if (e == hipSuccess && (c->cfg.flags & TP_FLAG_THROTTLE)) e = k::delay(c->cfg.throttle_us, s);
+  const bool traced = c->tl.active && i < c->tl.copy_begin.size();
+  if (e == hipSuccess && traced) e = hipEventRecord(c->tl.copy_begin[i], s);
   if (e == hipSuccess) {
     if (c->cfg.copy_method == TP_COPY_GATHER)
       e = k::gather_copy(static_cast<char*>(m->host_dev) + ch.begin, dst, nb, c->cfg.gather_wgs, s);
@@ -125,6 +132,7 @@ hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
       e = hipMemcpyAsync(dst, static_cast<char*>(m->host) + ch.begin, nb, hipMemcpyHostToDevice, s);
   }
   if (e == hipSuccess) e = hipEventRecord(m->chunk_ev[i], s);
+  if (e == hipSuccess && traced) e = hipEventRecord(c->tl.copy_end[i], s);
   return e;
 }
 
@@ -150,6 +158,11 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
 }
 
 }  // namespace
+
+hipError_t tp::Waiter::trace_exec(int c) {
+  if (!ctx || !ctx->tl.active || c >= (int)ctx->tl.exec_begin.size()) return hipSuccess;
+  return hipEventRecord(ctx->tl.exec_begin[c], stream);
+}
 
 hipError_t tp::Waiter::issue_through(int c) {
   hipError_t e = hipSuccess;
@@ -242,6 +255,11 @@ tp_status begin_request(tp_ctx* c, hipStream_t stream) {
 }
 
 tp_status end_request(tp_ctx* c, Model* m, hipStream_t stream) {
+  if (c->tl.active) {
+    c->tl.active = false;
+    TP_HIP(hipEventRecord(c->tl.done, stream));
+    c->tl.valid = true;
+  }
   TP_HIP(hipEventRecord(m->last_use, stream));
   m->used = true;
   TP_HIP(hipEventRecord(c->req_done, stream));
@@ -296,6 +314,8 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming);
+  if (e == hipSuccess && (cfg->flags & TP_FLAG_TRACE)) e = hipEventCreate(&c->tl.start);
+  if (e == hipSuccess && (cfg->flags & TP_FLAG_TRACE)) e = hipEventCreate(&c->tl.done);
   if (e != hipSuccess) {
     destroy_streams(c.get());
     return hip_fail(e, "tp_create: stream or event creation");
@@ -359,6 +379,15 @@ tp_status tp_register_model(tp_ctx* c, const tp_model_desc* desc, const void* ho
     std::memcpy(m->pageable.get(), m->host, nb);
   }
   e = hipHostGetDevicePointer(&m->host_dev, m->host, 0);
+  if (c->cfg.flags & TP_FLAG_TRACE) {
+    // timing events for as many chunks as the largest plan so far (made once, kept)
+    for (auto* v : {&c->tl.copy_begin, &c->tl.copy_end, &c->tl.exec_begin})
+      while (e == hipSuccess && v->size() < m->chunks.size()) {
+        hipEvent_t ev = nullptr;
+        e = hipEventCreate(&ev);
+        if (e == hipSuccess) v->push_back(ev);
+      }
+  }
   m->chunk_ev.assign(m->chunks.size(), nullptr);
   for (size_t i = 0; e == hipSuccess && i < m->chunks.size(); ++i)
     e = hipEventCreateWithFlags(&m->chunk_ev[i], hipEventDisableTiming);
@@ -473,6 +502,12 @@ tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, 
     w.ctx = c;
     w.base_off = off;
     ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w, make_split(c, m, batch)};
+    if (swapped && (c->cfg.flags & TP_FLAG_TRACE)) {
+      c->tl.active = true;
+      c->tl.valid = false;
+      c->tl.n = (uint32_t)m->chunks.size();
+      e = hipEventRecord(c->tl.start, stream);
+    }
     // swap, then execute: every chunk is waited for before the first kernel
     if (swapped && (c->cfg.flags & TP_FLAG_SERIAL)) e = w.need(m->spec.n_layers - 1);
     if (e == hipSuccess) e = run_forward(x);
@@ -523,6 +558,22 @@ tp_status tp_evict(tp_ctx* c, int32_t id) {
   const uint64_t off = c->policy->offset(id), len = c->policy->bytes(id);
   c->policy->evict(id);
   return retire(c, id, off, len);
+}
+
+tp_status tp_last_timeline(tp_ctx* c, float* copy_begin, float* copy_end, float* exec_begin, uint32_t cap,
+                           uint32_t* n, float* total_ms) {
+  if (!c || !n) return fail(TP_E_INVAL, "NULL argument");
+  if (!(c->cfg.flags & TP_FLAG_TRACE) || !c->tl.valid) return fail(TP_E_STATE, "no traced cold request");
+  TP_HIP(hipEventSynchronize(c->tl.done));
+  *n = c->tl.n;
+  if (total_ms) TP_HIP(hipEventElapsedTime(total_ms, c->tl.start, c->tl.done));
+  const uint32_t k = std::min<uint32_t>(std::min<uint32_t>(cap, c->tl.n), (uint32_t)c->tl.copy_begin.size());
+  for (uint32_t i = 0; i < k; ++i) {
+    if (copy_begin) TP_HIP(hipEventElapsedTime(&copy_begin[i], c->tl.start, c->tl.copy_begin[i]));
+    if (copy_end) TP_HIP(hipEventElapsedTime(&copy_end[i], c->tl.start, c->tl.copy_end[i]));
+    if (exec_begin) TP_HIP(hipEventElapsedTime(&exec_begin[i], c->tl.start, c->tl.exec_begin[i]));
+  }
+  return ok();
 }
 
 tp_status tp_is_resident(tp_ctx* c, int32_t id, int32_t* resident) {

@@ -66,9 +66,11 @@ struct Waiter {
     while (e == hipSuccess && waited < c) {
       ++waited;
       e = hipStreamWaitEvent(stream, m->chunk_ev[waited], 0);
+      if (e == hipSuccess) e = trace_exec(waited);
     }
     return e;
   }
+  hipError_t trace_exec(int c);
 };
 
 // Device addresses of the running request.
@@ -119,4 +121,12 @@ struct tp_ctx {
     int32_t model;
   };
   std::vector<Retired> retired;
+  // TP_FLAG_TRACE: timing events of the last traced cold request
+  struct Timeline {
+    hipEvent_t start = nullptr, done = nullptr;
+    std::vector<hipEvent_t> copy_begin, copy_end, exec_begin;   // per chunk
+    uint32_t n = 0;                  // chunks of the traced request
+    bool active = false;             // the request being enqueued is traced
+    bool valid = false;
+  } tl;
 };

@@ -8,83 +8,21 @@
 // register e of lane l holds D[n = 4 (l / 16) + e][m = l % 16]: four consecutive output
 // features of one row, which the epilogue stores as one vector.
 //
-// Two kernels:
-//   * k_gemv: skinny M (<= 32). The weights dominate the traffic (HBM-bound), so each
-//     workgroup owns 16 weight rows and its 16 waves stream disjoint 128-wide k-blocks
-//     with 4 x 16-byte loads per lane in flight, then reduce across waves through LDS in
-//     a fixed order.
+// Kernels here (the skinny M <= 32 case is in gemv_bf16.hip):
 //   * k_gemm: LDS-tiled BN x BM x BK tiles, 4 waves in a 2 x 2 arrangement, global loads
 //     of the next k-stage issued before the MFMAs of the current one, double-buffered LDS,
 //     and a deterministic split over k when the tile grid alone cannot fill the chip. The
 //     activation loader is either a plain row-major matrix or an NHWC implicit-GEMM
 //     (im2col) gather for convolutions, k = (kh * KW + kw) * C + c, matching OHWI weight
 //     rows.
-#include "common.hpp"
-#include "kernels.hpp"
+//   * k_conv_smallc: convolutions with fewer than 8 input channels (the ResNet stem),
+//     whose input window rows are staged in LDS.
+#include "gemm_args.hpp"
 
 namespace tp {
 namespace k {
 
 namespace {
-
-// activation loaders: row-major matrix; NHWC im2col with C % 64 == 0 (a 64-deep k-stage
-// then lies inside one filter tap); NHWC im2col with C % 8 == 0; element-wise im2col
-enum { X_ROWS = 0, X_CONV8 = 1, X_CONV1 = 2, X_CONV64 = 3 };
-
-struct GemmArgs {
-  const uint16_t* x;
-  const uint16_t* w;
-  int M, N, K;
-  int H, W, C, KW, stride, pad, Ho, Wo;   // convolution geometry (X_CONV*)
-  Epilogue ep;
-  int kst, splits;                        // k-stages per split, number of splits
-  float* partials;                        // [splits][M][N] fp32 when splits > 1
-};
-
-__device__ __forceinline__ void store_row4(const GemmArgs& a, int m, int n0, f32x4 acc) {
-  if (m >= a.M || n0 >= a.N) return;
-  const Epilogue& ep = a.ep;
-  const size_t base = (size_t)m * a.N + n0;
-  float v[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) v[e] = acc[e];
-  const bool full = (n0 + 3 < a.N) && ((a.N & 3) == 0);
-  if (full) {
-    if (ep.bias) {
-      const uint2 b = *reinterpret_cast<const uint2*>(ep.bias + n0);
-      v[0] += bf2f(b.x & 0xffff); v[1] += bf2f(b.x >> 16); v[2] += bf2f(b.y & 0xffff); v[3] += bf2f(b.y >> 16);
-    }
-    if (ep.res) {
-      if (ep.res_f32) {
-        const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(ep.res) + base);
-        v[0] += r.x; v[1] += r.y; v[2] += r.z; v[3] += r.w;
-      } else {
-        const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(ep.res) + base);
-        v[0] += bf2f(r.x & 0xffff); v[1] += bf2f(r.x >> 16); v[2] += bf2f(r.y & 0xffff); v[3] += bf2f(r.y >> 16);
-      }
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = act_apply(v[e], ep.act);
-    if (ep.out_f32) {
-      *reinterpret_cast<float4*>(static_cast<float*>(ep.out) + base) = make_float4(v[0], v[1], v[2], v[3]);
-    } else {
-      uint2 o;
-      o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-      o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(ep.out) + base) = o;
-    }
-    return;
-  }
-  for (int e = 0; e < 4 && n0 + e < a.N; ++e) {
-    float t = v[e];
-    if (ep.bias) t += bf2f(ep.bias[n0 + e]);
-    if (ep.res) t += ep.res_f32 ? static_cast<const float*>(ep.res)[base + e]
-                                : bf2f(static_cast<const uint16_t*>(ep.res)[base + e]);
-    t = act_apply(t, ep.act);
-    if (ep.out_f32) static_cast<float*>(ep.out)[base + e] = t;
-    else static_cast<uint16_t*>(ep.out)[base + e] = f2bf(t);
-  }
-}
 
 // Epilogue of 16 consecutive outputs n0 .. n0+15 of row m (contiguous loads and stores)
 __device__ __forceinline__ void store_row16(const GemmArgs& a, int m, int n0, const float (&v_in)[16]) {
@@ -154,75 +92,6 @@ __device__ __forceinline__ void store_row16(const GemmArgs& a, int m, int n0, co
     t = act_apply(t, ep.act);
     if (ep.out_f32) static_cast<float*>(ep.out)[base + e] = t;
     else static_cast<uint16_t*>(ep.out)[base + e] = f2bf(t);
-  }
-}
-
-// ------------------------------------------------------------------ skinny M
-
-// PK: weights in 16 x 128 blocks (see pack_rows16x128 in the host code), so load j of
-// lane (r, q) in k-block kb reads 16 bytes at block offset j*512 + (q*16 + r)*8 and one
-// load instruction covers a contiguous 1 KB; otherwise rows are [N][K] and an instruction
-// reads 64 contiguous bytes of each of 16 rows. Activation rows beyond M issue no load.
-template <int MT, int NW, bool PK>
-__global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = lane & 15, q = lane >> 4;
-  const int n0 = blockIdx.x * 16;
-  const bool nvalid = n0 + r < a.N;
-  const int nkb = (a.K + 127) >> 7;
-  const uint16_t* wrow = PK ? a.w + (size_t)blockIdx.x * nkb * 2048 + lane * 8
-                            : a.w + (size_t)(nvalid ? n0 + r : 0) * a.K;
-  const uint16_t* xrow[MT];
-  bool mvalid[MT];
-#pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    const int m = (t << 4) + r;
-    mvalid[t] = m < a.M;
-    xrow[t] = a.x + (size_t)(mvalid[t] ? m : 0) * a.K;
-  }
-  f32x4 acc[MT];
-#pragma unroll
-  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // k-block of 128: load j of lane (r, q) covers k = kb*128 + 32 j + 8 q .. +8
-  for (int kb0 = wave; kb0 < nkb; kb0 += 2 * NW) {
-    uint4 av[2][4], bv[2][MT][4];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int kb = kb0 + u * NW;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int kk = (kb << 7) + (j << 5) + (q << 3);
-        const bool kin = kb < nkb && kk < a.K;
-        const int ks = kin ? kk : 0;
-        if (PK)
-          av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + (size_t)(kin ? kb : 0) * 2048 + j * 512), kin);
-        else
-          av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + ks), nvalid && kin);
-#pragma unroll
-        for (int t = 0; t < MT; ++t) {
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (mvalid[t] && kin) v = *reinterpret_cast<const uint4*>(xrow[t] + ks);
-          bv[u][t][j] = v;
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int t = 0; t < MT; ++t)
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[u][j]), as_bf16x8(bv[u][t][j]), acc[t], 0, 0,
-                                                           0);
-  }
-  __shared__ f32x4 red[NW][MT][64];
-#pragma unroll
-  for (int t = 0; t < MT; ++t) red[wave][t][lane] = acc[t];
-  __syncthreads();
-  if (wave < MT) {
-    f32x4 s = red[0][wave][lane];
-    for (int w = 1; w < NW; ++w) s += red[w][wave][lane];
-    store_row4(a, (wave << 4) + r, n0 + (q << 2), s);
   }
 }
 
@@ -469,6 +338,139 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
+// ------------------------------------------------------------------ few input channels
+
+// Convolutions whose input has fewer than 8 channels (the ResNet stem: 7 x 7, stride 2,
+// 3 channels), where an im2col row is not made of 16-byte runs. A workgroup owns all
+// (<= 64) output channels and SC_W consecutive output pixels of `rows` output rows of one
+// sample. The weights are brought in once per workgroup as 16-byte loads of the flat
+// [N][K] array and re-laid out in LDS with rows zero-padded to a multiple of 32. Per
+// output row, the KH input rows that its windows touch are staged in LDS (zero where a
+// window leaves the image), every global load of a stage issued before the first LDS
+// store, and the next row's loads are issued before this row's multiplications. Wave w
+// multiplies the 16 pixels 16w .. 16w+15 against every output channel: the activation
+// operand is gathered element by element from the staged rows (k = (kh * KW + kw) * C +
+// c, so a k-run inside one filter row is a run of a staged input row), the weight
+// operand read as 16-byte vectors.
+constexpr int SC_W = 64, SC_MAXC = 4, SC_MAXK = 7, SC_MAXS = 2;
+constexpr int SC_KP = ((SC_MAXK * SC_MAXK * SC_MAXC + 31) / 32) * 32;   // 224
+constexpr int SC_KS = SC_KP + 8;                                        // weight row stride in LDS
+constexpr int SC_RL = ((SC_W - 1) * SC_MAXS + SC_MAXK) * SC_MAXC;       // longest staged input row
+constexpr int SC_PER = (SC_RL + 255) / 256;                             // staged elements per thread and row
+constexpr int SC_WV = (64 * SC_MAXK * SC_MAXK * SC_MAXC * 2 / 16 + 255) / 256;  // 16-byte weight loads per thread
+
+template <int C>
+struct SmallConvRow {
+  uint16_t v[SC_MAXK][SC_PER];
+  // loads of output row oh's input window rows (zero outside the image or beyond KH)
+  __device__ void load(const GemmArgs& a, int b, int oh, int iw0, int KH, int rl, int tid) {
+    const int ih0 = oh * a.stride - a.pad;
+#pragma unroll
+    for (int kh = 0; kh < SC_MAXK; ++kh) {
+      const int ih = ih0 + kh;
+      const bool hin = kh < KH && ih >= 0 && ih < a.H;
+      const uint16_t* xrow = a.x + ((size_t)b * a.H + (hin ? ih : 0)) * a.W * C;
+#pragma unroll
+      for (int u = 0; u < SC_PER; ++u) {
+        const int j = u * 256 + tid;
+        const int col = j / C, iw = iw0 + col;
+        v[kh][u] = (hin && j < rl && iw >= 0 && iw < a.W) ? xrow[(size_t)iw * C + (j - col * C)] : (uint16_t)0;
+      }
+    }
+  }
+  __device__ void store(uint16_t* xl, int KH, int rl, int tid) const {
+#pragma unroll
+    for (int kh = 0; kh < SC_MAXK; ++kh)
+#pragma unroll
+      for (int u = 0; u < SC_PER; ++u) {
+        const int j = u * 256 + tid;
+        if (kh < KH && j < rl) xl[kh * rl + j] = v[kh][u];
+      }
+  }
+};
+
+template <int C>
+__global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
+  __shared__ __align__(16) uint16_t wl[64 * SC_KS];
+  __shared__ __align__(16) uint16_t xl[SC_MAXK * SC_RL > 64 * SC_KP ? SC_MAXK * SC_RL : 64 * SC_KP];
+  __shared__ __align__(16) int koff[SC_KP];   // staged-row offset of window element k, -1 beyond K
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int KW = a.KW, K = a.K, KWC = KW * C, KH = K / KWC;
+  const int KP = (K + 31) & ~31;
+  const int ow0 = blockIdx.x * SC_W, b = blockIdx.z;
+  const int rl = ((SC_W - 1) * a.stride + KW) * C;
+  for (int k = tid; k < KP; k += 256) {
+    const int kh = k / KWC;
+    koff[k] = k < K ? kh * rl + (k - kh * KWC) : -1;
+  }
+  const int iw0 = ow0 * a.stride - a.pad;
+  const int oh_first = blockIdx.y * rows;
+  SmallConvRow<C> nxt;
+  {
+    // the flat weights through xl (all loads first), then padded rows into wl
+    const int nw = a.N * K;                       // elements; the array starts 16-byte aligned
+    const int nv = (nw * 2 + 15) / 16;
+    uint4 wv[SC_WV];
+#pragma unroll
+    for (int u = 0; u < SC_WV; ++u) {
+      const int i = u * 256 + tid;
+      // the last vector may extend past the array end; it stays inside the 256-byte
+      // aligned allocation unit of the weight tensor
+      wv[u] = i < nv ? reinterpret_cast<const uint4*>(a.w)[i] : make_uint4(0, 0, 0, 0);
+    }
+    nxt.load(a, b, oh_first, iw0, KH, rl, tid);
+#pragma unroll
+    for (int u = 0; u < SC_WV; ++u) {
+      const int i = u * 256 + tid;
+      if (i < nv) reinterpret_cast<uint4*>(xl)[i] = wv[u];
+    }
+    __syncthreads();
+    for (int i = tid; i < 64 * KP; i += 256) {
+      const int n = i / KP, k = i - n * KP;
+      wl[n * SC_KS + k] = (n < a.N && k < K) ? xl[n * K + k] : (uint16_t)0;
+    }
+  }
+  const int p = wave * 16 + (lane & 15), q = lane >> 4;
+  const int pofs = p * a.stride * C;
+  for (int r = 0; r < rows; ++r) {
+    const int oh = oh_first + r;
+    if (oh >= a.Ho) break;
+    __syncthreads();                  // wl written; every read of xl (weights or last row) done
+    nxt.store(xl, KH, rl, tid);
+    __syncthreads();
+    if (r + 1 < rows && oh + 1 < a.Ho) nxt.load(a, b, oh + 1, iw0, KH, rl, tid);
+    f32x4 acc[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the same number of k-steps in every lane; element reads are unconditional (offset
+    // clamped to 0) and masked afterwards
+    for (int ks = 0; ks < KP / 32; ++ks) {
+      const int k0 = ks * 32 + q * 8;
+      const int4 o0 = *reinterpret_cast<const int4*>(&koff[k0]);
+      const int4 o1 = *reinterpret_cast<const int4*>(&koff[k0 + 4]);
+      const int o[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+      uint32_t bw[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t v = xl[(o[e] < 0 ? 0 : o[e]) + pofs];
+        bw[e >> 1] |= (o[e] < 0 ? 0u : v) << (16 * (e & 1));
+      }
+      const uint4 bv = make_uint4(bw[0], bw[1], bw[2], bw[3]);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const uint4 av = *reinterpret_cast<const uint4*>(&wl[(16 * g + (lane & 15)) * SC_KS + k0]);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), as_bf16x8(bv), acc[g], 0, 0, 0);
+      }
+    }
+    if (ow0 + p < a.Wo) {
+      const int m = ((b * a.Ho) + oh) * a.Wo + ow0 + p;
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        if (16 * g < a.N) store_row4(a, m, 16 * g + 4 * q, acc[g]);
+    }
+  }
+}
+
 // y = epilogue(sum over splits z = 0, 1, ... of P[z]) for four consecutive outputs per thread
 __global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
   const long q = (long)blockIdx.x * 256 + threadIdx.x;       // index of a group of 4 outputs
@@ -536,17 +538,7 @@ hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N
   if (ep.w_packed && ((N & 15) || (K & 127))) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = x; a.w = w; a.M = M; a.N = N; a.K = K; a.ep = ep;
-  if (M <= 32) {
-    const dim3 grid((N + 15) / 16), block(1024);
-    if (M <= 16) {
-      if (ep.w_packed) hipLaunchKernelGGL((k_gemv<1, 16, true>), grid, block, 0, s, a);
-      else hipLaunchKernelGGL((k_gemv<1, 16, false>), grid, block, 0, s, a);
-    } else {
-      if (ep.w_packed) hipLaunchKernelGGL((k_gemv<2, 16, true>), grid, block, 0, s, a);
-      else hipLaunchKernelGGL((k_gemv<2, 16, false>), grid, block, 0, s, a);
-    }
-    return hipGetLastError();
-  }
+  if (M <= 32) return launch_skinny(a, s);
   return pick_tiled<X_ROWS, true>(a, sp, s);
 }
 
@@ -564,6 +556,20 @@ hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16
   a.H = H; a.W = W; a.C = C; a.KW = KW; a.stride = stride; a.pad = pad; a.Ho = Ho; a.Wo = Wo;
   a.ep = ep;
   a.ep.w_packed = 0;
+  if (C <= SC_MAXC && KH <= SC_MAXK && KW <= SC_MAXK && stride <= SC_MAXS && O <= 64 && (O & 15) == 0 &&
+      a.K <= SC_KP) {
+    // enough workgroups to fill the chip, each reusing its staged weights over `rows` rows
+    const int segs = (Wo + SC_W - 1) / SC_W;
+    const int rows = max(1, min(8, segs * Ho * B / 448));
+    dim3 grid(segs, (Ho + rows - 1) / rows, B);
+    switch (C) {
+      case 1: hipLaunchKernelGGL(k_conv_smallc<1>, grid, dim3(256), 0, s, a, rows); break;
+      case 2: hipLaunchKernelGGL(k_conv_smallc<2>, grid, dim3(256), 0, s, a, rows); break;
+      case 3: hipLaunchKernelGGL(k_conv_smallc<3>, grid, dim3(256), 0, s, a, rows); break;
+      default: hipLaunchKernelGGL(k_conv_smallc<4>, grid, dim3(256), 0, s, a, rows); break;
+    }
+    return hipGetLastError();
+  }
   if ((C & 63) == 0) return pick_tiled<X_CONV64, true>(a, sp, s);
   if ((C & 7) == 0) return pick_tiled<X_CONV8, true>(a, sp, s);
   if ((a.K & 7) == 0) return pick_tiled<X_CONV1, true>(a, sp, s);

@@ -46,15 +46,28 @@ __global__ __launch_bounds__(256) void k_maxpool3s2(const uint16_t* __restrict__
 }
 
 // one thread per (sample, channel), positions summed in order in fp32
-__global__ __launch_bounds__(256) void k_avgpool(const uint16_t* __restrict__ x, int B, int HW, int C,
-                                                 uint16_t* __restrict__ y) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
+// One thread per (sample, channel). The HW loads are independent, so they are issued 8 at
+// a time into 8 partial sums, which are then added in a fixed order.
+__global__ __launch_bounds__(64) void k_avgpool(const uint16_t* __restrict__ x, int B, int HW, int C,
+                                                uint16_t* __restrict__ y) {
+  const int i = blockIdx.x * 64 + threadIdx.x;
   if (i >= B * C) return;
   const int b = i / C, c = i - b * C;
   const uint16_t* p = x + (size_t)b * HW * C + c;
-  float s = 0.f;
-  for (int j = 0; j < HW; ++j) s += bf2f(p[(size_t)j * C]);
-  y[i] = f2bf(s / (float)HW);
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  int j = 0;
+  for (; j + 8 <= HW; j += 8) {
+    uint16_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = p[(size_t)(j + u) * C];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s[u] += bf2f(v[u]);
+  }
+  for (; j < HW; ++j) s[0] += bf2f(p[(size_t)j * C]);
+  float t = 0.f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) t += s[u];
+  y[i] = f2bf(t / (float)HW);
 }
 
 // grid-stride copy with U independent 16-byte loads in flight per thread
@@ -88,7 +101,7 @@ hipError_t maxpool3s2(const uint16_t* x, int B, int H, int W, int C, uint16_t* y
 
 hipError_t avgpool(const uint16_t* x, int B, int HW, int C, uint16_t* y, hipStream_t s) {
   if (!x || !y || B < 1 || HW < 1 || C < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_avgpool, dim3((B * C + 255) / 256), dim3(256), 0, s, x, B, HW, C, y);
+  hipLaunchKernelGGL(k_avgpool, dim3((B * C + 63) / 64), dim3(64), 0, s, x, B, HW, C, y);
   return hipGetLastError();
 }
 

@@ -24,7 +24,7 @@ TP_F32, TP_BF16 = 0, 1
 TP_ARCH_MLP, TP_ARCH_RESNET50, TP_ARCH_BERT = 0, 1, 2
 TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
 TP_COPY_MEMCPY, TP_COPY_GATHER, TP_COPY_PAGEABLE, TP_COPY_ZERO = 0, 1, 2, 3
-TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR = 1, 2, 4, 8, 16
+TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR, TP_FLAG_TRACE = 1, 2, 4, 8, 16, 32
 ROLES = {
     "w": 0, "b": 1,
     "tok_emb": 10, "pos_emb": 11, "type_emb": 12, "emb_ln_g": 13, "emb_ln_b": 14,
@@ -106,6 +106,8 @@ _SIGS = {
     "tp_model_chunks": [_P, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
                         C.c_uint32, C.POINTER(C.c_uint32)],
     "tp_workspace_bytes": [C.POINTER(tp_model_desc), C.c_int32, C.POINTER(C.c_uint64)],
+    "tp_last_timeline": [_P, C.POINTER(C.c_float), C.POINTER(C.c_float), C.POINTER(C.c_float), C.c_uint32,
+                         C.POINTER(C.c_uint32), C.POINTER(C.c_float)],
     "tp_model_host_image": [_P, C.c_int32, C.POINTER(_P), C.POINTER(C.c_uint64)],
     "tp_run_trace": [_P, C.POINTER(tp_request), C.c_uint32, _P, C.POINTER(tp_request_result)],
     "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
@@ -279,6 +281,16 @@ def tp_model_chunks(ctx, model_id):
     return [{"begin": b[i], "end": e[i], "first_layer": f[i]} for i in range(n.value)]
 
 
+def tp_last_timeline(ctx):
+    """Per-chunk copy begin/end and wait-passed times (ms) of the last traced cold request."""
+    L = lib()
+    n, total = C.c_uint32(), C.c_float()
+    _check(L, L.tp_last_timeline(ctx, None, None, None, 0, C.byref(n), C.byref(total)))
+    cb, ce, xb = (C.c_float * n.value)(), (C.c_float * n.value)(), (C.c_float * n.value)()
+    _check(L, L.tp_last_timeline(ctx, cb, ce, xb, n.value, C.byref(n), C.byref(total)))
+    return {"total_ms": total.value, "copy_begin_ms": list(cb), "copy_end_ms": list(ce), "exec_begin_ms": list(xb)}
+
+
 def tp_model_host_image(ctx, model_id) -> np.ndarray:
     """Read-only uint8 view of the library's pinned host image of a model."""
     p, n = _P(), C.c_uint64()
@@ -421,6 +433,9 @@ class Runtime:
 
     def info(self, mid) -> dict:
         return tp_model_info(self.ctx, mid)
+
+    def timeline(self):
+        return tp_last_timeline(self.ctx)
 
     def chunks(self, mid):
         return tp_model_chunks(self.ctx, mid)

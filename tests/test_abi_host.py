@@ -26,7 +26,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 24, sorted(names)
+    assert len(names) == 25, sorted(names)
     L = tp.lib()
     for n in names:
         assert hasattr(L, n), n

@@ -246,3 +246,26 @@ def test_direct_access_then_background_swap(flags):
     st = rt.stats()
     assert st["misses"] == 6 and st["hits"] == 6
     rt.close()
+
+
+def test_traced_timeline_is_causal():
+    # chunk c's first kernel passes its wait only after its copy ended; copies run in order
+    m = synth.resnet50(seed=63, classes=10, image=32)
+    x = synth.config_input(m, 2, 71)
+    rt, ids = make_runtime([m], batch_max=2, chunk_min_bytes=2 << 20, flags=tp.TP_FLAG_TRACE)
+    ref_rt, ref_ids = make_runtime([m], batch_max=2)
+    want = infer(ref_rt, ref_ids[0], m, x)
+    ref_rt.close()
+    for rep in range(3):
+        rt.evict(ids[0])
+        assert np.array_equal(infer(rt, ids[0], m, x), want)
+        tl = rt.timeline()
+        n = len(rt.chunks(ids[0]))
+        assert n > 3 and len(tl["copy_begin_ms"]) == n
+        cb, ce, xb = tl["copy_begin_ms"], tl["copy_end_ms"], tl["exec_begin_ms"]
+        log(f"timeline rep {rep}: total {tl['total_ms']:.3f} ms, last copy end {ce[-1]:.3f} ms")
+        for c in range(n):
+            assert cb[c] <= ce[c] <= xb[c] + 1e-3 <= tl["total_ms"] + 2e-3, (c, cb[c], ce[c], xb[c])
+            if c:
+                assert ce[c - 1] <= cb[c] + 1e-3 and xb[c - 1] <= xb[c] + 1e-3
+    rt.close()
