@@ -76,7 +76,8 @@ def link_peak(torch, dev, reps=10, nbytes=1 << 30):
 
 
 class Bench:
-    def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0, flags=0, direct=None):
+    def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0, flags=0, direct=None, plan="greedy",
+                 link_gbs=0.0):
         import paper_2306_03622_amd as tp
         self.tp, self.torch, self.dev, self.m = tp, torch, dev, model
         self.desc = tp.ModelDesc.of(model)
@@ -85,7 +86,9 @@ class Bench:
               "zero": tp.TP_COPY_ZERO}[method]
         self.rt = tp.Runtime(model.total_bytes + (1 << 20), ws, chunk_min_bytes=chunk, copy_method=cm,
                              copy_streams=copy_streams, flags=flags,
-                             direct_max_bytes=tp.DEFAULT_DIRECT if direct is None else direct)
+                             direct_max_bytes=tp.DEFAULT_DIRECT if direct is None else direct,
+                             plan=tp.TP_PLAN_COST if plan == "cost" else tp.TP_PLAN_GREEDY,
+                             plan_batch=max(batches), link_gbs=link_gbs)
         self.mid = self.rt.register(self.desc, model.blob())
         self.stream = torch.cuda.Stream(device=dev)
 
@@ -182,21 +185,22 @@ def elbow_sweep(torch, dev, method, copy_streams=0, sizes=(256 << 10, 512 << 10,
 # Swap designs of the breakdown (Sec. 6.1, "Performance breakdown of model swapping"), each
 # changing one thing from the row above, then the alternatives the library also offers.
 # (name, copy method, group size or None for the default, flags, copy streams, direct-access
-# size limit)
+# size limit, chunk plan)
 ABLATION = (
-    ("baseline: pageable copy per tensor, then execute", "pageable", 0, "serial|per_tensor", 1, 0),
-    ("pinned: pinned copy per tensor, then execute", "memcpy", 0, "serial|per_tensor", 1, 0),
-    ("pipeline: per-tensor transfers overlapped with execution", "memcpy", 0, "per_tensor", 1, 0),
-    ("group: tensors grouped to >= G, overlapped", "memcpy", None, "per_tensor", 1, 0),
-    ("group by layer: whole layers grouped to >= G", "memcpy", None, "", 1, 0),
-    ("gather kernel instead of the copy engine, grouped by layer", "gather", None, "", 1, 0),
-    ("two copy streams, grouped by layer", "memcpy", None, "", 2, 0),
-    ("zero-copy: kernels read the pinned host copy, never resident", "zero", None, "", 1, 0),
-    ("direct access first, swap behind it (default for models <= 2 MiB)", "memcpy", None, "", 1, 1 << 62),
+    ("baseline: pageable copy per tensor, then execute", "pageable", 0, "serial|per_tensor", 1, 0, "greedy"),
+    ("pinned: pinned copy per tensor, then execute", "memcpy", 0, "serial|per_tensor", 1, 0, "greedy"),
+    ("pipeline: per-tensor transfers overlapped with execution", "memcpy", 0, "per_tensor", 1, 0, "greedy"),
+    ("group: tensors grouped to >= G, overlapped", "memcpy", None, "per_tensor", 1, 0, "greedy"),
+    ("group by layer: whole layers grouped to >= G", "memcpy", None, "", 1, 0, "greedy"),
+    ("gather kernel instead of the copy engine, grouped by layer", "gather", None, "", 1, 0, "greedy"),
+    ("two copy streams, grouped by layer", "memcpy", None, "", 2, 0, "greedy"),
+    ("zero-copy: kernels read the pinned host copy, never resident", "zero", None, "", 1, 0, "greedy"),
+    ("direct access first, swap behind it (default for models <= 2 MiB)", "memcpy", None, "", 1, 1 << 62, "greedy"),
+    ("cost-model grouping: boundaries minimising the modelled completion time", "memcpy", None, "", 1, 0, "cost"),
 )
 
 
-def ablation(torch, dev, chunk, budget_s=2.5, max_reps=20):
+def ablation(torch, dev, chunk, link_gbs, budget_s=2.5, max_reps=20):
     """Cold p50 of every swap design on the single-GPU workloads (batch 8, and batch 1 for
     the 1 MB MLP). A design is timed until max_reps cold requests or budget_s seconds."""
     import synth
@@ -208,12 +212,12 @@ def ablation(torch, dev, chunk, budget_s=2.5, max_reps=20):
         m.blob()
         rows = []
         ref = None
-        for name, method, g, fl, ns, direct in ABLATION:
+        for name, method, g, fl, ns, direct, plan in ABLATION:
             flags = 0
             for f in filter(None, fl.split("|")):
                 flags |= bits[f]
             log(f"ablation cfg{cfg} b{bt}: {name}")
-            b = Bench(torch, dev, m, [bt], method, chunk if g is None else g, ns, flags, direct)
+            b = Bench(torch, dev, m, [bt], method, chunk if g is None else g, ns, flags, direct, plan, link_gbs)
             x, y = b.io(bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt))
             b.request(x, y, cold=True)
             got = y.cpu()
@@ -386,6 +390,9 @@ def main():
                     help="transfer group size G in bytes, 'default' (the library's) or 'elbow' (this run's sweep)")
     ap.add_argument("--no-sweep", action="store_true", help="skip the group-size sweep")
     ap.add_argument("--copy-streams", type=int, default=0, help="copy streams of the library (0: its default)")
+    ap.add_argument("--plan", choices=["cost", "greedy"], default="cost",
+                    help="chunk plan: cost model (boundaries minimising the modelled completion time, with the "
+                         "measured link rate) or the greedy >= G rule")
     ap.add_argument("--tenants", type=int, default=0, metavar="N_REQUESTS",
                     help="run the multi-tenant open-loop workload with this many requests instead")
     ap.add_argument("--tenant-models", type=int, default=100)
@@ -418,7 +425,7 @@ def main():
     if a.ablation:
         import paper_2306_03622_amd as tp
         link = link_peak(torch, dev)
-        print(json.dumps({"ablation": ablation(torch, dev, tp.DEFAULT_CHUNK), "link_peak_gbs": round(link, 2),
+        print(json.dumps({"ablation": ablation(torch, dev, tp.DEFAULT_CHUNK, link), "link_peak_gbs": round(link, 2),
                           "group_bytes": tp.DEFAULT_CHUNK}), flush=True)
         return
 
@@ -462,7 +469,7 @@ def main():
     if method == "auto":
         rates = {}
         for meth in ("memcpy", "gather"):
-            b = Bench(torch, dev, model, batches, meth, a.chunk, a.copy_streams)
+            b = Bench(torch, dev, model, batches, meth, a.chunk, a.copy_streams, plan=a.plan, link_gbs=link)
             b.swap_only()
             rates[meth] = model.total_bytes / (p50([b.swap_only() for _ in range(5)]) / 1e3) / 1e9
             b.close()
@@ -470,7 +477,8 @@ def main():
         extra["swap_rate_by_method_gbs"] = {k: round(v, 2) for k, v in rates.items()}
         log(f"  swap rates {rates} -> {method}")
 
-    b = Bench(torch, dev, model, batches, method, a.chunk, a.copy_streams)
+    b = Bench(torch, dev, model, batches, method, a.chunk, a.copy_streams, plan=a.plan, link_gbs=link)
+    n_chunks = len(b.rt.chunks(b.mid))
     results = {}
     for bt in batches:
         log(f"cold/warm requests, batch {bt}")
@@ -512,7 +520,7 @@ def main():
         for cfg, bts in ((1, [1]), (3, [1, 8]), (4, [1, 8])):
             m = synth.config_model(cfg)
             log(f"workload {cfg}")
-            bb = Bench(torch, dev, m, bts, method, a.chunk, a.copy_streams)
+            bb = Bench(torch, dev, m, bts, method, a.chunk, a.copy_streams, plan=a.plan, link_gbs=link)
             for bt in bts:
                 rr = measure(bb, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt), a.steps, a.warmup,
                              max(4 * a.steps, 100))
@@ -521,7 +529,8 @@ def main():
                 fl = forward_flops(m, bt)
                 fwd = bb.event_time_ms(rr["x"], rr["out"], 20)
                 extra[f"cfg{cfg}_b{bt}"] = {
-                    "weight_bytes": m.total_bytes, "cold_p50_ms": round(p50(rr["cold"]), 4),
+                    "weight_bytes": m.total_bytes, "chunks": len(bb.rt.chunks(bb.mid)),
+                    "cold_p50_ms": round(p50(rr["cold"]), 4),
                     "warm_p50_ms": round(wp, 4), "bound_ms": round(bnd, 4),
                     "cold_over_bound": round(p50(rr["cold"]) / bnd, 4),
                     "swap_only_gbs": round(m.total_bytes / (p50(rr["swap"]) / 1e3) / 1e9, 2),
@@ -543,7 +552,8 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"24-layer MLP, hidden 4096, bf16 weights (805,502,976 B) swapped cold from pinned "
                                f"host memory, batch {B}", "batch": B, "copy_method": method,
-                   "chunk_min_bytes": a.chunk, "copy_streams": a.copy_streams or 1,
+                   "chunk_plan": a.plan, "chunks": n_chunks,
+                   "chunk_min_bytes": a.chunk if a.plan == "greedy" else None, "copy_streams": a.copy_streams or 1,
                    "direct_max_bytes": tp.DEFAULT_DIRECT},
         "bound_ms": round(bound, 3), "cold_over_bound": round(cold_p50 / bound, 4),
         "swap_gbs": round(swap_gbs, 2), "link_peak_gbs": round(link, 2), "link_theoretical_gbs": PCIE5_X16_GBS,

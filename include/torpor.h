@@ -110,8 +110,13 @@ enum {
 
 /* Context configuration. arena_dev/work_dev are caller-owned device buffers that must
  * stay valid until tp_destroy; the library never frees them. copy_stream: the primary
- * copy stream (NULL: the library creates and later destroys one non-blocking stream);
- * with copy_streams == 2 the library adds a second non-blocking stream and alternates
+ * copy stream (NULL: the library creates and later destroys one). Streams the library
+ * creates for copies are given a hardware queue of their own (a stream with a full CU
+ * mask), because a copy stream that shares the compute stream's hardware queue serialises
+ * the swap behind the kernels; they synchronise with the legacy null stream, so requests
+ * should run on created streams. A caller-supplied copy_stream should likewise not share
+ * the compute stream's hardware queue.
+ * With copy_streams == 2 the library adds a second such stream and alternates
  * chunks between the two, forked from the primary after every ordering wait (0 or 1:
  * one stream, so chunks arrive in first-use order at the full link rate).
  * chunk_min_bytes is the transfer group size G (0 = one chunk per layer). copy_method:
@@ -126,7 +131,20 @@ enum {
  * for its first chunk, and the copy stream swaps the model in behind it; the next request
  * for the model waits for that swap. This removes the copy engine's start-up and hand-off
  * latency from the cold path of models small enough that it dominates. It applies with
- * one copy stream and copy_method TP_COPY_MEMCPY or TP_COPY_GATHER only. */
+ * one copy stream and copy_method TP_COPY_MEMCPY or TP_COPY_GATHER only.
+ *
+ * plan chooses how a model's layers are grouped into transfers (chunks):
+ *   TP_PLAN_GREEDY: the paper's rule (Sec. 4.3): whole layers in first-use order, a chunk
+ *     closed at the first layer boundary where it holds >= chunk_min_bytes, the group size
+ *     at the elbow of transfer throughput.
+ *   TP_PLAN_COST: the boundaries that minimise a model of the cold request's completion
+ *     time: copies back to back, each costing chunk_us (0: 15) plus its bytes at link_gbs
+ *     (0: 57 GB/s); a layer starts when the previous one has finished and its chunk has
+ *     landed; layer times from the library's per-kernel estimate at plan_batch samples
+ *     (0: 1). Small chunks where compute could start early or would finish late, large
+ *     ones where the link is the bottleneck. chunk_min_bytes is ignored, and so is
+ *     TP_FLAG_PER_TENSOR. */
+enum { TP_PLAN_GREEDY = 0, TP_PLAN_COST = 1 };
 typedef struct {
   void* arena_dev;
   uint64_t arena_bytes;
@@ -140,6 +158,10 @@ typedef struct {
   int32_t throttle_us;
   int32_t copy_streams;
   uint64_t direct_max_bytes;
+  int32_t plan;           /* TP_PLAN_* */
+  int32_t plan_batch;
+  float link_gbs;
+  float chunk_us;
 } tp_config;
 
 typedef struct {

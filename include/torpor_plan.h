@@ -30,6 +30,27 @@ TP_API tp_status tph_validate(const tp_model_desc* desc, uint64_t host_bytes);
 TP_API tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes, int32_t flags,
                    uint64_t* begin, uint64_t* end, uint32_t* first_layer, uint32_t cap, uint32_t* n);
 
+/* The cost-model chunk plan of TP_PLAN_COST for this model at plan_batch samples, with
+ * link_gbs and chunk_us as in tp_config (0: defaults); same outputs as tph_plan, plus the
+ * modelled completion time in *est_us (may be NULL). */
+TP_API tp_status tph_plan_cost_model(const tp_model_desc* desc, uint64_t host_bytes, int32_t plan_batch, float link_gbs,
+                              float chunk_us, uint64_t* begin, uint64_t* end, uint32_t* first_layer, uint32_t cap,
+                              uint32_t* n, double* est_us);
+
+/* The grouping of TP_PLAN_COST over explicit units: n_units units starting at host offsets
+ * unit_begin[] (increasing, unit_begin[0] = 0) of a buffer of total_bytes bytes, running
+ * for unit_us[] microseconds each; link_bytes_per_us, chunk_us and wait_us model the copies
+ * and hand-offs (all > 0 except wait_us >= 0). Writes the first unit of each chunk (up to
+ * cap), the chunk count and the modelled completion time. */
+TP_API tp_status tph_plan_cost(const uint64_t* unit_begin, const double* unit_us, uint32_t n_units, uint64_t total_bytes,
+                        double link_bytes_per_us, double chunk_us, double wait_us, uint32_t* first_unit, uint32_t cap,
+                        uint32_t* n_chunks, double* est_us);
+
+/* Per-layer time estimate (us) of the cost model at `batch` samples; *n receives the layer
+ * count, up to cap values are written. */
+TP_API tp_status tph_layer_costs(const tp_model_desc* desc, uint64_t host_bytes, int32_t batch, double* us, uint32_t cap,
+                          uint32_t* n);
+
 struct tph_arena;
 /* An arena of `capacity` bytes whose extents are rounded up to `align` (power of two). */
 TP_API tp_status tph_arena_create(uint64_t capacity, uint64_t align, struct tph_arena** out);

@@ -11,9 +11,10 @@ the host copy of a model is always kept (Sec. 4.3, "Model eviction"), and swappi
 relocates memory blocks whose internal offsets are unchanged (Sec. 4.4, "Memory address
 management"). So the oracle is the plain forward pass of each model from the same weight
 bytes (``forward``), plus the byte-level placement and eviction rules (``arena_sim``) and
-the transfer grouping rule (``chunks``).
+the transfer grouping rule (``chunks``) and the modelled time of a pipelined request
+under a grouping (``pipeline``).
 
 Precision: float64 by default (the paper fixes none); ``dt=np.float32`` gives the fp32
 variant. bf16 weights and inputs are widened exactly.
 """
-from . import ops, forward, arena_sim, chunks  # noqa: F401
+from . import ops, forward, arena_sim, chunks, pipeline  # noqa: F401

@@ -233,6 +233,144 @@ std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes, bool per_
   return out;
 }
 
+double plan_time(const std::vector<uint64_t>& unit_begin, uint64_t total_bytes, const std::vector<double>& layer_us,
+                 const LinkModel& lm, const std::vector<uint32_t>& first) {
+  const size_t n = unit_begin.size(), nc = first.size();
+  double copy_end = 0.0, done = 0.0;
+  for (size_t c = 0; c < nc; ++c) {
+    const uint32_t u0 = first[c], u1 = c + 1 < nc ? first[c + 1] : (uint32_t)n;
+    const uint64_t b0 = c == 0 ? 0 : unit_begin[u0], b1 = c + 1 < nc ? unit_begin[u1] : total_bytes;
+    copy_end += lm.chunk_us + (double)(b1 - b0) / lm.link_bytes_per_us;
+    done = std::max(done, copy_end + lm.wait_us);
+    for (uint32_t u = u0; u < u1; ++u) done += layer_us[u];
+  }
+  return done;
+}
+
+std::vector<uint32_t> plan_cost(const std::vector<uint64_t>& unit_begin, uint64_t total_bytes,
+                                const std::vector<double>& layer_us, const LinkModel& lm, double* est_us) {
+  // F[k][j]: earliest modelled finish of units [0, j) split into k chunks, the k-th ending
+  // at unit j. The k-th chunk lands at A = k * chunk_us + begin(j) / rate whatever its own
+  // start, so F[k][j] = min_i max(F[k-1][i], A + wait) + T(i, j).
+  const size_t n = unit_begin.size();
+  std::vector<double> T(n + 1, 0.0);
+  for (size_t u = 0; u < n; ++u) T[u + 1] = T[u] + layer_us[u];
+  auto bytes_to = [&](size_t j) { return j == n ? total_bytes : unit_begin[j]; };
+  const double inf = 1e300;
+  std::vector<double> F((n + 1) * (n + 1), inf);
+  std::vector<uint32_t> arg((n + 1) * (n + 1), 0);
+  auto at = [&](size_t k, size_t j) -> size_t { return k * (n + 1) + j; };
+  F[at(0, 0)] = 0.0;
+  for (size_t k = 1; k <= n; ++k)
+    for (size_t j = k; j <= n; ++j) {
+      const double land = (double)k * lm.chunk_us + (double)bytes_to(j) / lm.link_bytes_per_us + lm.wait_us;
+      double best = inf;
+      uint32_t bi = 0;
+      for (size_t i = k - 1; i < j; ++i) {
+        const double f = F[at(k - 1, i)];
+        if (f >= inf) continue;
+        const double v = std::max(f, land) + (T[j] - T[i]);
+        if (v < best) { best = v; bi = (uint32_t)i; }
+      }
+      F[at(k, j)] = best;
+      arg[at(k, j)] = bi;
+    }
+  double best = inf;
+  for (size_t k = 1; k <= n; ++k) best = std::min(best, F[at(k, n)]);
+  size_t kb = 1;
+  while (F[at(kb, n)] > best + 1e-6 * (1.0 + best)) ++kb;   // fewest chunks among the optima
+  std::vector<uint32_t> first(kb);
+  size_t j = n;
+  for (size_t k = kb; k >= 1; --k) {
+    const uint32_t i = arg[at(k, j)];
+    first[k - 1] = i;
+    j = i;
+  }
+  if (est_us) *est_us = F[at(kb, n)];
+  return first;
+}
+
+namespace {
+
+// sustained rates of the layer kernels for the cost model (MI355X, bf16 MFMA kernels of
+// this library at the shapes of the model families; measured per kernel)
+constexpr double kKernelUs = 7.0;            // launch, fill and drain of one dependent kernel
+constexpr double kFlopPerUs = 200.0e6;       // 200 TFLOP/s
+constexpr double kBytePerUs = 3.5e6;         // 3.5 TB/s
+
+double kernel_us(double flops, double bytes) { return kKernelUs + flops / kFlopPerUs + bytes / kBytePerUs; }
+
+}  // namespace
+
+std::vector<double> layer_cost_us(const ModelSpec& m, int32_t batch) {
+  const double B = std::max(batch, 1);
+  std::vector<double> t(m.n_layers, 0.0);
+  switch (m.arch) {
+    case TP_ARCH_MLP: {
+      const double W = m.dims[1], esz = m.dtype == TP_F32 ? 4 : 2;
+      for (auto& v : t) v = kernel_us(2 * B * W * W, W * W * esz + 2 * B * W * esz);
+      break;
+    }
+    case TP_ARCH_RESNET50: {
+      const auto g = resnet50_geometry(m.dims[1]);
+      for (size_t l = 0; l < g.size() && l < t.size(); ++l) {
+        const ConvGeom& c = g[l];
+        const double hw_in = (double)c.hin * c.hin, hw_out = (double)c.hout * c.hout;
+        const double k2 = (double)c.c.k * c.c.k;
+        t[l] = kernel_us(2 * B * hw_out * c.c.cout * k2 * c.c.cin,
+                         2 * (c.c.cout * k2 * c.c.cin + B * hw_in * c.c.cin + B * hw_out * c.c.cout));
+      }
+      // conv1 is followed by the max-pool; the FC by nothing but is preceded by the avg-pool
+      const ConvGeom& c0 = g[0];
+      const int hp = (c0.hout + 2 - 3) / 2 + 1;
+      t[0] += kernel_us(0, 2 * B * c0.c.cout * ((double)c0.hout * c0.hout + (double)hp * hp));
+      const double cls = m.dims[0];
+      const ConvGeom& gl = g.back();
+      t.back() = kernel_us(0, 2 * B * 2048 * ((double)gl.hout * gl.hout + 1)) +
+                 kernel_us(2 * B * 2048 * cls, 2 * (2048 * cls + B * 2048) + 4 * B * cls);
+      break;
+    }
+    case TP_ARCH_BERT: {
+      const double d = m.dims[1], F = m.dims[3], S = m.dims[4], M = B * S;
+      t[0] = kernel_us(0, M * d * 8);
+      for (size_t l = 1; l < t.size(); ++l)
+        t[l] = kernel_us(2 * M * d * 3 * d, 2 * (3 * d * d + M * d + 3 * M * d)) +        // QKV
+               kernel_us(4 * B * S * S * d, 2 * (3 * M * d + M * d)) +                    // attention
+               kernel_us(2 * M * d * d, 2 * (d * d + M * d) + 8 * M * d) +                 // O + residual
+               kernel_us(0, 6 * M * d) +                                                 // LN
+               kernel_us(2 * M * d * F, 2 * (d * F + M * d + M * F)) +                   // FFN1
+               kernel_us(2 * M * F * d, 2 * (d * F + M * F) + 8 * M * d) +               // FFN2 + residual
+               kernel_us(0, 6 * M * d);                                                  // LN
+      break;
+    }
+  }
+  return t;
+}
+
+std::vector<Chunk> plan_chunks_cost(const ModelSpec& m, int32_t batch, const LinkModel& lm, double* est_us) {
+  // one unit per layer, starting at the layer's first tensor (unit 0 at byte 0)
+  std::vector<uint64_t> begin;
+  std::vector<uint32_t> layer_of;
+  for (const auto& t : m.tensors)
+    if (begin.empty() || layer_of.back() != t.layer) {
+      begin.push_back(begin.empty() ? 0 : t.offset);
+      layer_of.push_back(t.layer);
+    }
+  const std::vector<double> all = layer_cost_us(m, batch);
+  std::vector<double> us(layer_of.size());
+  for (size_t u = 0; u < us.size(); ++u) us[u] = all[layer_of[u]];
+  const std::vector<uint32_t> first = plan_cost(begin, m.host_bytes, us, lm, est_us);
+  std::vector<Chunk> out(first.size());
+  for (size_t c = 0; c < first.size(); ++c) {
+    const uint32_t u1 = c + 1 < first.size() ? first[c + 1] : (uint32_t)begin.size();
+    out[c].begin = c == 0 ? 0 : begin[first[c]];
+    out[c].end = c + 1 < first.size() ? begin[u1] : m.host_bytes;
+    out[c].first_layer = layer_of[first[c]];
+    out[c].last_layer = layer_of[u1 - 1];
+  }
+  return out;
+}
+
 uint64_t workspace_bytes(const ModelSpec& m, int32_t batch) {
   return activation_bytes(m, batch) + (m.dtype == TP_BF16 ? kSplitScratch : 0);
 }

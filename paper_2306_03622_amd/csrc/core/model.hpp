@@ -56,6 +56,33 @@ tp_status validate_model(const tp_model_desc* d, uint64_t host_bytes, ModelSpec*
 // last_layer are the layers of a chunk's first and last tensor.
 std::vector<Chunk> plan_chunks(const ModelSpec& m, uint64_t min_bytes, bool per_tensor = false);
 
+// Pipeline-aware grouping. Model of a cold request: chunk copies run back to back on one
+// copy stream, each costing chunk_us plus its bytes at link_bytes_per_us; a layer's kernels
+// start when the previous layer has finished and, for the first layer of a chunk, wait_us
+// after that chunk has landed; layer l then runs for layer_us[l]. Over the units (layers)
+// starting at host offsets unit_begin[0..n) (unit 0 at byte 0) of a buffer of total_bytes,
+// plan_cost picks the chunk boundaries that minimise the modelled completion time (ties:
+// fewer chunks) by dynamic programming, and returns the first unit of every chunk.
+struct LinkModel {
+  double link_bytes_per_us = 57.0e3;   // bytes per microsecond (57 GB/s)
+  double chunk_us = 15.0;              // fixed cost of one copy and its event
+  double wait_us = 5.0;                // from a chunk's event to the first kernel that waits for it
+};
+std::vector<uint32_t> plan_cost(const std::vector<uint64_t>& unit_begin, uint64_t total_bytes,
+                                const std::vector<double>& layer_us, const LinkModel& lm, double* est_us);
+
+// Modelled completion time of a given grouping (chunk c starts at unit first[c]).
+double plan_time(const std::vector<uint64_t>& unit_begin, uint64_t total_bytes, const std::vector<double>& layer_us,
+                 const LinkModel& lm, const std::vector<uint32_t>& first);
+
+// Estimated time (us) of each layer's kernels for a batch of `batch` samples: per kernel a
+// fixed launch-and-drain cost plus its FLOPs and bytes at sustained rates of the layer
+// kernels. Coarse by design: the plan only needs compute and transfer in proportion.
+std::vector<double> layer_cost_us(const ModelSpec& m, int32_t batch);
+
+// plan_cost over the model's layers with layer_cost_us(batch), as chunks tiling the buffer.
+std::vector<Chunk> plan_chunks_cost(const ModelSpec& m, int32_t batch, const LinkModel& lm, double* est_us = nullptr);
+
 // Activation buffers of the executors for `batch` samples (each buffer 256-aligned).
 uint64_t activation_bytes(const ModelSpec& m, int32_t batch);
 

@@ -39,6 +39,67 @@ tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chun
   return ok();
 }
 
+tp_status tph_plan_cost_model(const tp_model_desc* desc, uint64_t host_bytes, int32_t plan_batch, float link_gbs,
+                              float chunk_us, uint64_t* begin, uint64_t* end, uint32_t* first_layer, uint32_t cap,
+                              uint32_t* n, double* est_us) {
+  ModelSpec m;
+  std::string err;
+  tp_status s = validate_model(desc, host_bytes, &m, &err);
+  if (s != TP_OK) return fail(s, err);
+  if (!n || plan_batch < 0 || link_gbs < 0 || chunk_us < 0) return fail(TP_E_INVAL, "tph_plan_cost_model: bad argument");
+  LinkModel lm;
+  if (link_gbs > 0) lm.link_bytes_per_us = link_gbs * 1e3;
+  if (chunk_us > 0) lm.chunk_us = chunk_us;
+  double est = 0;
+  const auto plan = plan_chunks_cost(m, plan_batch > 0 ? plan_batch : 1, lm, &est);
+  *n = (uint32_t)plan.size();
+  for (uint32_t i = 0; i < plan.size() && i < cap; ++i) {
+    if (begin) begin[i] = plan[i].begin;
+    if (end) end[i] = plan[i].end;
+    if (first_layer) first_layer[i] = plan[i].first_layer;
+  }
+  if (est_us) *est_us = est;
+  return ok();
+}
+
+tp_status tph_plan_cost(const uint64_t* unit_begin, const double* unit_us, uint32_t n_units, uint64_t total_bytes,
+                        double link_bytes_per_us, double chunk_us, double wait_us, uint32_t* first_unit, uint32_t cap,
+                        uint32_t* n_chunks, double* est_us) {
+  if (!unit_begin || !unit_us || !n_chunks || n_units == 0 || n_units > 4096)
+    return fail(TP_E_INVAL, "tph_plan_cost: NULL argument or unit count outside 1..4096");
+  if (!(link_bytes_per_us > 0) || !(chunk_us > 0) || !(wait_us >= 0)) return fail(TP_E_INVAL, "tph_plan_cost: bad link model");
+  if (unit_begin[0] != 0) return fail(TP_E_INVAL, "tph_plan_cost: unit_begin[0] must be 0");
+  for (uint32_t u = 0; u < n_units; ++u) {
+    if (u && unit_begin[u] <= unit_begin[u - 1]) return fail(TP_E_INVAL, "tph_plan_cost: unit offsets must increase");
+    if (!(unit_us[u] >= 0)) return fail(TP_E_INVAL, "tph_plan_cost: negative unit time");
+  }
+  if (total_bytes <= unit_begin[n_units - 1]) return fail(TP_E_INVAL, "tph_plan_cost: total_bytes too small");
+  LinkModel lm;
+  lm.link_bytes_per_us = link_bytes_per_us;
+  lm.chunk_us = chunk_us;
+  lm.wait_us = wait_us;
+  double est = 0;
+  const auto first = plan_cost(std::vector<uint64_t>(unit_begin, unit_begin + n_units), total_bytes,
+                               std::vector<double>(unit_us, unit_us + n_units), lm, &est);
+  *n_chunks = (uint32_t)first.size();
+  for (uint32_t i = 0; first_unit && i < first.size() && i < cap; ++i) first_unit[i] = first[i];
+  if (est_us) *est_us = est;
+  return ok();
+}
+
+tp_status tph_layer_costs(const tp_model_desc* desc, uint64_t host_bytes, int32_t batch, double* us, uint32_t cap,
+                          uint32_t* n) {
+  ModelSpec m;
+  std::string err;
+  tp_status s = validate_model(desc, host_bytes, &m, &err);
+  if (s != TP_OK) return fail(s, err);
+  if (!n || batch < 1) return fail(TP_E_INVAL, "tph_layer_costs: bad argument");
+  const auto t = layer_cost_us(m, batch);
+  *n = (uint32_t)t.size();
+  for (uint32_t i = 0; us && i < t.size() && i < cap; ++i) us[i] = t[i];
+  return ok();
+}
+
 tp_status tph_arena_create(uint64_t capacity, uint64_t align, tph_arena** out) {
   if (!out || align == 0 || (align & (align - 1))) return fail(TP_E_INVAL, "tph_arena_create: bad arguments");
   *out = new (std::nothrow) tph_arena(capacity, align);

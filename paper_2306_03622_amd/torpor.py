@@ -25,6 +25,7 @@ TP_ARCH_MLP, TP_ARCH_RESNET50, TP_ARCH_BERT = 0, 1, 2
 TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
 TP_COPY_MEMCPY, TP_COPY_GATHER, TP_COPY_PAGEABLE, TP_COPY_ZERO = 0, 1, 2, 3
 TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR, TP_FLAG_TRACE = 1, 2, 4, 8, 16, 32
+TP_PLAN_GREEDY, TP_PLAN_COST = 0, 1
 ROLES = {
     "w": 0, "b": 1,
     "tok_emb": 10, "pos_emb": 11, "type_emb": 12, "emb_ln_g": 13, "emb_ln_b": 14,
@@ -55,7 +56,8 @@ class tp_config(C.Structure):
     _fields_ = [("arena_dev", C.c_void_p), ("arena_bytes", C.c_uint64), ("work_dev", C.c_void_p),
                 ("work_bytes", C.c_uint64), ("copy_stream", C.c_void_p), ("chunk_min_bytes", C.c_uint64),
                 ("copy_method", C.c_int32), ("gather_wgs", C.c_int32), ("flags", C.c_int32),
-                ("throttle_us", C.c_int32), ("copy_streams", C.c_int32), ("direct_max_bytes", C.c_uint64)]
+                ("throttle_us", C.c_int32), ("copy_streams", C.c_int32), ("direct_max_bytes", C.c_uint64),
+                ("plan", C.c_int32), ("plan_batch", C.c_int32), ("link_gbs", C.c_float), ("chunk_us", C.c_float)]
 
 
 class tp_arena_stats_t(C.Structure):
@@ -113,6 +115,13 @@ _SIGS = {
     "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
     "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                  C.POINTER(C.c_uint32), C.c_uint32, C.POINTER(C.c_uint32)],
+    "tph_plan_cost_model": [C.POINTER(tp_model_desc), C.c_uint64, C.c_int32, C.c_float, C.c_float,
+                            C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint32), C.c_uint32,
+                            C.POINTER(C.c_uint32), C.POINTER(C.c_double)],
+    "tph_plan_cost": [C.POINTER(C.c_uint64), C.POINTER(C.c_double), C.c_uint32, C.c_uint64, C.c_double, C.c_double,
+                      C.c_double, C.POINTER(C.c_uint32), C.c_uint32, C.POINTER(C.c_uint32), C.POINTER(C.c_double)],
+    "tph_layer_costs": [C.POINTER(tp_model_desc), C.c_uint64, C.c_int32, C.POINTER(C.c_double), C.c_uint32,
+                        C.POINTER(C.c_uint32)],
     "tph_arena_create": [C.c_uint64, C.c_uint64, C.POINTER(_P)],
     "tph_arena_destroy": [_P],
     "tph_arena_register": [_P, C.c_int32, C.c_uint64],
@@ -218,10 +227,12 @@ class ModelDesc:
 # ------------------------------------------------------------------ C calls
 
 def tp_create(arena_dev, arena_bytes, work_dev, work_bytes, copy_stream=None, chunk_min_bytes=DEFAULT_CHUNK,
-              copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0, copy_streams=0, direct_max_bytes=0):
+              copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0, copy_streams=0, direct_max_bytes=0,
+              plan=TP_PLAN_GREEDY, plan_batch=0, link_gbs=0.0, chunk_us=0.0):
     L = lib()
     cfg = tp_config(_ptr(arena_dev), arena_bytes, _ptr(work_dev), work_bytes, _ptr(copy_stream), chunk_min_bytes,
-                    copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes)
+                    copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes, plan, plan_batch,
+                    link_gbs, chunk_us)
     ctx = _P()
     _check(L, L.tp_create(C.byref(cfg), C.byref(ctx)))
     return ctx
@@ -338,6 +349,42 @@ def tph_plan(desc: ModelDesc, host_bytes: int, chunk_min_bytes: int, flags: int 
     return [{"begin": b[i], "end": e[i], "first_layer": f[i]} for i in range(n.value)]
 
 
+def tph_plan_cost_model(desc: ModelDesc, host_bytes: int, plan_batch: int = 1, link_gbs: float = 0.0,
+                        chunk_us: float = 0.0, L=None):
+    """The TP_PLAN_COST chunk plan of a model: (chunks as tph_plan returns them, modelled us)."""
+    L = L or lib()
+    n, est = C.c_uint32(), C.c_double()
+    _check(L, L.tph_plan_cost_model(C.byref(desc.desc), host_bytes, plan_batch, link_gbs, chunk_us, None, None, None, 0,
+                                    C.byref(n), None))
+    b, e, f = (C.c_uint64 * n.value)(), (C.c_uint64 * n.value)(), (C.c_uint32 * n.value)()
+    _check(L, L.tph_plan_cost_model(C.byref(desc.desc), host_bytes, plan_batch, link_gbs, chunk_us, b, e, f, n.value,
+                                    C.byref(n), C.byref(est)))
+    return [{"begin": b[i], "end": e[i], "first_layer": f[i]} for i in range(n.value)], est.value
+
+
+def tph_plan_cost(unit_begin, unit_us, total_bytes: int, link_bytes_per_us: float, chunk_us: float, wait_us: float,
+                  L=None):
+    """Cost-model grouping over explicit units: (first unit of each chunk, modelled us)."""
+    L = L or lib()
+    nu = len(unit_begin)
+    ub = (C.c_uint64 * nu)(*[int(v) for v in unit_begin])
+    us = (C.c_double * nu)(*[float(v) for v in unit_us])
+    first = (C.c_uint32 * nu)()
+    n, est = C.c_uint32(), C.c_double()
+    _check(L, L.tph_plan_cost(ub, us, nu, total_bytes, link_bytes_per_us, chunk_us, wait_us, first, nu, C.byref(n),
+                              C.byref(est)))
+    return [first[i] for i in range(n.value)], est.value
+
+
+def tph_layer_costs(desc: ModelDesc, host_bytes: int, batch: int, L=None):
+    L = L or lib()
+    n = C.c_uint32()
+    _check(L, L.tph_layer_costs(C.byref(desc.desc), host_bytes, batch, None, 0, C.byref(n)))
+    out = (C.c_double * n.value)()
+    _check(L, L.tph_layer_costs(C.byref(desc.desc), host_bytes, batch, out, n.value, C.byref(n)))
+    return list(out)
+
+
 class HostArena:
     """tph_arena_*: the arena bookkeeping without a device."""
 
@@ -379,7 +426,8 @@ class Runtime:
 
     def __init__(self, arena_bytes: int, work_bytes: int, device: int = 0, chunk_min_bytes: int = DEFAULT_CHUNK,
                  copy_method: int = TP_COPY_MEMCPY, gather_wgs: int = 0, flags: int = 0, throttle_us: int = 0,
-                 copy_stream=None, copy_streams: int = 0, direct_max_bytes: int = DEFAULT_DIRECT):
+                 copy_stream=None, copy_streams: int = 0, direct_max_bytes: int = DEFAULT_DIRECT,
+                 plan: int = TP_PLAN_GREEDY, plan_batch: int = 0, link_gbs: float = 0.0, chunk_us: float = 0.0):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("libtorpor needs a HIP device")
@@ -390,7 +438,8 @@ class Runtime:
         self.work = torch.empty(max(work_bytes, 256), dtype=torch.uint8, device=self.device)
         self.copy_stream = copy_stream
         self.ctx = tp_create(self.arena, arena_bytes, self.work, self.work.numel(), copy_stream, chunk_min_bytes,
-                             copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes)
+                             copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes, plan,
+                             plan_batch, link_gbs, chunk_us)
         self.descs = {}
 
     def close(self):

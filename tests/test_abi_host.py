@@ -26,7 +26,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 25, sorted(names)
+    assert len(names) == 28, sorted(names)
     L = tp.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -166,3 +166,69 @@ def test_blocked_layout_definition():
     # group j = 1 starts at 512: row 0, columns 32..39
     assert p[512:520].tolist() == list(range(32, 40))
     assert sorted(p.tolist()) == list(range(16 * 128))
+
+
+def _random_instance(rng, n):
+    sizes = rng.integers(1, 200, size=n) * 256
+    begin = np.concatenate([[0], np.cumsum(sizes)[:-1]]).tolist()
+    total = int(sizes.sum()) + int(rng.integers(0, 4)) * 256
+    us = (rng.random(n) * rng.choice([1.0, 30.0, 300.0])).tolist()
+    return begin, total, us
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_cost_plan_is_optimal_against_exhaustion(seed):
+    from oracle import pipeline
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 11))
+    begin, total, us = _random_instance(rng, n)
+    rate, o, h = float(rng.choice([50.0, 500.0, 5000.0])), float(rng.choice([1.0, 15.0, 200.0])), float(rng.random() * 10)
+    want_first, want_t = pipeline.best_grouping(begin, total, us, rate, o, h)
+    for L in (tp.lib(), tp.host_lib()):
+        first, est = tp.tph_plan_cost(begin, us, total, rate, o, h, L=L)
+        # the library's modelled time is the oracle's time of the library's grouping, and no
+        # grouping is faster; the number of groups is the fewest among the fastest
+        assert est == pytest.approx(pipeline.simulate(begin, total, us, first, rate, o, h), rel=1e-9, abs=1e-9)
+        assert est <= want_t * (1 + 1e-9) + 1e-9
+        assert len(first) <= len(want_first)
+
+
+def test_cost_plan_errors():
+    bad = [([5, 10], [1.0, 1.0], 20),        # unit 0 must start at byte 0
+           ([0, 10, 10], [1.0] * 3, 20),     # offsets must increase
+           ([0, 10], [1.0, -1.0], 20),       # negative time
+           ([0, 10], [1.0, 1.0], 10)]        # the buffer must extend past the last unit
+    for begin, us, total in bad:
+        with pytest.raises(tp.TorporError) as e:
+            tp.tph_plan_cost(begin, us, total, 10.0, 1.0, 1.0, L=tp.host_lib())
+        assert e.value.status == tp.TP_E_INVAL
+    with pytest.raises(tp.TorporError):
+        tp.tph_plan_cost([0], [1.0], 10, 0.0, 1.0, 1.0, L=tp.host_lib())
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+@pytest.mark.parametrize("batch", [1, 8])
+def test_cost_plan_of_workloads(cfg, batch):
+    from oracle import pipeline
+    m = synth.config_model(cfg)
+    d = tp.ModelDesc.of(m)
+    plan, est = tp.tph_plan_cost_model(d, m.total_bytes, batch, 57.0, 15.0, L=tp.host_lib())
+    # chunks tile the buffer at layer starts, in first-use order
+    assert plan[0]["begin"] == 0 and plan[-1]["end"] == m.total_bytes
+    assert all(a["end"] == b["begin"] for a, b in zip(plan, plan[1:]))
+    layer_start = {}
+    for t in m.tensors:
+        layer_start.setdefault(t.layer, t.offset)
+    assert all(c["begin"] == layer_start[c["first_layer"]] for c in plan[1:])
+    # the modelled time is the oracle's simulation of this grouping, and it is no worse than
+    # the greedy plan at the default group size under the same model
+    us = tp.tph_layer_costs(d, m.total_bytes, batch, L=tp.host_lib())
+    begin = [0] + [layer_start[l] for l in range(1, len(us))]
+    first = [c["first_layer"] for c in plan]
+    assert est == pytest.approx(pipeline.simulate(begin, m.total_bytes, us, first, 57e3, 15.0, 5.0), rel=1e-9)
+    greedy = tp.tph_plan(d, m.total_bytes, tp.DEFAULT_CHUNK, 0, L=tp.host_lib())
+    g_first = [c["first_layer"] for c in greedy]
+    assert est <= pipeline.simulate(begin, m.total_bytes, us, g_first, 57e3, 15.0, 5.0) + 1e-6
+    # the transfer alone bounds the modelled time from below
+    assert est >= m.total_bytes / 57e3
+    assert all(u > 0 for u in us)

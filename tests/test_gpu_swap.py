@@ -8,7 +8,8 @@ import pytest
 import paper_2306_03622_amd as tp
 import synth
 from oracle.arena_sim import ArenaSim
-from tests.common import expected_host_image, infer, log, make_runtime, out_shape, to_device, torch_dev
+from tests.common import (check_parity, expected_host_image, infer, log, make_runtime, out_shape, to_device,
+                          torch_dev)
 
 
 def infer_shape(m):
@@ -64,6 +65,32 @@ def test_pipelined_equals_preloaded(method, streams):
     rt.close()
 
 
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_cost_plan_pipelined_equals_preloaded_full_size(cfg):
+    # the cost-model plan groups layers unevenly (tiny head chunks, one large middle chunk);
+    # the pipelined cold request must compute the same bits as the preloaded one, and match
+    # the oracle
+    m = synth.config_model(cfg)
+    batch = 2
+    x = synth.config_input(m, batch, 777)
+    rt, ids = make_runtime([m], batch_max=batch, plan=tp.TP_PLAN_COST, plan_batch=8, link_gbs=57.0)
+    chunks = rt.chunks(ids[0])
+    log(f"cost plan cfg{cfg}: {len(chunks)} chunks, first layers {[c['first_layer'] for c in chunks]}")
+    torch, dev = torch_dev()
+    s = torch.cuda.Stream(device=dev)
+    pipelined = infer(rt, ids[0], m, x, stream=s)
+    rt.evict(ids[0])
+    rt.swap_in(ids[0], stream=s)
+    s.synchronize()
+    preloaded = infer(rt, ids[0], m, x, stream=s)
+    assert np.array_equal(pipelined, preloaded)
+    got = rt.extent(ids[0]).cpu().numpy()
+    assert np.array_equal(got, rt.host_image(ids[0]))
+    rt.close()
+    check_parity(pipelined, m, x, 2e-2)
+    m.drop_blob()
+
+
 def test_warm_graph_replay_equals_kernel_by_kernel():
     # every family with a forward pass long enough (>= 16 launches) to be replayed as a graph
     ms = [synth.mlp(18, 256, "bf16", "gelu", seed=61),
@@ -114,7 +141,8 @@ def test_eviction_order_and_placement_do_not_change_outputs():
     rt.close()
 
 
-def test_throttled_poisoned_swaps_are_bit_identical():
+@pytest.mark.parametrize("plan", [tp.TP_PLAN_GREEDY, tp.TP_PLAN_COST])
+def test_throttled_poisoned_swaps_are_bit_identical(plan):
     ms = _models()
     xs = _inputs(ms)
     ref_rt, ref_ids = make_runtime(ms, batch_max=2)
@@ -124,7 +152,8 @@ def test_throttled_poisoned_swaps_are_bit_identical():
     # would read 0xFF bytes (NaN) left by the poisoned eviction of the previous tenant
     arena = max(m.total_bytes for m in ms) + 4096
     rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, chunk_min_bytes=0,
-                           flags=tp.TP_FLAG_POISON | tp.TP_FLAG_THROTTLE, throttle_us=200)
+                           flags=tp.TP_FLAG_POISON | tp.TP_FLAG_THROTTLE, throttle_us=200, plan=plan,
+                           link_gbs=0.5, chunk_us=1.0)
     for rep in range(2):
         for k in range(3):
             got = infer(rt, ids[k], ms[k], xs[k])

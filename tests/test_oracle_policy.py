@@ -104,3 +104,44 @@ def test_chunk_plans_of_workloads():
     pt = chunks.plan([(x.layer, x.offset, x.nbytes) for x in m3.tensors], m3.total_bytes, 0, per_tensor=True)
     assert len(pt) == len(m3.tensors) == 108
     assert [c["begin"] for c in pt[1:]] == [x.offset for x in m3.tensors[1:]]
+
+
+# ------------------------------------------------------------------ pipelined request model
+
+from oracle import pipeline
+
+
+def test_pipeline_simulation_closed_forms():
+    begin, total = [0, 100, 300, 600], 1000          # units of 100, 200, 300, 400 B
+    us = [5.0, 7.0, 11.0, 13.0]
+    r, o, h = 10.0, 3.0, 2.0                         # 10 B/us, 3 us per copy, 2 us hand-off
+    # one group: everything lands at o + 1000 / r, then all layers run
+    assert pipeline.simulate(begin, total, us, [0], r, o, h) == pytest.approx(3 + 100 + 2 + 36)
+    # no compute: k groups cost k fixed costs plus the bytes, then the hand-off
+    z = [0.0] * 4
+    assert pipeline.simulate(begin, total, z, [0, 1, 2, 3], r, o, h) == pytest.approx(4 * 3 + 100 + 2)
+    assert pipeline.simulate(begin, total, z, [0, 2], r, o, h) == pytest.approx(2 * 3 + 100 + 2)
+    # hand-worked: groups {0,1} (300 B) and {2,3} (700 B)
+    # group 0 lands at 3 + 30 = 33, layers 0-1 run 35 .. 47; group 1 lands at 33 + 3 + 70 = 106,
+    # layers 2-3 run 108 .. 132
+    assert pipeline.simulate(begin, total, us, [0, 2], r, o, h) == pytest.approx(132.0)
+    # compute-bound: with a fast link the time is the first hand-off plus all layers, plus
+    # the idle gap of any group that lands after its predecessor's layers finish
+    fast = pipeline.simulate(begin, total, [100.0] * 4, [0, 1, 2, 3], 1e9, 1.0, 0.5)
+    assert fast == pytest.approx(1.0 + 0.5 + 400.0)
+
+
+def test_best_grouping_hand_worked():
+    # two heavy-compute layers up front and a big last layer: the first layer goes alone so
+    # it computes while the rest streams, the rest stay together (one fixed cost)
+    begin, total = [0, 10, 20], 1010
+    us = [50.0, 50.0, 1.0]
+    first, t = pipeline.best_grouping(begin, total, us, 10.0, 5.0, 0.0)
+    # [0],[1,2]: lands 6 and 6+5+100=111 -> layers run 6..56, 111..162 ; [0],[1],[2]: layer 2's
+    # group lands at 6+6+5+99 = 116 -> 117 ; [0,1],[2]: 7..107, lands 7+5+99=111 -> 112
+    assert first == [0, 1, 2] or first == [0, 2]
+    assert t == pytest.approx(min(pipeline.simulate(begin, total, us, f, 10.0, 5.0, 0.0)
+                                  for f in ([0], [0, 1], [0, 2], [0, 1, 2])))
+    # with a huge fixed cost per copy a single group wins
+    first, _ = pipeline.best_grouping(begin, total, us, 10.0, 1e6, 0.0)
+    assert first == [0]
