@@ -10,8 +10,8 @@
 //
 // Kernels here (the skinny M <= 32 case is in gemv_bf16.hip):
 //   * k_gemm: LDS-tiled BN x BM x BK tiles, 4 waves in a 2 x 2 arrangement, global loads
-//     of the next k-stage issued before the MFMAs of the current one, double-buffered LDS,
-//     and a deterministic split over k when the tile grid alone cannot fill the chip. The
+//     issued several k-stages ahead into a register ring, double-buffered LDS, and a
+//     deterministic split over k when the tile grid alone cannot fill the chip. The
 //     activation loader is either a plain row-major matrix or an NHWC implicit-GEMM
 //     (im2col) gather for convolutions, k = (kh * KW + kw) * C + c, matching OHWI weight
 //     rows.
@@ -132,39 +132,34 @@ struct TapPos {
     kh = tap / a.KW;
     kw = tap - kh * a.KW;
   }
-  __device__ void advance(const GemmArgs& a, int bk) {
-    c0 += bk;
-    if (c0 >= a.C) {
-      c0 = 0;
-      if (++kw == a.KW) {
-        kw = 0;
-        ++kh;
-      }
-    }
-  }
 };
 
-__device__ __forceinline__ uint4 load_x_tap(const GemmArgs& a, const RowInfo& ri, const TapPos& tp, int kq) {
+// The loaders below return the raw 16 bytes of an always-in-bounds load (clamped address)
+// and report in `ok` whether they are real operand data; the caller zeroes invalid ones
+// when it stores them to LDS, stages later. Masking right after the load would make every
+// wave wait for each load as soon as it is issued.
+__device__ __forceinline__ uint4 load_x_tap(const GemmArgs& a, const RowInfo& ri, const TapPos& tp, int kq, bool& ok) {
   const int ih = ri.ih0 + tp.kh, iw = ri.iw0 + tp.kw;
-  const bool ok = ri.valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+  ok = ri.valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
   const size_t off = ri.base + ((size_t)tp.kh * a.W + tp.kw) * a.C + tp.c0 + kq;
-  return mask_u4(*reinterpret_cast<const uint4*>(a.x + (ok ? off : 0)), ok);
+  return *reinterpret_cast<const uint4*>(a.x + (ok ? off : 0));
 }
 
 template <int MODE>
-__device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, int k) {
+__device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, int k, bool& ok) {
   if (MODE == X_ROWS) {
-    const bool ok = ri.valid && k < a.K;
-    return mask_u4(*reinterpret_cast<const uint4*>(a.x + (size_t)ri.b * a.K + (ok ? k : 0)), ok);
+    ok = ri.valid && k < a.K;
+    return *reinterpret_cast<const uint4*>(a.x + (size_t)ri.b * a.K + (ok ? k : 0));
   }
   if (MODE == X_CONV8) {
     const int tap = k / a.C, c = k - tap * a.C;
     const int kh = tap / a.KW, kw = tap - kh * a.KW;
     const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
-    const bool ok = ri.valid && k < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+    ok = ri.valid && k < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
     const size_t off = ok ? (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c : 0;
-    return mask_u4(*reinterpret_cast<const uint4*>(a.x + off), ok);
+    return *reinterpret_cast<const uint4*>(a.x + off);
   }
+  ok = true;                                   // element-wise gather: already zero-filled
   uint32_t v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -180,23 +175,24 @@ __device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, i
 }
 
 // weights in 16 x 128 blocks (N % 16 == 0, K % 128 == 0): element (n, k) of an 8-run
-__device__ __forceinline__ uint4 load_w8_packed(const GemmArgs& a, int n, int k) {
-  const bool ok = n < a.N && k < a.K;
+__device__ __forceinline__ uint4 load_w8_packed(const GemmArgs& a, int n, int k, bool& ok) {
+  ok = n < a.N && k < a.K;
   const int nn = ok ? n : 0, kk = ok ? k : 0;
   const size_t off = ((((size_t)(nn >> 4) * (a.K >> 7) + (kk >> 7)) * 4 + ((kk >> 5) & 3)) * 512) +
                      ((((kk >> 3) & 3) << 4) + (nn & 15)) * 8;
-  return mask_u4(*reinterpret_cast<const uint4*>(a.w + off), ok);
+  return *reinterpret_cast<const uint4*>(a.w + off);
 }
 
-template <bool WVEC>
-__device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
-  if (a.ep.w_packed) return load_w8_packed(a, n, k);
+template <bool WVEC, bool PK>
+__device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k, bool& ok) {
+  if (PK) return load_w8_packed(a, n, k, ok);
   const bool row_ok = n < a.N;
   const uint16_t* p = a.w + (size_t)(row_ok ? n : 0) * a.K;
   if (WVEC) {
-    const bool ok = row_ok && k < a.K;
-    return mask_u4(*reinterpret_cast<const uint4*>(p + (ok ? k : 0)), ok);
+    ok = row_ok && k < a.K;
+    return *reinterpret_cast<const uint4*>(p + (ok ? k : 0));
   }
+  ok = true;                                   // element-wise: already zero-filled
   uint32_t v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -206,19 +202,23 @@ __device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
   return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
-// One BN x BM output tile over the k-stages [s0, s1) of this split (blockIdx.z). Global
-// loads of stage s+1 are issued before the MFMAs of stage s; LDS is double-buffered so
-// one barrier per stage suffices. With a.splits > 1 every split stores its fp32 partial
-// to a.partials and k_split_reduce (the next launch on the stream) sums the partials in
-// split order, which is fixed, so results are bit-reproducible.
-template <int BN, int BM, int BK, int MODE, bool WVEC>
+// One BN x BM output tile over the k-stages [s0, s0 + n) of this split (blockIdx.z). The
+// global loads of a stage are issued D stages before its multiplications, into a ring of D
+// register sets, so D memory round trips overlap (the tiles are small and the contractions
+// short, so latency, not bandwidth, bounds these kernels); LDS is double-buffered, one
+// barrier per stage. Invalid operand data (outside the matrix or the image) is zeroed only
+// when it is stored to LDS, so no wave waits for a load when it issues it. With a.splits > 1
+// every split stores its fp32 partial to a.partials and k_split_reduce (the next launch on
+// the stream) sums the partials in split order, which is fixed, so results are
+// bit-reproducible.
+template <int BN, int BM, int BK, int MODE, bool WVEC, bool PK, int D>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int LDK = BK + 8;
   constexpr int KV = BK / 8;                    // 16-byte vectors per row and stage
   constexpr int RSTEP = 256 / KV;               // rows covered by one pass of 256 threads
   constexpr int VA = BN / RSTEP, VB = BM / RSTEP;
   constexpr int NB = BN / 32, MB = BM / 32;     // 16 x 16 blocks per wave (wave tile BN/2 x BM/2)
-  static_assert(VA >= 1 && VB >= 1 && BK % 32 == 0, "tile shape");
+  static_assert(VA >= 1 && VB >= 1 && BK % 32 == 0 && D >= 2 && D % 2 == 0, "tile shape");
   static_assert(MODE != X_CONV64 || BK == 64, "X_CONV64 steps one 64-deep stage per tap position");
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * (BN + BM) * LDK];
 
@@ -239,40 +239,33 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 
   const int nst = (a.K + BK - 1) / BK;
   const int s0 = blockIdx.z * a.kst;
-  const int s1 = min(s0 + a.kst, nst);
-  uint4 ra[VA], rb[VB];
-  TapPos tap;
-  if (MODE == X_CONV64) tap.init(a, s0 * BK);
-  auto load = [&](int s) {
+  const int n = min(s0 + a.kst, nst) - s0;      // stages of this split (>= 1: no empty split)
+  uint4 ra[D][VA], rb[D][VB];
+  bool oka[D][VA], okb[D][VB];
+  auto load = [&](int s, uint4 (&A)[VA], bool (&OA)[VA], uint4 (&Bv)[VB], bool (&OB)[VB]) {
     const int k = s * BK + kq;
 #pragma unroll
-    for (int p = 0; p < VA; ++p) ra[p] = load_w8<WVEC>(a, n_base + row0 + RSTEP * p, k);
+    for (int p = 0; p < VA; ++p) A[p] = load_w8<WVEC, PK>(a, n_base + row0 + RSTEP * p, k, OA[p]);
     if (MODE == X_CONV64) {
+      TapPos tap;
+      tap.init(a, s * BK);
 #pragma unroll
-      for (int p = 0; p < VB; ++p) rb[p] = load_x_tap(a, ri[p], tap, kq);
-      tap.advance(a, BK);
+      for (int p = 0; p < VB; ++p) Bv[p] = load_x_tap(a, ri[p], tap, kq, OB[p]);
     } else {
 #pragma unroll
-      for (int p = 0; p < VB; ++p) rb[p] = load_x8<MODE>(a, ri[p], k);
+      for (int p = 0; p < VB; ++p) Bv[p] = load_x8<MODE>(a, ri[p], k, OB[p]);
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const uint4 (&A)[VA], const bool (&OA)[VA], const uint4 (&Bv)[VB], const bool (&OB)[VB]) {
     uint16_t* As = lds + buf * (BN + BM) * LDK;
     uint16_t* Bs = As + BN * LDK;
 #pragma unroll
-    for (int p = 0; p < VA; ++p) *reinterpret_cast<uint4*>(&As[(row0 + RSTEP * p) * LDK + kq]) = ra[p];
+    for (int p = 0; p < VA; ++p) *reinterpret_cast<uint4*>(&As[(row0 + RSTEP * p) * LDK + kq]) = mask_u4(A[p], OA[p]);
 #pragma unroll
-    for (int p = 0; p < VB; ++p) *reinterpret_cast<uint4*>(&Bs[(row0 + RSTEP * p) * LDK + kq]) = rb[p];
+    for (int p = 0; p < VB; ++p) *reinterpret_cast<uint4*>(&Bs[(row0 + RSTEP * p) * LDK + kq]) = mask_u4(Bv[p], OB[p]);
   };
-  if (s0 < s1) {
-    load(s0);
-    store(0);
-  }
-  __syncthreads();
-  for (int s = s0; s < s1; ++s) {
-    const int cur = (s - s0) & 1;
-    if (s + 1 < s1) load(s + 1);
-    const uint16_t* As = lds + cur * (BN + BM) * LDK;
+  auto compute = [&](int buf) {
+    const uint16_t* As = lds + buf * (BN + BM) * LDK;
     const uint16_t* Bs = As + BN * LDK;
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 32) {
@@ -289,8 +282,42 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
         for (int j = 0; j < MB; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[i]), as_bf16x8(fb[j]), acc[i][j], 0, 0, 0);
     }
-    if (s + 1 < s1) store(cur ^ 1);
-    __syncthreads();
+  };
+
+  // prologue: stages 0 .. D-1 (relative) into ring slots 0 .. D-1, stage 0 into LDS buffer 0,
+  // then stage D into the freed slot 0
+#pragma unroll
+  for (int i = 0; i < D; ++i)
+    if (i < n) load(s0 + i, ra[i], oka[i], rb[i], okb[i]);
+  store(0, ra[0], oka[0], rb[0], okb[0]);
+  if (D < n) load(s0 + D, ra[0], oka[0], rb[0], okb[0]);
+  __syncthreads();
+  // Stage j sits in ring slot j % D and LDS buffer j % 2; the loops are unrolled by D (even),
+  // so every slot and buffer index is a constant. Steady state: trips whose loads are all
+  // needed, with no branch around any load, so the compiler waits for exactly the stage it
+  // stores. Drain: the last trips, where loads and stores beyond the split are skipped.
+  int j0 = 0;
+  for (; j0 + 2 * D < n; j0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int nx = (u + 1) % D;
+      compute(u & 1);
+      store((u + 1) & 1, ra[nx], oka[nx], rb[nx], okb[nx]);        // stage j0+u+1
+      load(s0 + j0 + u + 1 + D, ra[nx], oka[nx], rb[nx], okb[nx]);  // stage j0+u+1+D
+      __syncthreads();
+    }
+  }
+  for (; j0 < n; j0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int j = j0 + u, nx = (u + 1) % D;
+      if (j < n) {
+        compute(u & 1);
+        if (j + 1 < n) store((u + 1) & 1, ra[nx], oka[nx], rb[nx], okb[nx]);
+        if (j + 1 + D < n) load(s0 + j + 1 + D, ra[nx], oka[nx], rb[nx], okb[nx]);
+        __syncthreads();
+      }
+    }
   }
 
   // Output: the fp32 tile is staged in LDS (row-major [m][n], padded) so that each thread then
@@ -313,6 +340,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int TPR = BN / 16, RPI = 256 / TPR;
   const int nl = (tid % TPR) * 16;
   const int n0 = n_base + nl;
+  const bool vec = n0 + 15 < a.N && (a.N & 3) == 0;
   for (int ml = tid / TPR; ml < BM; ml += RPI) {
     const int m = m_base + ml;
     if (m >= a.M || n0 >= a.N) continue;
@@ -325,7 +353,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     if (a.splits > 1) {
       // fp32 partial of this split: P[split][m][n]
       float* p = a.partials + (size_t)blockIdx.z * a.M * a.N + (size_t)m * a.N + n0;
-      if (n0 + 15 < a.N && (a.N & 3) == 0) {
+      if (vec) {
 #pragma unroll
         for (int h = 0; h < 4; ++h)
           *reinterpret_cast<float4*>(p + 4 * h) = make_float4(v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]);
@@ -492,7 +520,15 @@ __global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
   store_row4(a, m, n0, sum);
 }
 
-template <int BN, int BM, int BK, int MODE, bool WVEC>
+hipError_t reduce_splits(const GemmArgs& a, hipStream_t s) {
+  if (a.splits > 1) {
+    const long groups = (long)a.M * ((a.N + 3) / 4);
+    hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+template <int BN, int BM, int BK, int MODE, bool WVEC, int D>
 hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   const int tn = (a.N + BN - 1) / BN, tm = (a.M + BM - 1) / BM, tiles = tn * tm;
   const int nst = (a.K + BK - 1) / BK;
@@ -511,12 +547,14 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   a.splits = (nst + a.kst - 1) / a.kst;        // no empty split
   a.partials = sp.partials;
   dim3 grid(tn, tm, a.splits);
-  hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC>), grid, dim3(256), 0, s, a);
-  if (a.splits > 1) {
-    const long groups = (long)a.M * ((a.N + 3) / 4);
-    hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, s, a);
+  if constexpr (MODE == X_ROWS) {
+    if (a.ep.w_packed) {
+      hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, true, D>), grid, dim3(256), 0, s, a);
+      return reduce_splits(a, s);
+    }
   }
-  return hipGetLastError();
+  hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, false, D>), grid, dim3(256), 0, s, a);
+  return reduce_splits(a, s);
 }
 
 template <int MODE, bool WVEC>
@@ -524,8 +562,8 @@ hipError_t pick_tiled(const GemmArgs& a, const Split& sp, hipStream_t s) {
   // 64 x 64 tiles keep several workgroups per CU resident (latency hiding by occupancy);
   // 128 x 128 only once the grid has well over a few tiles per CU
   const long tiles128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
-  if (tiles128 >= 1024) return launch_tiled<128, 128, 64, MODE, WVEC>(a, sp, s);
-  return launch_tiled<64, 64, 64, MODE, WVEC>(a, sp, s);
+  if (tiles128 >= 1024) return launch_tiled<128, 128, 64, MODE, WVEC, 2>(a, sp, s);
+  return launch_tiled<64, 64, 64, MODE, WVEC, 4>(a, sp, s);
 }
 
 bool ep_ok(const Epilogue& ep) { return ep.out != nullptr && ep.act >= 0 && ep.act <= 2; }
