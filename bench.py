@@ -502,7 +502,8 @@ def main():
     flops = 2 * B * N * K
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": counted_traffic(B),
-                "kernel": "k_gemv<1,16,packed> (bf16 [B x 4096] x [4096 x 4096]^T + bias, GELU)",
+                "kernel": "k_gemv<1,4,8,true> (bf16 [B x 4096] x [4096 x 4096]^T + bias, GELU; 4 waves x 8 "
+                          "k-blocks, blocked weights)",
                 "avg_launch_us": round(kern_us, 2), "algorithmic_bytes_per_launch": alg_bytes,
                 "mfma_util": round(flops / (kern_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 5)}
 

@@ -30,6 +30,14 @@ __device__ __forceinline__ float act_apply(float v, int act) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load marked non-temporal (data streamed once, not worth keeping in the caches)
+__device__ __forceinline__ uint4 load_nt16(const void* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // branch-free zeroing of a loaded vector (the load itself is always in bounds)
 __device__ __forceinline__ uint4 mask_u4(uint4 v, bool ok) {
   const uint32_t m = ok ? 0xffffffffu : 0u;

@@ -7,6 +7,11 @@
 // rows, so accumulator register e of lane l holds D[n = 4 (l / 16) + e][m = l % 16].
 #include "gemm_args.hpp"
 
+#ifndef GEMV_NW
+#define GEMV_NW 4
+#define GEMV_U 8
+#endif
+
 namespace tp {
 namespace k {
 
@@ -16,7 +21,7 @@ namespace {
 // lane (r, q) in k-block kb reads 16 bytes at block offset j*512 + (q*16 + r)*8 and one
 // load instruction covers a contiguous 1 KB; otherwise rows are [N][K] and an instruction
 // reads 64 contiguous bytes of each of 16 rows. Activation rows beyond M issue no load.
-template <int MT, int NW, bool PK>
+template <int MT, int NW, int U, bool PK>
 __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, q = lane >> 4;
@@ -36,21 +41,28 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
   f32x4 acc[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // the epilogue's bias, fetched now (raw bits, converted at the end) so that its latency
+  // hides behind the weight stream
+  const int nst = n0 + (q << 2);
+  const bool bias_pre = wave < MT && a.ep.bias && nst + 3 < a.N && (a.N & 3) == 0;
+  uint2 braw = make_uint2(0, 0);
+  if (bias_pre) braw = *reinterpret_cast<const uint2*>(a.ep.bias + nst);
   // k-block of 128: load j of lane (r, q) covers k = kb*128 + 32 j + 8 q .. +8
-  for (int kb0 = wave; kb0 < nkb; kb0 += 2 * NW) {
-    uint4 av[2][4], bv[2][MT][4];
+  for (int kb0 = wave; kb0 < nkb; kb0 += U * NW) {
+    uint4 av[U][4], bv[U][MT][4];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int kb = kb0 + u * NW;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int kk = (kb << 7) + (j << 5) + (q << 3);
         const bool kin = kb < nkb && kk < a.K;
         const int ks = kin ? kk : 0;
+        // weights are streamed once per forward pass: non-temporal loads
         if (PK)
-          av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + (size_t)(kin ? kb : 0) * 2048 + j * 512), kin);
+          av[u][j] = mask_u4(load_nt16(wrow + (size_t)(kin ? kb : 0) * 2048 + j * 512), kin);
         else
-          av[u][j] = mask_u4(*reinterpret_cast<const uint4*>(wrow + ks), nvalid && kin);
+          av[u][j] = mask_u4(load_nt16(wrow + ks), nvalid && kin);
 #pragma unroll
         for (int t = 0; t < MT; ++t) {
           uint4 v = make_uint4(0, 0, 0, 0);
@@ -60,7 +72,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
       }
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -75,20 +87,28 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
   if (wave < MT) {
     f32x4 s = red[0][wave][lane];
     for (int w = 1; w < NW; ++w) s += red[w][wave][lane];
-    store_row4(a, (wave << 4) + r, n0 + (q << 2), s);
+    if (bias_pre) {
+      // the same arithmetic as store_row4 with the bias it would load
+      GemmArgs b = a;
+      b.ep.bias = nullptr;
+      s[0] += bf2f(braw.x & 0xffff); s[1] += bf2f(braw.x >> 16); s[2] += bf2f(braw.y & 0xffff); s[3] += bf2f(braw.y >> 16);
+      store_row4(b, (wave << 4) + r, nst, s);
+    } else {
+      store_row4(a, (wave << 4) + r, nst, s);
+    }
   }
 }
 
 }  // namespace
 
 hipError_t launch_skinny(const GemmArgs& a, hipStream_t s) {
-  const dim3 grid((a.N + 15) / 16), block(1024);
+  const dim3 grid((a.N + 15) / 16), block(GEMV_NW * 64);
   if (a.M <= 16) {
-    if (a.ep.w_packed) hipLaunchKernelGGL((k_gemv<1, 16, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_gemv<1, 16, false>), grid, block, 0, s, a);
+    if (a.ep.w_packed) hipLaunchKernelGGL((k_gemv<1, GEMV_NW, GEMV_U, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_gemv<1, GEMV_NW, GEMV_U, false>), grid, block, 0, s, a);
   } else {
-    if (a.ep.w_packed) hipLaunchKernelGGL((k_gemv<2, 16, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_gemv<2, 16, false>), grid, block, 0, s, a);
+    if (a.ep.w_packed) hipLaunchKernelGGL((k_gemv<2, GEMV_NW, GEMV_U, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_gemv<2, GEMV_NW, GEMV_U, false>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }
