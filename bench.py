@@ -234,18 +234,20 @@ def ablation(torch, dev, chunk, link_gbs, budget_s=2.5, max_reps=20):
     return out
 
 
-def tenants(torch, dev, n_requests, n_models, arena_gib, workers):
+def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost"):
     """Open-loop multi-tenant run: n_models registered models of the three families, an
-    arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU."""
+    arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU or
+    heaviness-aware eviction."""
     import paper_2306_03622_amd as tp
     import synth
     specs = synth.tenant_models(n_models)
     trace = synth.tenant_trace(n_requests, n_models=n_models)
     ws = 0
-    descs, kinds, host_bytes = {}, {}, {}
+    descs, kinds, host_bytes, heavy = {}, {}, {}, {}
     for cfg in (2, 3, 4):
         ws = max(ws, tp.tp_workspace_bytes(tp.ModelDesc.of(synth.config_model(cfg)), 1))
-    rt = tp.Runtime(arena_gib << 30, ws)
+    rt = tp.Runtime(arena_gib << 30, ws, plan=tp.TP_PLAN_COST if plan == "cost" else tp.TP_PLAN_GREEDY,
+                    evict_policy=tp.TP_EVICT_HEAVINESS if evict == "heaviness" else tp.TP_EVICT_LRU)
     t0 = time.perf_counter()
     ids = []
     for i, m in synth.build_models(specs, workers):
@@ -253,6 +255,7 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers):
         mid = rt.register(d, m.blob())
         ids.append(mid)
         kinds[mid] = m.arch
+        heavy[m.arch] = bool(rt.info(mid)["heavy"])
         host_bytes[mid] = m.total_bytes
         if i % 10 == 9:
             log(f"  registered {i + 1} models ({(time.perf_counter() - t0):.0f} s)")
@@ -301,9 +304,10 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers):
             "hit_rate": round(float(hit.mean()), 4), "requests": n_requests, "models": n_models,
             "arena_gib": arena_gib, "registered_host_bytes": int(sum(host_bytes.values())),
             "register_s": round(reg_s, 1), "trace_s": round(float(trace.arrival_s[-1]), 2),
-            "per_family": per, "arena": delta,
+            "per_family": per, "arena": delta, "heavy_by_family": heavy,
             "config": {"workload": f"{n_models} models (24x4096 MLP / ResNet-50 / BERT-base by index mod 3), "
-                                   f"Poisson 50 req/s, Zipf(1.1), {arena_gib} GiB arena, batch 1"}}
+                                   f"Poisson 50 req/s, Zipf(1.1), {arena_gib} GiB arena, batch 1",
+                       "eviction": evict, "chunk_plan": plan}}
 
 
 def kernel_fingerprint():
@@ -397,6 +401,8 @@ def main():
                     help="run the multi-tenant open-loop workload with this many requests instead")
     ap.add_argument("--tenant-models", type=int, default=100)
     ap.add_argument("--tenant-arena-gib", type=int, default=8)
+    ap.add_argument("--evict", choices=["lru", "heaviness"], default="lru",
+                    help="eviction policy of the multi-tenant run")
     ap.add_argument("--pmc-workload", action="store_true",
                     help="run only a fixed workload for hardware-counter passes: 20 warm forwards of the "
                          "bench model, then one 256 MiB device-to-device copy (the byte-count calibration)")
@@ -419,7 +425,8 @@ def main():
     torch.cuda.set_device(dev)
 
     if a.tenants:
-        print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16)), flush=True)
+        print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16, a.evict, a.plan)),
+              flush=True)
         return
 
     if a.ablation:

@@ -145,6 +145,19 @@ enum {
  *     ones where the link is the bottleneck. chunk_min_bytes is ignored, and so is
  *     TP_FLAG_PER_TENSOR. */
 enum { TP_PLAN_GREEDY = 0, TP_PLAN_COST = 1 };
+/* evict_policy chooses the victim when a non-resident model needs room (one victim at a
+ * time until a first-fit gap exists):
+ *   TP_EVICT_LRU: the least recently used resident model.
+ *   TP_EVICT_HEAVINESS: the paper's policy (Sec. 5.4, "Model eviction policy"): light
+ *     models first (least recently used among them), and only when no light model is
+ *     resident the least recently used heavy one. A model is heavy when swapping it slows
+ *     its inference much: at registration, when the modelled cold time of its best chunk
+ *     plan (the TP_PLAN_COST model) exceeds heavy_ratio (0: 3.0) times its modelled warm
+ *     time; tp_set_model_class overrides this. The default separates the paper's light
+ *     models, whose swapped latency is within about 1.2x of native, from its heavy one
+ *     (about 3.4x; Sec. 7, table of remoting and swapping latencies). */
+enum { TP_EVICT_LRU = 0, TP_EVICT_HEAVINESS = 1 };
+enum { TP_CLASS_AUTO = 0, TP_CLASS_LIGHT = 1, TP_CLASS_HEAVY = 2 };
 typedef struct {
   void* arena_dev;
   uint64_t arena_bytes;
@@ -162,6 +175,8 @@ typedef struct {
   int32_t plan_batch;
   float link_gbs;
   float chunk_us;
+  int32_t evict_policy;   /* TP_EVICT_* */
+  float heavy_ratio;
 } tp_config;
 
 typedef struct {
@@ -177,6 +192,9 @@ typedef struct {
   int32_t resident;
   uint64_t extent_offset;  /* arena offset of the model's extent when resident */
   uint64_t last_use_clock; /* logical clock of the last request, 0 if never used */
+  int32_t heavy;           /* 1 if the model is classed heavy (see TP_EVICT_HEAVINESS) */
+  float cold_est_us;       /* modelled cold time of its best chunk plan (plan_batch samples) */
+  float warm_est_us;       /* modelled warm time (sum of the per-layer estimates) */
 } tp_model_info_t;
 
 /* Creates a context bound to the current HIP device. The arena (Sec. 4.4: all GPU
@@ -231,6 +249,11 @@ TP_API tp_status tp_evict(struct tp_ctx* ctx, int32_t model_id);
 TP_API tp_status tp_is_resident(struct tp_ctx* ctx, int32_t model_id, int32_t* resident);
 TP_API tp_status tp_arena_stats(struct tp_ctx* ctx, tp_arena_stats_t* out);
 TP_API tp_status tp_model_info(struct tp_ctx* ctx, int32_t model_id, tp_model_info_t* out);
+
+/* Sets a model's eviction class: TP_CLASS_LIGHT, TP_CLASS_HEAVY, or TP_CLASS_AUTO (back to
+ * the registration-time estimate). Affects later evictions under TP_EVICT_HEAVINESS only.
+ * Errors: TP_E_NOENT, TP_E_INVAL (unknown class). */
+TP_API tp_status tp_set_model_class(struct tp_ctx* ctx, int32_t model_id, int32_t model_class);
 
 /* The library's pinned host image of a registered model (what a swap copies, byte for byte).
  * It equals the registered bytes except that bf16 MLP weight matrices whose width is a

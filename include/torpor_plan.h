@@ -63,6 +63,9 @@ TP_API tp_status tph_arena_unregister(struct tph_arena* a, int32_t model_id);
 TP_API tp_status tph_arena_request(struct tph_arena* a, int32_t model_id, int32_t* hit, uint64_t* offset,
                             int32_t* victims, uint32_t cap, uint32_t* n_victims);
 TP_API tp_status tph_arena_evict(struct tph_arena* a, int32_t model_id);
+/* Eviction policy (TP_EVICT_*, default LRU) and a model's class for TP_EVICT_HEAVINESS. */
+TP_API tp_status tph_arena_set_policy(struct tph_arena* a, int32_t policy);
+TP_API tp_status tph_arena_set_heavy(struct tph_arena* a, int32_t model_id, int32_t heavy);
 TP_API tp_status tph_arena_stats(struct tph_arena* a, tp_arena_stats_t* out);
 
 #ifdef __cplusplus

@@ -8,11 +8,18 @@ Test infrastructure only. Rules it follows:
   nothing is copied back (Sec. 4.3, "Model eviction").
 * Victims are chosen least-recently-used (Sec. 5.4; the paper's LRU baseline in Sec. 7.3).
 
+* Heaviness-aware variant (Sec. 5.4, "Model eviction policy"): models are heavy or light
+  by how much swapping them slows their inference; light models are evicted first, and
+  only when no light model is resident does LRU pick among the heavy ones.
+
 Readings where the paper is silent: a logical clock ticks once per request, so there are
 no ties; a model is placed in the lowest-addressed free gap that fits (first fit); while
-no gap fits, the least recently used resident model is evicted, one at a time. An
-eviction is counted as a fragmentation eviction when the total free space already
-sufficed before it. A model larger than the whole arena is refused with no state change.
+no gap fits, one victim at a time is invalidated: the least recently used resident model
+(policy "lru"), or the least recently used resident light model if there is one, else the
+least recently used heavy model (policy "heaviness"; a model's class is given, and may be
+changed between requests). An eviction is counted as a fragmentation eviction when the
+total free space already sufficed before it. A model larger than the whole arena is refused
+with no state change.
 """
 from __future__ import annotations
 
@@ -26,9 +33,12 @@ class NoSpace(Exception):
 
 
 class ArenaSim:
-    def __init__(self, capacity: int, align: int = 256):
+    def __init__(self, capacity: int, align: int = 256, policy: str = "lru"):
+        assert policy in ("lru", "heaviness")
         self.capacity = capacity
         self.align = align
+        self.policy = policy
+        self.heavy = {}         # model id -> True if heavy (heaviness policy)
         self.size = {}          # model id -> extent bytes
         self.where = {}         # resident model id -> offset
         self.last = {}          # model id -> clock of last request
@@ -36,13 +46,24 @@ class ArenaSim:
         self.hits = self.misses = self.evictions = self.frag_evictions = 0
         self.bytes_swapped = 0
 
-    def register(self, mid: int, nbytes: int) -> None:
+    def register(self, mid: int, nbytes: int, heavy: bool = False) -> None:
         self.size[mid] = round_up(nbytes, self.align)
         self.last[mid] = 0
+        self.heavy[mid] = heavy
+
+    def set_heavy(self, mid: int, heavy: bool) -> None:
+        self.heavy[mid] = heavy
 
     def unregister(self, mid: int) -> None:
         self.where.pop(mid, None)
-        del self.size[mid], self.last[mid]
+        del self.size[mid], self.last[mid], self.heavy[mid]
+
+    def victim(self) -> int:
+        candidates = list(self.where)
+        if self.policy == "heaviness":
+            light = [m for m in candidates if not self.heavy[m]]
+            candidates = light or candidates
+        return min(candidates, key=lambda m: self.last[m])
 
     def used(self) -> int:
         return sum(self.size[m] for m in self.where)
@@ -77,7 +98,7 @@ class ArenaSim:
         evicted = []
         off = self.first_fit(need)
         while off is None:
-            victim = min(self.where, key=lambda m: self.last[m])
+            victim = self.victim()
             if self.capacity - self.used() >= need:
                 self.frag_evictions += 1
             del self.where[victim]

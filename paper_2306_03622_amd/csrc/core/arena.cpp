@@ -4,10 +4,11 @@
 
 namespace tp {
 
-tp_status Arena::add_model(int32_t id, uint64_t bytes) {
+tp_status Arena::add_model(int32_t id, uint64_t bytes, bool heavy) {
   if (models_.count(id)) return TP_E_STATE;
   Rec r;
   r.bytes = (bytes + align_ - 1) / align_ * align_;
+  r.heavy = heavy;
   models_[id] = r;
   return TP_OK;
 }
@@ -34,6 +35,24 @@ bool Arena::first_fit(uint64_t need, uint64_t* off) const {
   return false;
 }
 
+int32_t Arena::victim() const {
+  // least recently used resident model; under the heaviness-aware policy only light models
+  // are candidates while any is resident (never the requester: it is not resident)
+  int32_t best = -1;
+  bool best_light = false;
+  uint64_t oldest = UINT64_MAX;
+  for (int32_t r : by_addr_) {
+    const Rec& rec = models_.at(r);
+    const bool light = policy_ == TP_EVICT_HEAVINESS && !rec.heavy;
+    if ((light && !best_light) || (light == best_light && rec.last < oldest)) {
+      best = r;
+      best_light = light;
+      oldest = rec.last;
+    }
+  }
+  return best;
+}
+
 Arena::Decision Arena::request(int32_t id) {
   Rec& me = models_.at(id);
   me.last = ++clock_;
@@ -47,13 +66,7 @@ Arena::Decision Arena::request(int32_t id) {
   ++misses_;
   uint64_t off = 0;
   while (!first_fit(me.bytes, &off)) {
-    // least recently used resident model (never the requester: it is not resident)
-    int32_t victim = -1;
-    uint64_t oldest = UINT64_MAX;
-    for (int32_t r : by_addr_) {
-      const uint64_t t = models_.at(r).last;
-      if (t < oldest) { oldest = t; victim = r; }
-    }
+    const int32_t victim = this->victim();
     if (capacity_ - used() >= me.bytes) ++frag_evictions_;
     evict(victim);
     ++evictions_;

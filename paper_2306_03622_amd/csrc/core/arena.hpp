@@ -1,7 +1,9 @@
 // The HBM weight arena's bookkeeping: one reserved device range, one contiguous extent
-// per resident model, placement in the lowest-addressed free gap that fits, and
-// least-recently-used eviction (invalidate only) until a gap fits. Host-only C++; the
-// runtime attaches device-side ordering (events) to the decisions made here.
+// per resident model, placement in the lowest-addressed free gap that fits, and eviction
+// (invalidate only) one victim at a time until a gap fits: least recently used, or, under
+// the heaviness-aware policy, the least recently used light model while one is resident and
+// only then the least recently used heavy one. Host-only C++; the runtime attaches
+// device-side ordering (events) to the decisions made here.
 #pragma once
 #include <cstdint>
 #include <unordered_map>
@@ -13,7 +15,8 @@ namespace tp {
 
 class Arena {
  public:
-  Arena(uint64_t capacity, uint64_t align) : capacity_(capacity), align_(align) {}
+  Arena(uint64_t capacity, uint64_t align, int policy = TP_EVICT_LRU)
+      : capacity_(capacity), align_(align), policy_(policy) {}
 
   struct Decision {
     bool hit = false;
@@ -21,7 +24,10 @@ class Arena {
     std::vector<int32_t> victims;   // evicted by this request, in eviction order
   };
 
-  tp_status add_model(int32_t id, uint64_t bytes);
+  tp_status add_model(int32_t id, uint64_t bytes, bool heavy = false);
+  void set_heavy(int32_t id, bool heavy) { models_.at(id).heavy = heavy; }
+  bool heavy(int32_t id) const { return models_.at(id).heavy; }
+  void set_policy(int policy) { policy_ = policy; }
   void remove_model(int32_t id);               // also drops residency
   bool known(int32_t id) const { return models_.count(id) != 0; }
   bool fits_at_all(int32_t id) const { return models_.at(id).bytes <= capacity_; }
@@ -42,11 +48,14 @@ class Arena {
   struct Rec {
     uint64_t bytes = 0, offset = 0, last = 0;
     bool resident = false;
+    bool heavy = false;
   };
   bool first_fit(uint64_t need, uint64_t* off) const;
+  int32_t victim() const;
   uint64_t used() const;
 
   uint64_t capacity_, align_;
+  int policy_;
   uint64_t clock_ = 0;
   uint64_t hits_ = 0, misses_ = 0, evictions_ = 0, frag_evictions_ = 0, swapped_ = 0;
   std::unordered_map<int32_t, Rec> models_;

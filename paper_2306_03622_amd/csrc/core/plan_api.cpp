@@ -144,6 +144,20 @@ tp_status tph_arena_evict(tph_arena* a, int32_t id) {
   return ok();
 }
 
+tp_status tph_arena_set_policy(tph_arena* a, int32_t policy) {
+  if (!a) return fail(TP_E_INVAL, "NULL arena");
+  if (policy != TP_EVICT_LRU && policy != TP_EVICT_HEAVINESS) return fail(TP_E_INVAL, "unknown eviction policy");
+  a->a.set_policy(policy);
+  return ok();
+}
+
+tp_status tph_arena_set_heavy(tph_arena* a, int32_t id, int32_t heavy) {
+  if (!a) return fail(TP_E_INVAL, "NULL arena");
+  if (!a->a.known(id)) return fail(TP_E_NOENT, "unknown model id");
+  a->a.set_heavy(id, heavy != 0);
+  return ok();
+}
+
 tp_status tph_arena_stats(tph_arena* a, tp_arena_stats_t* out) {
   if (!a || !out) return fail(TP_E_INVAL, "NULL argument");
   a->a.stats(out);

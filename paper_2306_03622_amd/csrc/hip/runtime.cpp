@@ -317,13 +317,16 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   if (cfg->plan < TP_PLAN_GREEDY || cfg->plan > TP_PLAN_COST || cfg->plan_batch < 0 || cfg->plan_batch > 65536 ||
       !(cfg->link_gbs >= 0) || cfg->link_gbs > 1e4 || !(cfg->chunk_us >= 0) || cfg->chunk_us > 1e5)
     return fail(TP_E_INVAL, "tp_create: plan, plan_batch, link_gbs or chunk_us out of range");
+  if ((cfg->evict_policy != TP_EVICT_LRU && cfg->evict_policy != TP_EVICT_HEAVINESS) || !(cfg->heavy_ratio >= 0) ||
+      cfg->heavy_ratio > 1e6)
+    return fail(TP_E_INVAL, "tp_create: evict_policy or heavy_ratio out of range");
   std::unique_ptr<tp_ctx> c(new (std::nothrow) tp_ctx);
   if (!c) return fail(TP_E_NOSPC, "out of host memory");
   c->cfg = *cfg;
   if (c->cfg.gather_wgs == 0) c->cfg.gather_wgs = 64;
   c->arena = static_cast<char*>(cfg->arena_dev);
   c->work = static_cast<char*>(cfg->work_dev);
-  c->policy.reset(new Arena(cfg->arena_bytes, 256));
+  c->policy.reset(new Arena(cfg->arena_bytes, 256, cfg->evict_policy));
   TP_HIP(hipGetDevice(&c->device));
   c->ncopy = cfg->copy_streams == 2 ? 2 : 1;
   hipError_t e = hipSuccess;
@@ -369,12 +372,21 @@ tp_status tp_register_model(tp_ctx* c, const tp_model_desc* desc, const void* ho
   tp_status s = validate_model(desc, host_bytes, &m->spec, &err);
   if (s != TP_OK) return fail(s, err);
   m->id = c->next_id;
-  if (c->cfg.plan == TP_PLAN_COST) {
+  {
+    // cost-model estimates: the plan of TP_PLAN_COST and the heaviness class
     LinkModel lm;
     if (c->cfg.link_gbs > 0) lm.link_bytes_per_us = c->cfg.link_gbs * 1e3;
     if (c->cfg.chunk_us > 0) lm.chunk_us = c->cfg.chunk_us;
-    m->chunks = plan_chunks_cost(m->spec, c->cfg.plan_batch > 0 ? c->cfg.plan_batch : 1, lm);
-  } else {
+    const int pb = c->cfg.plan_batch > 0 ? c->cfg.plan_batch : 1;
+    double cold = 0, warm = 0;
+    std::vector<Chunk> best = plan_chunks_cost(m->spec, pb, lm, &cold);
+    for (double t : layer_cost_us(m->spec, pb)) warm += t;
+    m->cold_est_us = (float)cold;
+    m->warm_est_us = (float)warm;
+    m->heavy_auto = cold > (c->cfg.heavy_ratio > 0 ? c->cfg.heavy_ratio : 3.0) * warm;
+    if (c->cfg.plan == TP_PLAN_COST) m->chunks = std::move(best);
+  }
+  if (c->cfg.plan != TP_PLAN_COST) {
     m->chunks = plan_chunks(m->spec, c->cfg.chunk_min_bytes, (c->cfg.flags & TP_FLAG_PER_TENSOR) != 0);
   }
   m->chunk_of_layer.assign(m->spec.n_layers, 0);
@@ -426,7 +438,7 @@ tp_status tp_register_model(tp_ctx* c, const tp_model_desc* desc, const void* ho
     free_model(m.get());
     return hip_fail(e, "tp_register_model: event or mapping setup");
   }
-  if (c->policy->add_model(m->id, nb) != TP_OK) {
+  if (c->policy->add_model(m->id, nb, m->heavy_auto) != TP_OK) {
     free_model(m.get());
     return fail(TP_E_STATE, "model id collision");
   }
@@ -629,6 +641,18 @@ tp_status tp_model_info(tp_ctx* c, int32_t id, tp_model_info_t* out) {
   out->resident = c->policy->resident(id) ? 1 : 0;
   out->extent_offset = c->policy->offset(id);
   out->last_use_clock = c->policy->last_use(id);
+  out->heavy = c->policy->heavy(id) ? 1 : 0;
+  out->cold_est_us = m->cold_est_us;
+  out->warm_est_us = m->warm_est_us;
+  return ok();
+}
+
+tp_status tp_set_model_class(tp_ctx* c, int32_t id, int32_t cls) {
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  Model* m = find(c, id);
+  if (!m) return fail(TP_E_NOENT, "unknown model id " + std::to_string(id));
+  if (cls < TP_CLASS_AUTO || cls > TP_CLASS_HEAVY) return fail(TP_E_INVAL, "unknown model class");
+  c->policy->set_heavy(id, cls == TP_CLASS_AUTO ? m->heavy_auto : cls == TP_CLASS_HEAVY);
   return ok();
 }
 

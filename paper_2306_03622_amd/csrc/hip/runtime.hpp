@@ -41,6 +41,8 @@ struct Model {
                                  // request must wait for the last chunk's event
   std::vector<GraphEntry> graphs;
   bool graph_failed = false;     // capture failed once: launch this model kernel by kernel
+  float cold_est_us = 0, warm_est_us = 0;   // cost-model estimates at the context's plan batch
+  bool heavy_auto = false;       // heaviness class from the estimates
 };
 
 // Drives a cold request's swap from the layer loop. Before the first kernel of a layer,

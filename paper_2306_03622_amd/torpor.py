@@ -26,6 +26,8 @@ TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
 TP_COPY_MEMCPY, TP_COPY_GATHER, TP_COPY_PAGEABLE, TP_COPY_ZERO = 0, 1, 2, 3
 TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR, TP_FLAG_TRACE = 1, 2, 4, 8, 16, 32
 TP_PLAN_GREEDY, TP_PLAN_COST = 0, 1
+TP_EVICT_LRU, TP_EVICT_HEAVINESS = 0, 1
+TP_CLASS_AUTO, TP_CLASS_LIGHT, TP_CLASS_HEAVY = 0, 1, 2
 ROLES = {
     "w": 0, "b": 1,
     "tok_emb": 10, "pos_emb": 11, "type_emb": 12, "emb_ln_g": 13, "emb_ln_b": 14,
@@ -57,7 +59,8 @@ class tp_config(C.Structure):
                 ("work_bytes", C.c_uint64), ("copy_stream", C.c_void_p), ("chunk_min_bytes", C.c_uint64),
                 ("copy_method", C.c_int32), ("gather_wgs", C.c_int32), ("flags", C.c_int32),
                 ("throttle_us", C.c_int32), ("copy_streams", C.c_int32), ("direct_max_bytes", C.c_uint64),
-                ("plan", C.c_int32), ("plan_batch", C.c_int32), ("link_gbs", C.c_float), ("chunk_us", C.c_float)]
+                ("plan", C.c_int32), ("plan_batch", C.c_int32), ("link_gbs", C.c_float), ("chunk_us", C.c_float),
+                ("evict_policy", C.c_int32), ("heavy_ratio", C.c_float)]
 
 
 class tp_arena_stats_t(C.Structure):
@@ -72,7 +75,8 @@ class tp_arena_stats_t(C.Structure):
 
 class tp_model_info_t(C.Structure):
     _fields_ = [("host_bytes", C.c_uint64), ("param_bytes", C.c_uint64), ("n_chunks", C.c_uint32),
-                ("resident", C.c_int32), ("extent_offset", C.c_uint64), ("last_use_clock", C.c_uint64)]
+                ("resident", C.c_int32), ("extent_offset", C.c_uint64), ("last_use_clock", C.c_uint64),
+                ("heavy", C.c_int32), ("cold_est_us", C.c_float), ("warm_est_us", C.c_float)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -105,6 +109,7 @@ _SIGS = {
     "tp_is_resident": [_P, C.c_int32, C.POINTER(C.c_int32)],
     "tp_arena_stats": [_P, C.POINTER(tp_arena_stats_t)],
     "tp_model_info": [_P, C.c_int32, C.POINTER(tp_model_info_t)],
+    "tp_set_model_class": [_P, C.c_int32, C.c_int32],
     "tp_model_chunks": [_P, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
                         C.c_uint32, C.POINTER(C.c_uint32)],
     "tp_workspace_bytes": [C.POINTER(tp_model_desc), C.c_int32, C.POINTER(C.c_uint64)],
@@ -129,6 +134,8 @@ _SIGS = {
     "tph_arena_request": [_P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_uint64), C.POINTER(C.c_int32),
                           C.c_uint32, C.POINTER(C.c_uint32)],
     "tph_arena_evict": [_P, C.c_int32],
+    "tph_arena_set_policy": [_P, C.c_int32],
+    "tph_arena_set_heavy": [_P, C.c_int32, C.c_int32],
     "tph_arena_stats": [_P, C.POINTER(tp_arena_stats_t)],
 }
 HOST_ONLY = [n for n in _SIGS if n.startswith("tph_")]
@@ -228,11 +235,12 @@ class ModelDesc:
 
 def tp_create(arena_dev, arena_bytes, work_dev, work_bytes, copy_stream=None, chunk_min_bytes=DEFAULT_CHUNK,
               copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0, copy_streams=0, direct_max_bytes=0,
-              plan=TP_PLAN_GREEDY, plan_batch=0, link_gbs=0.0, chunk_us=0.0):
+              plan=TP_PLAN_GREEDY, plan_batch=0, link_gbs=0.0, chunk_us=0.0, evict_policy=TP_EVICT_LRU,
+              heavy_ratio=0.0):
     L = lib()
     cfg = tp_config(_ptr(arena_dev), arena_bytes, _ptr(work_dev), work_bytes, _ptr(copy_stream), chunk_min_bytes,
                     copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes, plan, plan_batch,
-                    link_gbs, chunk_us)
+                    link_gbs, chunk_us, evict_policy, heavy_ratio)
     ctx = _P()
     _check(L, L.tp_create(C.byref(cfg), C.byref(ctx)))
     return ctx
@@ -281,6 +289,10 @@ def tp_model_info(ctx, model_id) -> dict:
     s = tp_model_info_t()
     _check(lib(), lib().tp_model_info(ctx, model_id, C.byref(s)))
     return s.as_dict()
+
+
+def tp_set_model_class(ctx, model_id, model_class):
+    _check(lib(), lib().tp_set_model_class(ctx, model_id, model_class))
 
 
 def tp_model_chunks(ctx, model_id):
@@ -388,18 +400,25 @@ def tph_layer_costs(desc: ModelDesc, host_bytes: int, batch: int, L=None):
 class HostArena:
     """tph_arena_*: the arena bookkeeping without a device."""
 
-    def __init__(self, capacity: int, align: int = 256, L=None):
+    def __init__(self, capacity: int, align: int = 256, L=None, policy: int = TP_EVICT_LRU):
         self.L = L or lib()
         self.h = _P()
         _check(self.L, self.L.tph_arena_create(capacity, align, C.byref(self.h)))
+        if policy != TP_EVICT_LRU:
+            _check(self.L, self.L.tph_arena_set_policy(self.h, policy))
 
     def __del__(self):
         if getattr(self, "h", None):
             self.L.tph_arena_destroy(self.h)
             self.h = None
 
-    def register(self, mid, nbytes):
+    def register(self, mid, nbytes, heavy: bool = False):
         _check(self.L, self.L.tph_arena_register(self.h, mid, nbytes))
+        if heavy:
+            _check(self.L, self.L.tph_arena_set_heavy(self.h, mid, 1))
+
+    def set_heavy(self, mid, heavy: bool):
+        _check(self.L, self.L.tph_arena_set_heavy(self.h, mid, int(heavy)))
 
     def unregister(self, mid):
         _check(self.L, self.L.tph_arena_unregister(self.h, mid))
@@ -427,7 +446,8 @@ class Runtime:
     def __init__(self, arena_bytes: int, work_bytes: int, device: int = 0, chunk_min_bytes: int = DEFAULT_CHUNK,
                  copy_method: int = TP_COPY_MEMCPY, gather_wgs: int = 0, flags: int = 0, throttle_us: int = 0,
                  copy_stream=None, copy_streams: int = 0, direct_max_bytes: int = DEFAULT_DIRECT,
-                 plan: int = TP_PLAN_GREEDY, plan_batch: int = 0, link_gbs: float = 0.0, chunk_us: float = 0.0):
+                 plan: int = TP_PLAN_GREEDY, plan_batch: int = 0, link_gbs: float = 0.0, chunk_us: float = 0.0,
+                 evict_policy: int = TP_EVICT_LRU, heavy_ratio: float = 0.0):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("libtorpor needs a HIP device")
@@ -439,7 +459,7 @@ class Runtime:
         self.copy_stream = copy_stream
         self.ctx = tp_create(self.arena, arena_bytes, self.work, self.work.numel(), copy_stream, chunk_min_bytes,
                              copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes, plan,
-                             plan_batch, link_gbs, chunk_us)
+                             plan_batch, link_gbs, chunk_us, evict_policy, heavy_ratio)
         self.descs = {}
 
     def close(self):
@@ -482,6 +502,9 @@ class Runtime:
 
     def info(self, mid) -> dict:
         return tp_model_info(self.ctx, mid)
+
+    def set_class(self, mid, model_class: int):
+        tp_set_model_class(self.ctx, mid, model_class)
 
     def timeline(self):
         return tp_last_timeline(self.ctx)

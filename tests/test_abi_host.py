@@ -26,7 +26,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 28, sorted(names)
+    assert len(names) == 31, sorted(names)
     L = tp.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -107,16 +107,21 @@ def test_workspace_grows_with_batch():
         assert 0 < w[0] <= w[1] <= w[2]
 
 
-def _replay(trace, sizes, cap, L):
-    sim = ArenaSim(cap, align=256)
-    ha = tp.HostArena(cap, 256, L=L)
+def _replay(trace, sizes, cap, L, policy="lru", heavy=None):
+    sim = ArenaSim(cap, align=256, policy=policy)
+    ha = tp.HostArena(cap, 256, L=L, policy=tp.TP_EVICT_HEAVINESS if policy == "heaviness" else tp.TP_EVICT_LRU)
+    heavy = heavy or [False] * len(sizes)
     for i, nb in enumerate(sizes):
-        sim.register(i, nb)
-        ha.register(i, nb)
+        sim.register(i, nb, heavy=heavy[i])
+        ha.register(i, nb, heavy=heavy[i])
     for op, k in trace:
         if op == "evict":
             sim.evict(k)
             ha.evict(k)
+            continue
+        if op == "flip":
+            sim.set_heavy(k, not sim.heavy[k])
+            ha.set_heavy(k, sim.heavy[k])
             continue
         try:
             want = sim.request(k)
@@ -138,6 +143,29 @@ def test_arena_matches_simulator_random_traces(sizes, ops, frac):
     trace = [(op, k % len(sizes)) for op, k in ops]
     _replay(trace, sizes, cap, tp.lib())
     _replay(trace, sizes, cap, tp.host_lib())
+
+
+@settings(max_examples=60, deadline=None)
+@given(sizes=st.lists(st.integers(1, 40).map(lambda x: x * 1000), min_size=2, max_size=10),
+       ops=st.lists(st.tuples(st.sampled_from(["req", "req", "req", "req", "evict", "flip"]), st.integers(0, 9)),
+                    max_size=80),
+       frac=st.floats(0.2, 1.2), heavy_bits=st.integers(0, 1023))
+def test_arena_heaviness_policy_matches_simulator(sizes, ops, frac, heavy_bits):
+    cap = max(int(sum(sizes) * frac), 256) // 256 * 256
+    heavy = [bool((heavy_bits >> i) & 1) for i in range(len(sizes))]
+    trace = [(op, k % len(sizes)) for op, k in ops]
+    _replay(trace, sizes, cap, tp.lib(), "heaviness", heavy)
+    _replay(trace, sizes, cap, tp.host_lib(), "heaviness", heavy)
+
+
+def test_arena_policy_errors():
+    ha = tp.HostArena(10_000, 256)
+    with pytest.raises(tp.TorporError) as e:
+        tp.torpor._check(ha.L, ha.L.tph_arena_set_policy(ha.h, 7))
+    assert e.value.status == tp.TP_E_INVAL
+    with pytest.raises(tp.TorporError) as e:
+        ha.set_heavy(3, True)
+    assert e.value.status == tp.TP_E_NOENT
 
 
 def test_arena_unregister_and_errors():

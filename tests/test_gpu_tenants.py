@@ -1,5 +1,6 @@
 """Multi-tenant open-loop replay (tp_run_trace) on the GPU, scaled down: 9 models of the
-three families, an arena that holds about a third of them, Poisson/Zipf arrivals.
+three families, an arena that holds about a third of them, Poisson/Zipf arrivals, under
+LRU and under heaviness-aware eviction.
 
 Checks: every request's hit flag and the arena's counters equal the reference simulator
 replayed on the same request sequence; every model's first output matches the oracle."""
@@ -15,15 +16,20 @@ from tests.common import log, out_shape, to_device, torch_dev
 pytestmark = pytest.mark.gpu
 
 
-def test_tenant_trace_lru_and_first_outputs():
+@pytest.mark.parametrize("policy", ["lru", "heaviness"])
+def test_tenant_trace_lru_and_first_outputs(policy):
     torch, dev = torch_dev()
     specs = synth.tenant_models(9)
     models = [m for _, m in synth.build_models(specs, workers=9)]
     trace = synth.tenant_trace(120, n_models=9)
     cap = (models[0].total_bytes + models[1].total_bytes + models[2].total_bytes) // 256 * 256 + (64 << 20)
     ws = max(tp.tp_workspace_bytes(tp.ModelDesc.of(m), 1) for m in models)
-    rt = tp.Runtime(cap, ws)
+    rt = tp.Runtime(cap, ws, evict_policy=tp.TP_EVICT_HEAVINESS if policy == "heaviness" else tp.TP_EVICT_LRU)
     ids = [rt.register(tp.ModelDesc.of(m), m.blob()) for m in models]
+    heavy = [bool(rt.info(i)["heavy"]) for i in ids]
+    # the cost model classes the transfer-bound families heavy and ResNet-50 (whose compute
+    # hides most of its transfer) light
+    assert heavy == [m.arch != "resnet50" for m in models], heavy
     xs_np, reqs, outs = [], [], []
     for r in range(len(trace.model)):
         m = models[int(trace.model[r])]
@@ -39,9 +45,9 @@ def test_tenant_trace_lru_and_first_outputs():
     assert all(r["status"] == 0 for r in res)
     assert all(r["done_ns"] >= r["issue_ns"] for r in res)
 
-    sim = ArenaSim(cap, align=256)
-    for i, m in zip(ids, models):
-        sim.register(i, m.total_bytes)
+    sim = ArenaSim(cap, align=256, policy=policy)
+    for i, m, h in zip(ids, models, heavy):
+        sim.register(i, m.total_bytes, heavy=h)
     want_hits = [sim.request(q[0])["hit"] for q in reqs]
     assert [r["hit"] for r in res] == want_hits
     got = rt.stats()

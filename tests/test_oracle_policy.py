@@ -145,3 +145,46 @@ def test_best_grouping_hand_worked():
     # with a huge fixed cost per copy a single group wins
     first, _ = pipeline.best_grouping(begin, total, us, 10.0, 1e6, 0.0)
     assert first == [0]
+
+
+# ------------------------------------------------------------------ heaviness-aware eviction
+
+def test_heaviness_policy_evicts_light_first_then_lru_among_heavy():
+    a = ArenaSim(1000, align=100, policy="heaviness")
+    a.register(0, 300, heavy=True)
+    a.register(1, 300, heavy=False)
+    a.register(2, 300, heavy=True)
+    a.register(3, 300, heavy=True)
+    for m in (0, 1, 2):
+        a.request(m)                                  # [0:300) [300:600) [600:900)
+    a.request(0)                                      # LRU order: 1 < 2 < 0
+    # LRU would evict 1 too (it is also the least recent): make the light model the most recent
+    a.request(1)                                      # LRU order: 2 < 0 < 1
+    r = a.request(3)                                  # needs 300 B, 100 free
+    assert r["evicted"] == [1] and r["offset"] == 300  # the light model goes although most recent
+    a.register(4, 400, heavy=True)
+    r = a.request(4)                                  # only heavy models left: LRU among them
+    # order: 2 (clock 3) < 0 (4) < 3 (6); evicting 2 leaves the 400 B gap 600..1000
+    assert r["evicted"] == [2] and r["offset"] == 600
+    a.register(5, 700, heavy=True)
+    r = a.request(5)                                  # 0 (clock 4), then 3 (6): gaps 0..300, then 0..600
+    assert r["evicted"] == [0, 3, 4] and r["offset"] == 0
+
+
+def test_heaviness_policy_with_all_models_of_one_class_is_lru():
+    for heavy in (False, True):
+        lru, hv = ArenaSim(900, align=1), ArenaSim(900, align=1, policy="heaviness")
+        for m in range(5):
+            lru.register(m, 300)
+            hv.register(m, 300, heavy=heavy)
+        for m in (0, 1, 2, 0, 3, 4, 1, 2, 0, 4, 3):
+            assert lru.request(m) == hv.request(m)
+
+
+def test_heaviness_class_change_applies_to_later_evictions():
+    a = ArenaSim(600, align=1, policy="heaviness")
+    for m in range(3):
+        a.register(m, 300, heavy=True)
+    a.request(0); a.request(1)
+    a.set_heavy(1, False)
+    assert a.request(2)["evicted"] == [1]             # LRU would have taken model 0
