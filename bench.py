@@ -27,6 +27,14 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+# Overlapping the swap with the forward pass needs the copy stream and the request's stream
+# on different hardware queues. HIP spreads a process's streams over GPU_MAX_HW_QUEUES
+# queues (4 by default), and with torch's streams in the same process some contexts then
+# land in an arrangement where chunk copies and layer kernels execute in lockstep (measured:
+# BERT-base cold 4.8-5.0 ms instead of 4.0 ms in about one context in ten); with 8 queues
+# none did. It must be set before the HIP runtime starts, so before torch is imported.
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "8")
+
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 PCIE5_X16_GBS = 63.0
@@ -310,6 +318,41 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                        "eviction": evict, "chunk_plan": plan}}
 
 
+def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, link, steps, warmup, trace):
+    """Cold, warm and swap-only latencies of workload `cfg` at batches `bts` (one context)."""
+    import paper_2306_03622_amd as tp
+    import synth
+    m = synth.config_model(cfg)
+    out = {}
+    bb = Bench(torch, dev, m, bts, method, chunk, copy_streams, plan=plan, link_gbs=link,
+               flags=tp.TP_FLAG_TRACE if trace else 0)
+    for bt in bts:
+        rr = measure(bb, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt), steps, warmup, max(4 * steps, 100))
+        if trace and m.total_bytes > tp.DEFAULT_DIRECT:     # direct-access requests are not traced
+            x, y = bb.io(bt, 1)
+            bb.request(x, y, cold=True)
+            tl = bb.rt.timeline()
+            out[f"cfg{cfg}_b{bt}_timeline"] = {k: ([round(v, 4) for v in tl[k]] if isinstance(tl[k], list)
+                                                   else round(tl[k], 4)) for k in tl}
+        wp = p50(rr["warm"])
+        bnd = max(m.total_bytes / (link * 1e9) * 1e3, wp)
+        fl = forward_flops(m, bt)
+        fwd = bb.event_time_ms(rr["x"], rr["out"], 20)
+        out[f"cfg{cfg}_b{bt}"] = {
+            "weight_bytes": m.total_bytes, "chunks": len(bb.rt.chunks(bb.mid)),
+            "cold_p50_ms": round(p50(rr["cold"]), 4), "cold_p10_ms": round(pct(rr["cold"], 10), 4),
+            "cold_p90_ms": round(pct(rr["cold"], 90), 4),
+            "warm_p50_ms": round(wp, 4), "bound_ms": round(bnd, 4),
+            "cold_over_bound": round(p50(rr["cold"]) / bnd, 4),
+            "swap_only_gbs": round(m.total_bytes / (p50(rr["swap"]) / 1e3) / 1e9, 2),
+            "forward_gflop": round(fl / 1e9, 3), "warm_forward_event_ms": round(fwd, 4),
+            "warm_tflops": round(fl / (fwd * 1e-3) / 1e12, 2),
+            "mfma_util": round(fl / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5)}
+    bb.close()
+    m.drop_blob()
+    return out
+
+
 def kernel_fingerprint():
     """First 16 hex digits of sha256 over the skinny-GEMM kernel sources."""
     import hashlib
@@ -410,11 +453,33 @@ def main():
     ap.add_argument("--ablation", action="store_true",
                     help="time the cold request under every swap design instead (breakdown table)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--workload", type=int, default=0, help=argparse.SUPPRESS)   # child process of --full
+    ap.add_argument("--batches", default="1", help=argparse.SUPPRESS)
+    ap.add_argument("--trace", action="store_true",
+                    help="with --full: record the per-chunk timeline of one more cold request per workload")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: swap-in and execution of a model is a per-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+
+    children = {}
+    if a.full and not a.workload:
+        # Each extra workload runs in a process of its own, started before this process touches
+        # the GPU: a serving process holds one context, and after many contexts and streams in
+        # one process HIP's stream-to-hardware-queue arrangement can serialise a swap behind
+        # the kernels (seen as BERT-base cold 4.5-4.8 ms instead of 4.0 ms).
+        import subprocess
+        for cfg, bts in ((1, [1]), (3, [1, 8]), (4, [1, 8])):
+            log(f"workload {cfg} (child process)")
+            cmd = [sys.executable, os.path.abspath(__file__), "--workload", str(cfg), "--batches",
+                   ",".join(map(str, bts)), "--steps", str(a.steps), "--warmup", str(a.warmup), "--method",
+                   "memcpy" if a.method == "auto" else a.method, "--chunk", str(a.chunk), "--copy-streams",
+                   str(a.copy_streams), "--plan", a.plan] + (["--trace"] if a.trace else [])
+            out = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)     # its log goes to our stderr
+            if out.returncode != 0:
+                raise SystemExit(f"workload {cfg} failed with status {out.returncode}")
+            children.update(json.loads(out.stdout.strip().splitlines()[-1]))
 
     import torch
     import synth
@@ -451,16 +516,28 @@ def main():
                           f"{a.batch}, then one 268435456-byte device copy"}), flush=True)
         return
 
+    import paper_2306_03622_amd as tp
     log("measuring host-link peak (1 GiB pinned H2D, best of 10)")
     link = link_peak(torch, dev)
     log(f"  link peak {link:.1f} GB/s")
+    if a.workload:
+        bts = [int(v) for v in a.batches.split(",")]
+        chunk = tp.DEFAULT_CHUNK if a.chunk in ("default", "elbow") else int(a.chunk)
+        res = measure_workload(torch, dev, a.workload, bts, a.method, chunk, a.copy_streams, a.plan, link, a.steps,
+                               a.warmup, a.trace)
+        for v in res.values():
+            if "cold_p50_ms" in v:
+                v["link_peak_gbs"] = round(link, 2)
+        print(json.dumps(res), flush=True)
+        return
 
-    import paper_2306_03622_amd as tp
+    # the group-size sweep creates many contexts; it runs after the measurements unless its
+    # elbow is asked for as the group size
     sweep = None
-    if not a.no_sweep:
+    sweep_method = "gather" if a.method == "gather" else "memcpy"
+    if a.chunk == "elbow" and not a.no_sweep:
         log("group-size sweep")
-        sweep = elbow_sweep(torch, dev, "gather" if a.method == "gather" else "memcpy", a.copy_streams)
-    if a.chunk == "elbow" and sweep:
+        sweep = elbow_sweep(torch, dev, sweep_method, a.copy_streams)
         a.chunk = sweep["elbow_bytes"]
     elif a.chunk in ("default", "elbow"):
         a.chunk = tp.DEFAULT_CHUNK
@@ -524,29 +601,11 @@ def main():
             "swap_only_p50_ms": round(p50(rr["swap"]), 3)}
     b.close()
 
-    if a.full:
-        for cfg, bts in ((1, [1]), (3, [1, 8]), (4, [1, 8])):
-            m = synth.config_model(cfg)
-            log(f"workload {cfg}")
-            bb = Bench(torch, dev, m, bts, method, a.chunk, a.copy_streams, plan=a.plan, link_gbs=link)
-            for bt in bts:
-                rr = measure(bb, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt), a.steps, a.warmup,
-                             max(4 * a.steps, 100))
-                wp = p50(rr["warm"])
-                bnd = max(m.total_bytes / (link * 1e9) * 1e3, wp)
-                fl = forward_flops(m, bt)
-                fwd = bb.event_time_ms(rr["x"], rr["out"], 20)
-                extra[f"cfg{cfg}_b{bt}"] = {
-                    "weight_bytes": m.total_bytes, "chunks": len(bb.rt.chunks(bb.mid)),
-                    "cold_p50_ms": round(p50(rr["cold"]), 4),
-                    "warm_p50_ms": round(wp, 4), "bound_ms": round(bnd, 4),
-                    "cold_over_bound": round(p50(rr["cold"]) / bnd, 4),
-                    "swap_only_gbs": round(m.total_bytes / (p50(rr["swap"]) / 1e3) / 1e9, 2),
-                    "forward_gflop": round(fl / 1e9, 3), "warm_forward_event_ms": round(fwd, 4),
-                    "warm_tflops": round(fl / (fwd * 1e-3) / 1e12, 2),
-                    "mfma_util": round(fl / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5)}
-            bb.close()
-            m.drop_blob()
+    extra.update(children)
+
+    if sweep is None and not a.no_sweep:
+        log("group-size sweep")
+        sweep = elbow_sweep(torch, dev, sweep_method, a.copy_streams)
 
     cpu = None
     if not a.no_cpu:
