@@ -242,14 +242,15 @@ def ablation(torch, dev, chunk, link_gbs, budget_s=2.5, max_reps=20):
     return out
 
 
-def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost"):
+def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost", queue=None, rate=50.0,
+            deadline_ms=None, slo_pct=0.98):
     """Open-loop multi-tenant run: n_models registered models of the three families, an
     arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU or
     heaviness-aware eviction."""
     import paper_2306_03622_amd as tp
     import synth
     specs = synth.tenant_models(n_models)
-    trace = synth.tenant_trace(n_requests, n_models=n_models)
+    trace = synth.tenant_trace(n_requests, rate_per_s=rate, n_models=n_models)
     ws = 0
     descs, kinds, host_bytes, heavy = {}, {}, {}, {}
     for cfg in (2, 3, 4):
@@ -293,7 +294,13 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
     st0 = rt.stats()
     torch.cuda.synchronize()
     log(f"running {n_requests} requests over {trace.arrival_s[-1]:.1f} s")
-    res = rt.run_trace(reqs, stream=stream)
+    sched = None
+    if queue is None:
+        res = rt.run_trace(reqs, stream=stream)
+    else:
+        dls = [int(deadline_ms[kinds[q[0]]] * 1e6) for q in reqs]
+        res, sched = rt.run_trace_sched(reqs, dls, stream=stream, slo_pct=slo_pct,
+                                        policy=tp.TP_QUEUE_SLO if queue == "slo" else tp.TP_QUEUE_FIFO)
     st1 = rt.stats()
     rt.close()
     lat = np.array([(r["done_ns"] - q[4]) / 1e6 for r, q in zip(res, reqs)])
@@ -307,14 +314,28 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                       "p99_ms": round(float(np.percentile(lat[sel], 99)), 3),
                       "hit_rate": round(float(hit[sel].mean()), 4)}
     delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped")}
+    slo = None
+    if queue is not None:
+        # a function (model) complies when at least slo_pct of its requests met their deadline
+        by_model = {}
+        for r, q in zip(res, reqs):
+            ok = (r["done_ns"] - q[4]) <= deadline_ms[kinds[q[0]]] * 1e6
+            by_model.setdefault(q[0], []).append(ok)
+        comp = {mid: np.mean(v) >= slo_pct for mid, v in by_model.items()}
+        slo = {"queue": queue, "deadline_ms": deadline_ms, "pct": slo_pct, "functions": len(comp),
+               "compliant_functions": int(sum(comp.values())),
+               "compliant_ratio": round(float(np.mean(list(comp.values()))), 4),
+               "requests_within_deadline": round(float(np.mean([(r["done_ns"] - q[4]) <= deadline_ms[kinds[q[0]]] * 1e6
+                                                                 for r, q in zip(res, reqs)])), 4),
+               "scheduler": sched}
     return {"metric": "multi-tenant request latency (open loop, LRU)", "unit": "ms",
             "p50_ms": round(float(np.percentile(lat, 50)), 3), "p99_ms": round(float(np.percentile(lat, 99)), 3),
             "hit_rate": round(float(hit.mean()), 4), "requests": n_requests, "models": n_models,
             "arena_gib": arena_gib, "registered_host_bytes": int(sum(host_bytes.values())),
             "register_s": round(reg_s, 1), "trace_s": round(float(trace.arrival_s[-1]), 2),
-            "per_family": per, "arena": delta, "heavy_by_family": heavy,
+            "per_family": per, "arena": delta, "heavy_by_family": heavy, "slo": slo,
             "config": {"workload": f"{n_models} models (24x4096 MLP / ResNet-50 / BERT-base by index mod 3), "
-                                   f"Poisson 50 req/s, Zipf(1.1), {arena_gib} GiB arena, batch 1",
+                                   f"Poisson {rate:g} req/s, Zipf(1.1), {arena_gib} GiB arena, batch 1",
                        "eviction": evict, "chunk_plan": plan}}
 
 
@@ -446,6 +467,11 @@ def main():
     ap.add_argument("--tenant-arena-gib", type=int, default=8)
     ap.add_argument("--evict", choices=["lru", "heaviness"], default="lru",
                     help="eviction policy of the multi-tenant run")
+    ap.add_argument("--queue", choices=["none", "fifo", "slo"], default="none",
+                    help="multi-tenant run: host-side request queue (FIFO or SLO-aware) instead of issuing at arrival")
+    ap.add_argument("--rate", type=float, default=50.0, help="multi-tenant arrival rate (requests/s)")
+    ap.add_argument("--deadlines", default="40,3,12",
+                    help="multi-tenant SLO deadlines in ms for the MLP, ResNet-50 and BERT-base families")
     ap.add_argument("--pmc-workload", action="store_true",
                     help="run only a fixed workload for hardware-counter passes: 20 warm forwards of the "
                          "bench model, then one 256 MiB device-to-device copy (the byte-count calibration)")
@@ -490,8 +516,9 @@ def main():
     torch.cuda.set_device(dev)
 
     if a.tenants:
-        print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16, a.evict, a.plan)),
-              flush=True)
+        dl = dict(zip(("mlp", "resnet50", "bert"), (float(v) for v in a.deadlines.split(","))))
+        print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16, a.evict, a.plan,
+                                 None if a.queue == "none" else a.queue, a.rate, dl)), flush=True)
         return
 
     if a.ablation:

@@ -306,6 +306,42 @@ typedef struct {
 TP_API tp_status tp_run_trace(struct tp_ctx* ctx, const tp_request* requests, uint32_t n, void* stream,
                               tp_request_result* results);
 
+/* Request queueing of tp_run_trace_sched. */
+enum { TP_QUEUE_FIFO = 0, TP_QUEUE_SLO = 1 };
+typedef struct {
+  int32_t policy;         /* TP_QUEUE_FIFO or TP_QUEUE_SLO */
+  int32_t max_inflight;   /* requests enqueued on the GPU at once (1..256) */
+  double slo_pct;         /* tail percentile p of every function's SLO, in (0, 1) (e.g. 0.98) */
+  double alpha;           /* initial high-priority threshold, in (0, 1] */
+  double scalar;          /* alpha update factor, > 1 (the paper's default 2) */
+  double threshold;       /* alpha update trigger (the paper's default 0.04) */
+  uint64_t period_ns;     /* alpha update period, > 0 */
+} tp_sched_config;
+
+typedef struct {
+  double alpha;           /* alpha at the end */
+  uint32_t periods;       /* periods closed */
+  uint32_t alpha_changes; /* periods that changed alpha */
+  uint32_t compliant;     /* functions whose served requests met the SLO over the whole trace */
+  uint32_t functions;     /* functions with at least one served request */
+} tp_sched_stats;
+
+/* Open-loop replay with a request queue on the host (Sec. 5.3 "Request queueing"): requests
+ * are queued at their arrival times, and whenever fewer than max_inflight are enqueued on the
+ * GPU the next one is chosen: TP_QUEUE_FIFO, the earliest arrival; TP_QUEUE_SLO, the paper's
+ * SLO-aware policy over the functions (model ids) of the trace: each function's required
+ * request count RRC = (p n - m) / (1 - p) from its n served requests, m of them within their
+ * deadline (deadline_ns[i], relative to request i's arrival); functions sorted by RRC
+ * ascending, the first k in the high-priority group with k the largest such that their positive
+ * RRCs sum to at most alpha times all of them; the high group first, largest RRC first, then
+ * the low group, smallest RRC first; a function's own requests in arrival order. alpha is
+ * updated every period_ns from the ratio of functions whose requests served in that period met
+ * the SLO (served within deadline / served >= p), as in the appendix's auto-configuration.
+ * Results and errors as tp_run_trace; *stats (may be NULL) summarises the run. */
+TP_API tp_status tp_run_trace_sched(struct tp_ctx* ctx, const tp_request* requests, uint32_t n, void* stream,
+                                    const tp_sched_config* cfg, const uint64_t* deadline_ns,
+                                    tp_request_result* results, tp_sched_stats* stats);
+
 /* Thread-local message describing the last non-OK status ("" if none). */
 TP_API const char* tp_last_error(void);
 

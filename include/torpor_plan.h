@@ -51,6 +51,27 @@ TP_API tp_status tph_plan_cost(const uint64_t* unit_begin, const double* unit_us
 TP_API tp_status tph_layer_costs(const tp_model_desc* desc, uint64_t host_bytes, int32_t batch, double* us, uint32_t cap,
                           uint32_t* n);
 
+/* SLO-aware queueing (Sec. 5.3 "Request queueing"; appendix "Function request
+ * prioritization"), as used by tp_run_trace_sched. tph_rrc: *out = (p n - m) / (1 - p), the
+ * required request count of a function with n requests served, m of them within the deadline,
+ * tail percentile p in (0, 1). */
+TP_API tp_status tph_rrc(uint64_t n, uint64_t m, double p, double* out);
+
+/* The request to run next among n_pending queued requests (pending_func: the function of
+ * each, in arrival order) of n_funcs functions with counters n[], m[]: functions sorted by
+ * RRC ascending (ties: lower index), the first k forming the high-priority group with k the
+ * largest such that the positive RRCs of the first k sum to at most alpha times those of all;
+ * a high-priority function with the largest RRC first, else the low-priority one with the
+ * smallest RRC (ties: lower index), its earliest queued request. *pick receives the index in
+ * pending_func (-1 if none is queued); high_out (n_funcs entries, may be NULL) the group. */
+TP_API tp_status tph_sched_pick(uint32_t n_funcs, const uint64_t* n, const uint64_t* m, double p, double alpha,
+                         uint32_t n_pending, const int32_t* pending_func, int32_t* pick, uint8_t* high_out);
+
+/* One step of the alpha auto-configuration: alpha * scalar (at most 1) if new_ratio - last_ratio
+ * > |threshold|, alpha / scalar if it is < -|threshold|, else alpha. scalar > 1. */
+TP_API tp_status tph_alpha_update(double alpha, double last_ratio, double new_ratio, double scalar, double threshold,
+                           double* out);
+
 struct tph_arena;
 /* An arena of `capacity` bytes whose extents are rounded up to `align` (power of two). */
 TP_API tp_status tph_arena_create(uint64_t capacity, uint64_t align, struct tph_arena** out);

@@ -12,9 +12,9 @@ relocates memory blocks whose internal offsets are unchanged (Sec. 4.4, "Memory 
 management"). So the oracle is the plain forward pass of each model from the same weight
 bytes (``forward``), plus the byte-level placement and eviction rules (``arena_sim``) and
 the transfer grouping rule (``chunks``) and the modelled time of a pipelined request
-under a grouping (``pipeline``).
+under a grouping (``pipeline``), and the SLO-aware queueing rules (``slo_queue``).
 
 Precision: float64 by default (the paper fixes none); ``dt=np.float32`` gives the fp32
 variant. bf16 weights and inputs are widened exactly.
 """
-from . import ops, forward, arena_sim, chunks, pipeline  # noqa: F401
+from . import ops, forward, arena_sim, chunks, pipeline, slo_queue  # noqa: F401

@@ -4,6 +4,7 @@
 #include "arena.hpp"
 #include "errors.hpp"
 #include "model.hpp"
+#include "sched.hpp"
 #include "torpor_plan.h"
 
 using namespace tp;
@@ -97,6 +98,38 @@ tp_status tph_layer_costs(const tp_model_desc* desc, uint64_t host_bytes, int32_
   const auto t = layer_cost_us(m, batch);
   *n = (uint32_t)t.size();
   for (uint32_t i = 0; us && i < t.size() && i < cap; ++i) us[i] = t[i];
+  return ok();
+}
+
+tp_status tph_rrc(uint64_t n, uint64_t m, double p, double* out) {
+  if (!out || !(p > 0 && p < 1) || m > n) return fail(TP_E_INVAL, "tph_rrc: need 0 < p < 1 and m <= n");
+  *out = rrc(n, m, p);
+  return ok();
+}
+
+tp_status tph_sched_pick(uint32_t n_funcs, const uint64_t* n, const uint64_t* m, double p, double alpha,
+                         uint32_t n_pending, const int32_t* pending_func, int32_t* pick, uint8_t* high_out) {
+  if (!pick || (n_funcs && (!n || !m)) || (n_pending && !pending_func) || !(p > 0 && p < 1) ||
+      !(alpha >= 0 && alpha <= 1))
+    return fail(TP_E_INVAL, "tph_sched_pick: bad argument");
+  std::vector<double> r(n_funcs);
+  for (uint32_t f = 0; f < n_funcs; ++f) {
+    if (m[f] > n[f]) return fail(TP_E_INVAL, "tph_sched_pick: m > n");
+    r[f] = rrc(n[f], m[f], p);
+  }
+  std::vector<int32_t> pend(pending_func, pending_func + n_pending);
+  for (int32_t f : pend)
+    if (f < 0 || (uint32_t)f >= n_funcs) return fail(TP_E_INVAL, "tph_sched_pick: function index out of range");
+  const std::vector<uint8_t> high = high_group(r, alpha);
+  if (high_out) std::copy(high.begin(), high.end(), high_out);
+  *pick = sched_pick(r, high, pend);
+  return ok();
+}
+
+tp_status tph_alpha_update(double alpha, double last_ratio, double new_ratio, double scalar, double threshold,
+                           double* out) {
+  if (!out || !(scalar > 1) || !(alpha > 0 && alpha <= 1)) return fail(TP_E_INVAL, "tph_alpha_update: bad argument");
+  *out = alpha_update(alpha, last_ratio, new_ratio, scalar, threshold);
   return ok();
 }
 

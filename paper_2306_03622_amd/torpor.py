@@ -28,6 +28,7 @@ TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_
 TP_PLAN_GREEDY, TP_PLAN_COST = 0, 1
 TP_EVICT_LRU, TP_EVICT_HEAVINESS = 0, 1
 TP_CLASS_AUTO, TP_CLASS_LIGHT, TP_CLASS_HEAVY = 0, 1, 2
+TP_QUEUE_FIFO, TP_QUEUE_SLO = 0, 1
 ROLES = {
     "w": 0, "b": 1,
     "tok_emb": 10, "pos_emb": 11, "type_emb": 12, "emb_ln_g": 13, "emb_ln_b": 14,
@@ -91,6 +92,19 @@ class tp_request_result(C.Structure):
     _fields_ = [("issue_ns", C.c_uint64), ("done_ns", C.c_uint64), ("hit", C.c_int32), ("status", C.c_int32)]
 
 
+class tp_sched_config(C.Structure):
+    _fields_ = [("policy", C.c_int32), ("max_inflight", C.c_int32), ("slo_pct", C.c_double), ("alpha", C.c_double),
+                ("scalar", C.c_double), ("threshold", C.c_double), ("period_ns", C.c_uint64)]
+
+
+class tp_sched_stats(C.Structure):
+    _fields_ = [("alpha", C.c_double), ("periods", C.c_uint32), ("alpha_changes", C.c_uint32),
+                ("compliant", C.c_uint32), ("functions", C.c_uint32)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
 class TorporError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"status {status}: {msg}")
@@ -117,6 +131,12 @@ _SIGS = {
                          C.POINTER(C.c_uint32), C.POINTER(C.c_float)],
     "tp_model_host_image": [_P, C.c_int32, C.POINTER(_P), C.POINTER(C.c_uint64)],
     "tp_run_trace": [_P, C.POINTER(tp_request), C.c_uint32, _P, C.POINTER(tp_request_result)],
+    "tp_run_trace_sched": [_P, C.POINTER(tp_request), C.c_uint32, _P, C.POINTER(tp_sched_config),
+                           C.POINTER(C.c_uint64), C.POINTER(tp_request_result), C.POINTER(tp_sched_stats)],
+    "tph_rrc": [C.c_uint64, C.c_uint64, C.c_double, C.POINTER(C.c_double)],
+    "tph_sched_pick": [C.c_uint32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.c_double, C.c_double, C.c_uint32,
+                       C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_uint8)],
+    "tph_alpha_update": [C.c_double, C.c_double, C.c_double, C.c_double, C.c_double, C.POINTER(C.c_double)],
     "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
     "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                  C.POINTER(C.c_uint32), C.c_uint32, C.POINTER(C.c_uint32)],
@@ -345,6 +365,24 @@ def tp_run_trace(ctx, requests, stream=None):
     return out
 
 
+def tp_run_trace_sched(ctx, requests, deadlines_ns, policy=TP_QUEUE_SLO, max_inflight=2, slo_pct=0.98, alpha=0.5,
+                       scalar=2.0, threshold=0.04, period_ns=1_000_000_000, stream=None):
+    """Like tp_run_trace with a host-side request queue (FIFO or SLO-aware). Returns
+    (results as tp_run_trace gives them, stats dict)."""
+    reqs = list(requests)
+    arr = (tp_request * len(reqs))()
+    for i, (mid, b, x, y, t) in enumerate(reqs):
+        arr[i] = tp_request(mid, b, _ptr(x), _ptr(y), int(t))
+    dl = (C.c_uint64 * len(reqs))(*[int(v) for v in deadlines_ns])
+    cfg = tp_sched_config(policy, max_inflight, slo_pct, alpha, scalar, threshold, period_ns)
+    res = (tp_request_result * len(reqs))()
+    st = tp_sched_stats()
+    status = lib().tp_run_trace_sched(ctx, arr, len(reqs), _ptr(stream), C.byref(cfg), dl, res, C.byref(st))
+    out = [{"issue_ns": r.issue_ns, "done_ns": r.done_ns, "hit": bool(r.hit), "status": r.status} for r in res]
+    _check(lib(), status)
+    return out, st.as_dict()
+
+
 # host-only planning calls; `L` picks the library (the HIP one by default)
 
 def tph_validate(desc: ModelDesc, host_bytes: int, L=None):
@@ -395,6 +433,31 @@ def tph_layer_costs(desc: ModelDesc, host_bytes: int, batch: int, L=None):
     out = (C.c_double * n.value)()
     _check(L, L.tph_layer_costs(C.byref(desc.desc), host_bytes, batch, out, n.value, C.byref(n)))
     return list(out)
+
+
+def tph_rrc(n: int, m: int, p: float, L=None) -> float:
+    L = L or lib()
+    out = C.c_double()
+    _check(L, L.tph_rrc(n, m, p, C.byref(out)))
+    return out.value
+
+
+def tph_sched_pick(n, m, p: float, alpha: float, pending_func, L=None):
+    """(index into pending_func of the request to run next or -1, high-priority flags)."""
+    L = L or lib()
+    nf, npend = len(n), len(pending_func)
+    na, ma = (C.c_uint64 * max(nf, 1))(*n), (C.c_uint64 * max(nf, 1))(*m)
+    pa = (C.c_int32 * max(npend, 1))(*pending_func)
+    pick, high = C.c_int32(), (C.c_uint8 * max(nf, 1))()
+    _check(L, L.tph_sched_pick(nf, na, ma, p, alpha, npend, pa, C.byref(pick), high))
+    return pick.value, [bool(high[i]) for i in range(nf)]
+
+
+def tph_alpha_update(alpha, last_ratio, new_ratio, scalar=2.0, threshold=0.04, L=None) -> float:
+    L = L or lib()
+    out = C.c_double()
+    _check(L, L.tph_alpha_update(alpha, last_ratio, new_ratio, scalar, threshold, C.byref(out)))
+    return out.value
 
 
 class HostArena:
@@ -518,6 +581,10 @@ class Runtime:
     def run_trace(self, requests, stream=None):
         s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
         return tp_run_trace(self.ctx, requests, s)
+
+    def run_trace_sched(self, requests, deadlines_ns, stream=None, **kw):
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        return tp_run_trace_sched(self.ctx, requests, deadlines_ns, stream=s, **kw)
 
     def extent(self, mid):
         """The model's arena bytes (a view of the arena), when resident."""

@@ -26,7 +26,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 31, sorted(names)
+    assert len(names) == 35, sorted(names)
     L = tp.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -260,3 +260,31 @@ def test_cost_plan_of_workloads(cfg, batch):
     # the transfer alone bounds the modelled time from below
     assert est >= m.total_bytes / 57e3
     assert all(u > 0 for u in us)
+
+
+@settings(max_examples=200, deadline=None)
+@given(counts=st.lists(st.tuples(st.integers(0, 60), st.integers(0, 60)), min_size=1, max_size=12),
+       alpha=st.sampled_from([0.0, 0.03125, 0.125, 0.25, 0.5, 0.75, 1.0]),
+       p=st.sampled_from([0.5, 0.9, 0.98, 0.99]), pend=st.lists(st.integers(0, 11), max_size=20))
+def test_sched_pick_matches_oracle(counts, alpha, p, pend):
+    from oracle import slo_queue
+    n = [max(a, b) for a, b in counts]
+    m = [min(a, b) for a, b in counts]
+    pend = [f % len(n) for f in pend]
+    rr = [slo_queue.rrc(a, b, p) for a, b in zip(n, m)]
+    want_high = slo_queue.high_group(rr, alpha)
+    want = slo_queue.pick(rr, want_high, pend)
+    for L in (tp.lib(), tp.host_lib()):
+        got, high = tp.tph_sched_pick(n, m, p, alpha, pend, L=L)
+        assert high == want_high and got == want
+        assert tp.tph_rrc(n[0], m[0], p, L=L) == pytest.approx(rr[0])
+
+
+@pytest.mark.parametrize("alpha,last,new", [(0.25, 0.5, 0.6), (0.75, 0.5, 0.6), (0.5, 0.6, 0.5), (0.5, 0.6, 0.63),
+                                            (1.0, 0.2, 0.9), (0.01, 0.9, 0.1)])
+def test_alpha_update_matches_oracle(alpha, last, new):
+    from oracle import slo_queue
+    for L in (tp.lib(), tp.host_lib()):
+        assert tp.tph_alpha_update(alpha, last, new, 2.0, 0.04, L=L) == slo_queue.alpha_update(alpha, last, new, 2.0, 0.04)
+    with pytest.raises(tp.TorporError):
+        tp.tph_alpha_update(alpha, last, new, 1.0, 0.04, L=tp.host_lib())

@@ -66,3 +66,54 @@ def test_tenant_trace_lru_and_first_outputs(policy):
         log(f"  model {k} ({models[k].arch}) first request {r}: error {err:.2e}")
         assert np.all(np.isfinite(y)) and err <= 2e-2
     rt.close()
+
+
+@pytest.mark.parametrize("policy", [tp.TP_QUEUE_FIFO, tp.TP_QUEUE_SLO])
+def test_scheduled_replay(policy):
+    # the same scaled workload at 4x the arrival rate with a host-side queue: every request
+    # completes after its arrival and issue, at most max_inflight are outstanding, FIFO issues
+    # in arrival order, and the first output of every model matches the oracle
+    torch, dev = torch_dev()
+    specs = synth.tenant_models(9)
+    models = [m for _, m in synth.build_models(specs, workers=9)]
+    trace = synth.tenant_trace(120, rate_per_s=200.0, n_models=9)
+    cap = (models[0].total_bytes + models[1].total_bytes + models[2].total_bytes) // 256 * 256 + (64 << 20)
+    ws = max(tp.tp_workspace_bytes(tp.ModelDesc.of(m), 1) for m in models)
+    rt = tp.Runtime(cap, ws)
+    ids = [rt.register(tp.ModelDesc.of(m), m.blob()) for m in models]
+    deadline_ms = {"mlp": 40.0, "resnet50": 3.0, "bert": 12.0}
+    xs_np, reqs, outs, dls = [], [], [], []
+    for r in range(len(trace.model)):
+        m = models[int(trace.model[r])]
+        x_np = synth.request_input(m, int(trace.input_seed[r]))
+        xs_np.append(x_np)
+        y = torch.full(out_shape(m, 1), float("nan"), dtype=torch.float32, device=dev)
+        outs.append(y)
+        reqs.append((ids[int(trace.model[r])], 1, to_device(x_np), y, int(trace.arrival_s[r] * 1e9)))
+        dls.append(int(deadline_ms[m.arch] * 1e6))
+    torch.cuda.synchronize()
+    res, stats = rt.run_trace_sched(reqs, dls, policy=policy, max_inflight=2, period_ns=100_000_000)
+    torch.cuda.synchronize()
+    log(f"policy {policy}: stats {stats}")
+    assert all(r["status"] == 0 for r in res)
+    for r, q in zip(res, reqs):
+        assert q[4] <= r["issue_ns"] <= r["done_ns"]
+    events = sorted([(r["issue_ns"], 1) for r in res] + [(r["done_ns"], -1) for r in res], key=lambda e: (e[0], e[1]))
+    live = 0
+    for _, d in events:
+        live += d
+        assert live <= 2
+    if policy == tp.TP_QUEUE_FIFO:
+        assert [r["issue_ns"] for r in res] == sorted(r["issue_ns"] for r in res)
+    assert stats["functions"] == len(set(int(v) for v in trace.model)) and stats["compliant"] <= stats["functions"]
+    assert 0 < stats["alpha"] <= 1 and stats["periods"] >= 1
+    seen = set()
+    for r, q in enumerate(reqs):
+        k = int(trace.model[r])
+        if k in seen:
+            continue
+        seen.add(k)
+        y = outs[r].cpu().numpy()
+        err = oracle.normwise_error(y, oracle.forward(models[k], xs_np[r])).max()
+        assert np.all(np.isfinite(y)) and err <= 2e-2, (k, err)
+    rt.close()

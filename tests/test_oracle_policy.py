@@ -188,3 +188,49 @@ def test_heaviness_class_change_applies_to_later_evictions():
     a.request(0); a.request(1)
     a.set_heavy(1, False)
     assert a.request(2)["evicted"] == [1]             # LRU would have taken model 0
+
+
+# ------------------------------------------------------------------ SLO-aware queueing
+
+from oracle import slo_queue
+
+
+def test_rrc_solves_its_defining_equation():
+    # (m + RRC) / (n + RRC) = p, multiplied out: m + RRC = p (n + RRC)
+    for n, m, p in [(0, 0, 0.98), (10, 10, 0.98), (10, 7, 0.9), (50, 49, 0.98), (100, 60, 0.5), (3, 0, 0.99)]:
+        r = slo_queue.rrc(n, m, p)
+        assert m + r == pytest.approx(p * (n + r), abs=1e-9)
+    # a function already above its percentile needs nothing more: RRC <= 0
+    assert slo_queue.rrc(100, 99, 0.98) < 0 and slo_queue.rrc(100, 98, 0.98) == pytest.approx(0)
+    assert slo_queue.rrc(100, 90, 0.98) == pytest.approx((98 - 90) / 0.02)
+
+
+def test_high_group_threshold():
+    rr = [5.0, -2.0, 1.0, 3.0, 0.0]          # sorted: f1 (-2), f4 (0), f2 (1), f3 (3), f0 (5); total 9
+    assert slo_queue.high_group(rr, 0.0) == [False, True, False, False, True]   # only non-positive
+    assert slo_queue.high_group(rr, 1 / 9) == [False, True, True, False, True]  # prefix 1 <= 1
+    assert slo_queue.high_group(rr, 4 / 9) == [False, True, True, True, True]   # prefix 4 <= 4
+    assert slo_queue.high_group(rr, 0.4) == [False, True, True, False, True]    # 4 > 3.6
+    assert slo_queue.high_group(rr, 1.0) == [True] * 5
+    assert slo_queue.high_group([-1.0, -3.0], 0.0) == [True, True]             # no positive RRC
+
+
+def test_pick_order_within_and_across_groups():
+    rr = [5.0, -2.0, 1.0, 3.0, 0.0]
+    high = slo_queue.high_group(rr, 4 / 9)    # f1, f2, f3, f4 high; f0 low
+    # high group first, largest RRC first: f3; its earliest queued request
+    assert slo_queue.pick(rr, high, [0, 1, 3, 2, 3]) == 2
+    assert slo_queue.pick(rr, high, [0, 4, 1]) == 1          # f4 (0) before f1 (-2)
+    assert slo_queue.pick(rr, high, [0, 0]) == 0             # only the low group: f0
+    low = [False] * 5                                        # all low: smallest RRC first
+    assert slo_queue.pick(rr, low, [0, 3, 1, 2]) == 2
+    assert slo_queue.pick([1.0, 1.0], [True, True], [1, 0]) == 1   # tie: lower index
+    assert slo_queue.pick(rr, high, []) == -1
+
+
+def test_alpha_auto_configuration_steps():
+    assert slo_queue.alpha_update(0.25, 0.50, 0.60) == 0.5          # rose by 0.10 > 0.04
+    assert slo_queue.alpha_update(0.75, 0.50, 0.60) == 1.0          # capped at 1
+    assert slo_queue.alpha_update(0.5, 0.60, 0.50) == 0.25          # fell
+    assert slo_queue.alpha_update(0.5, 0.60, 0.63) == 0.5           # within the threshold
+    assert slo_queue.alpha_update(0.5, 0.60, 0.63, scalar=3.0, threshold=-0.01) == 1.0
