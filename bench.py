@@ -242,6 +242,26 @@ def ablation(torch, dev, chunk, link_gbs, budget_s=2.5, max_reps=20):
     return out
 
 
+def native_alloc_us(sizes, reps=10):
+    """p50 of hipMalloc + hipFree of each size (the per-swap allocation that a reserved arena
+    avoids), through the HIP runtime torch has loaded."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so.7", mode=ctypes.RTLD_GLOBAL)   # the copy torch has loaded
+    out = {}
+    for name, nb in sizes.items():
+        ts = []
+        for _ in range(reps):
+            p = ctypes.c_void_p()
+            t0 = time.perf_counter()
+            if hip.hipMalloc(ctypes.byref(p), ctypes.c_size_t(nb)) != 0:
+                raise RuntimeError("hipMalloc failed")
+            if hip.hipFree(p) != 0:
+                raise RuntimeError("hipFree failed")
+            ts.append((time.perf_counter() - t0) * 1e6)
+        out[name] = round(p50(ts), 1)
+    return out
+
+
 def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost", queue=None, rate=50.0,
             deadline_ms=None, slo_pct=0.98):
     """Open-loop multi-tenant run: n_models registered models of the three families, an
@@ -314,6 +334,12 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                       "p99_ms": round(float(np.percentile(lat[sel], 99)), 3),
                       "hit_rate": round(float(hit[sel].mean()), 4)}
     delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped")}
+    calls = st1["admit_calls"] - st0["admit_calls"]
+    admit = {"admissions": calls,
+             "mean_us": round((st1["admit_ns_total"] - st0["admit_ns_total"]) / max(calls, 1) / 1e3, 2),
+             "max_us_since_start": round(st1["admit_ns_max"] / 1e3, 2),
+             "native_alloc_us": native_alloc_us({a: host_bytes[next(m for m in ids if kinds[m] == a)]
+                                                 for a in set(kinds.values())})}
     slo = None
     if queue is not None:
         # a function (model) complies when at least slo_pct of its requests met their deadline
@@ -333,7 +359,7 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
             "hit_rate": round(float(hit.mean()), 4), "requests": n_requests, "models": n_models,
             "arena_gib": arena_gib, "registered_host_bytes": int(sum(host_bytes.values())),
             "register_s": round(reg_s, 1), "trace_s": round(float(trace.arrival_s[-1]), 2),
-            "per_family": per, "arena": delta, "heavy_by_family": heavy, "slo": slo,
+            "per_family": per, "arena": delta, "admission": admit, "heavy_by_family": heavy, "slo": slo,
             "config": {"workload": f"{n_models} models (24x4096 MLP / ResNet-50 / BERT-base by index mod 3), "
                                    f"Poisson {rate:g} req/s, Zipf(1.1), {arena_gib} GiB arena, batch 1",
                        "eviction": evict, "chunk_plan": plan}}

@@ -183,6 +183,9 @@ typedef struct {
   uint64_t capacity, used, largest_free;
   uint32_t resident, registered;
   uint64_t hits, misses, evictions, frag_evictions, bytes_swapped;
+  /* host time of admissions (the arena decision, victim retirement and the copy stream's
+   * ordering waits) of the requests that missed, in tp_infer / tp_swap_in: count, sum, max */
+  uint64_t admit_calls, admit_ns_total, admit_ns_max;
 } tp_arena_stats_t;
 
 typedef struct {

@@ -106,6 +106,7 @@ void Arena::stats(tp_arena_stats_t* s) const {
   s->evictions = evictions_;
   s->frag_evictions = frag_evictions_;
   s->bytes_swapped = swapped_;
+  s->admit_calls = s->admit_ns_total = s->admit_ns_max = 0;   // timed by the runtime
 }
 
 }  // namespace tp

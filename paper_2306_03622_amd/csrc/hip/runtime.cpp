@@ -4,6 +4,7 @@
 #include "runtime.hpp"
 
 #include <algorithm>
+#include <chrono>
 #include <cstring>
 #include <new>
 #include <thread>
@@ -160,9 +161,21 @@ hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
 // the primary copy stream; the chunk copies are then issued by the request's Waiter. On
 // failure the model is left non-resident.
 tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
+  const auto t0 = std::chrono::steady_clock::now();
   Arena::Decision d = c->policy->request(m->id);
   *swapped = !d.hit;
   if (d.hit) return ok();
+  struct Timer {              // host time of this (missing) admission, on every return path
+    tp_ctx* c;
+    std::chrono::steady_clock::time_point t0;
+    ~Timer() {
+      const uint64_t ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                              std::chrono::steady_clock::now() - t0).count();
+      ++c->admit_calls;
+      c->admit_ns_total += ns;
+      c->admit_ns_max = std::max(c->admit_ns_max, ns);
+    }
+  } timer{c, t0};
   m->bg_pending = false;         // a new swap supersedes an earlier one
   tp_status s = TP_OK;
   for (int32_t v : d.victims)
@@ -628,6 +641,9 @@ tp_status tp_is_resident(tp_ctx* c, int32_t id, int32_t* resident) {
 tp_status tp_arena_stats(tp_ctx* c, tp_arena_stats_t* out) {
   if (!c || !out) return fail(TP_E_INVAL, "NULL argument");
   c->policy->stats(out);
+  out->admit_calls = c->admit_calls;
+  out->admit_ns_total = c->admit_ns_total;
+  out->admit_ns_max = c->admit_ns_max;
   return ok();
 }
 

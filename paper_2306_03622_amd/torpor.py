@@ -68,7 +68,8 @@ class tp_arena_stats_t(C.Structure):
     _fields_ = [("capacity", C.c_uint64), ("used", C.c_uint64), ("largest_free", C.c_uint64),
                 ("resident", C.c_uint32), ("registered", C.c_uint32), ("hits", C.c_uint64),
                 ("misses", C.c_uint64), ("evictions", C.c_uint64), ("frag_evictions", C.c_uint64),
-                ("bytes_swapped", C.c_uint64)]
+                ("bytes_swapped", C.c_uint64), ("admit_calls", C.c_uint64), ("admit_ns_total", C.c_uint64),
+                ("admit_ns_max", C.c_uint64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

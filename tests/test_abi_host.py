@@ -131,7 +131,9 @@ def _replay(trace, sizes, cap, L, policy="lru", heavy=None):
             assert e.value.status == tp.TP_E_NOSPC
             continue
         assert ha.request(k) == want
-    assert ha.stats() == {**sim.stats(), "registered": len(sizes)}
+    got = ha.stats()
+    assert {k: got[k] for k in sim.stats()} == sim.stats() and got["registered"] == len(sizes)
+    assert got["admit_calls"] == 0       # admissions are timed by the runtime, not the bookkeeping
 
 
 @settings(max_examples=60, deadline=None)
