@@ -263,10 +263,11 @@ def native_alloc_us(sizes, reps=10):
 
 
 def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost", queue=None, rate=50.0,
-            deadline_ms=None, slo_pct=0.98):
+            deadline_ms=None, slo_pct=0.98, alloc="first-fit", partition_mib=0):
     """Open-loop multi-tenant run: n_models registered models of the three families, an
     arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU or
-    heaviness-aware eviction."""
+    heaviness-aware eviction, first-fit or two-tier partitioned placement (with or without
+    consolidation)."""
     import paper_2306_03622_amd as tp
     import synth
     specs = synth.tenant_models(n_models)
@@ -275,8 +276,11 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
     descs, kinds, host_bytes, heavy = {}, {}, {}, {}
     for cfg in (2, 3, 4):
         ws = max(ws, tp.tp_workspace_bytes(tp.ModelDesc.of(synth.config_model(cfg)), 1))
+    alloc_mode = {"first-fit": tp.TP_ALLOC_FIRST_FIT, "partition": tp.TP_ALLOC_PARTITION,
+                  "consolidate": tp.TP_ALLOC_PARTITION_CONSOLIDATE}[alloc]
     rt = tp.Runtime(arena_gib << 30, ws, plan=tp.TP_PLAN_COST if plan == "cost" else tp.TP_PLAN_GREEDY,
-                    evict_policy=tp.TP_EVICT_HEAVINESS if evict == "heaviness" else tp.TP_EVICT_LRU)
+                    evict_policy=tp.TP_EVICT_HEAVINESS if evict == "heaviness" else tp.TP_EVICT_LRU,
+                    alloc=alloc_mode, partition_bytes=partition_mib << 20)
     t0 = time.perf_counter()
     ids = []
     for i, m in synth.build_models(specs, workers):
@@ -333,11 +337,16 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
             per[a] = {"requests": int(sel.sum()), "p50_ms": round(float(np.percentile(lat[sel], 50)), 3),
                       "p99_ms": round(float(np.percentile(lat[sel], 99)), 3),
                       "hit_rate": round(float(hit[sel].mean()), 4)}
-    delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped")}
+    delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
+                                          "evacuations", "bytes_moved")}
+    delta["partitions"] = st1["partitions"]
     calls = st1["admit_calls"] - st0["admit_calls"]
+    adm = np.array([r["admit_ns"] / 1e3 for r in res if not r["hit"]])
     admit = {"admissions": calls,
              "mean_us": round((st1["admit_ns_total"] - st0["admit_ns_total"]) / max(calls, 1) / 1e3, 2),
              "max_us_since_start": round(st1["admit_ns_max"] / 1e3, 2),
+             "cdf_us": ({f"p{q}": round(float(np.percentile(adm, q)), 2) for q in (50, 90, 99)} |
+                        {"max": round(float(adm.max()), 2)}) if adm.size else None,
              "native_alloc_us": native_alloc_us({a: host_bytes[next(m for m in ids if kinds[m] == a)]
                                                  for a in set(kinds.values())})}
     slo = None
@@ -362,7 +371,8 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
             "per_family": per, "arena": delta, "admission": admit, "heavy_by_family": heavy, "slo": slo,
             "config": {"workload": f"{n_models} models (24x4096 MLP / ResNet-50 / BERT-base by index mod 3), "
                                    f"Poisson {rate:g} req/s, Zipf(1.1), {arena_gib} GiB arena, batch 1",
-                       "eviction": evict, "chunk_plan": plan}}
+                       "eviction": evict, "chunk_plan": plan, "placement": alloc,
+                       "partition_mib": (partition_mib or (arena_gib << 10) // 8) if alloc != "first-fit" else None}}
 
 
 def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, link, steps, warmup, trace):
@@ -493,6 +503,11 @@ def main():
     ap.add_argument("--tenant-arena-gib", type=int, default=8)
     ap.add_argument("--evict", choices=["lru", "heaviness"], default="lru",
                     help="eviction policy of the multi-tenant run")
+    ap.add_argument("--alloc", choices=["first-fit", "partition", "consolidate"], default="first-fit",
+                    help="multi-tenant arena placement: first fit, two-tier partitions, or partitions with "
+                         "consolidation")
+    ap.add_argument("--partition-mib", type=int, default=0,
+                    help="partition size of --alloc partition/consolidate (0: arena / 8)")
     ap.add_argument("--queue", choices=["none", "fifo", "slo"], default="none",
                     help="multi-tenant run: host-side request queue (FIFO or SLO-aware) instead of issuing at arrival")
     ap.add_argument("--rate", type=float, default=50.0, help="multi-tenant arrival rate (requests/s)")
@@ -544,7 +559,8 @@ def main():
     if a.tenants:
         dl = dict(zip(("mlp", "resnet50", "bert"), (float(v) for v in a.deadlines.split(","))))
         print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16, a.evict, a.plan,
-                                 None if a.queue == "none" else a.queue, a.rate, dl)), flush=True)
+                                 None if a.queue == "none" else a.queue, a.rate, dl, alloc=a.alloc,
+                                 partition_mib=a.partition_mib)), flush=True)
         return
 
     if a.ablation:

@@ -146,7 +146,7 @@ enum {
  *     TP_FLAG_PER_TENSOR. */
 enum { TP_PLAN_GREEDY = 0, TP_PLAN_COST = 1 };
 /* evict_policy chooses the victim when a non-resident model needs room (one victim at a
- * time until a first-fit gap exists):
+ * time until a placement exists, see alloc):
  *   TP_EVICT_LRU: the least recently used resident model.
  *   TP_EVICT_HEAVINESS: the paper's policy (Sec. 5.4, "Model eviction policy"): light
  *     models first (least recently used among them), and only when no light model is
@@ -158,6 +158,26 @@ enum { TP_PLAN_GREEDY = 0, TP_PLAN_COST = 1 };
  *     (about 3.4x; Sec. 7, table of remoting and swapping latencies). */
 enum { TP_EVICT_LRU = 0, TP_EVICT_HEAVINESS = 1 };
 enum { TP_CLASS_AUTO = 0, TP_CLASS_LIGHT = 1, TP_CLASS_HEAVY = 2 };
+/* alloc chooses where in the arena a model's extent goes:
+ *   TP_ALLOC_FIRST_FIT: the lowest-addressed free gap that fits.
+ *   TP_ALLOC_PARTITION: the paper's two-tier scheme (appendix "Memory Block Allocation"): the
+ *     arena is cut into partitions of partition_bytes (0: the arena size / 8 rounded down to a
+ *     MiB, at least 256 bytes; otherwise a multiple of 256); a short remainder of at least 256
+ *     bytes is one more partition. A model no larger than a partition takes a slot of a
+ *     partition dedicated to its size (the size rounded up to 256 bytes) when at least two
+ *     registered models have that size, else a buddy block (sizes: a partition halved while
+ *     the half stays a multiple of 256) in a buddy-managed partition; a larger model takes a
+ *     run of consecutive free partitions. Fullest candidate partitions first; runs from the
+ *     low end, new slot or buddy partitions from the high end. A partition is free again when
+ *     its last model leaves. Victims (evict_policy) are taken one at a time until a placement
+ *     exists.
+ *   TP_ALLOC_PARTITION_CONSOLIDATE: as TP_ALLOC_PARTITION, and before each eviction one slot or
+ *     buddy partition is evacuated if possible (the appendix's consolidation across
+ *     partitions): the one with the fewest bytes in use whose models all fit, by the same
+ *     rules, in other partitions without taking a free one; they are copied there
+ *     device-to-device on the copy stream (after their swap-in and the destination's previous
+ *     readers), and the moved model's next request waits for its copy. */
+enum { TP_ALLOC_FIRST_FIT = 0, TP_ALLOC_PARTITION = 1, TP_ALLOC_PARTITION_CONSOLIDATE = 2 };
 typedef struct {
   void* arena_dev;
   uint64_t arena_bytes;
@@ -177,6 +197,8 @@ typedef struct {
   float chunk_us;
   int32_t evict_policy;   /* TP_EVICT_* */
   float heavy_ratio;
+  int32_t alloc;          /* TP_ALLOC_* */
+  uint64_t partition_bytes;
 } tp_config;
 
 typedef struct {
@@ -186,6 +208,8 @@ typedef struct {
   /* host time of admissions (the arena decision, victim retirement and the copy stream's
    * ordering waits) of the requests that missed, in tp_infer / tp_swap_in: count, sum, max */
   uint64_t admit_calls, admit_ns_total, admit_ns_max;
+  uint32_t partitions, partitions_free;   /* TP_ALLOC_PARTITION*: partitions in all, unoccupied */
+  uint64_t evacuations, bytes_moved;      /* TP_ALLOC_PARTITION_CONSOLIDATE: partitions freed by moves, bytes moved */
 } tp_arena_stats_t;
 
 typedef struct {
@@ -297,6 +321,7 @@ typedef struct {
   uint64_t done_ns;         /* when the host observed the request's completion */
   int32_t hit;              /* the model was resident when the request was issued */
   int32_t status;           /* tp_infer's status for this request */
+  uint64_t admit_ns;        /* host time of the request's admission if it missed, else 0 */
 } tp_request_result;
 
 /* Replays an open-loop request trace (the paper's serving setting, Sec. 3 and Sec. 7: requests

@@ -87,6 +87,16 @@ TP_API tp_status tph_arena_evict(struct tph_arena* a, int32_t model_id);
 /* Eviction policy (TP_EVICT_*, default LRU) and a model's class for TP_EVICT_HEAVINESS. */
 TP_API tp_status tph_arena_set_policy(struct tph_arena* a, int32_t policy);
 TP_API tp_status tph_arena_set_heavy(struct tph_arena* a, int32_t model_id, int32_t heavy);
+/* Placement: partition_bytes > 0 switches to the two-tier partition scheme of TP_ALLOC_PARTITION
+ * (torpor.h) with partitions of that size (a multiple of the alignment), with consolidation
+ * (TP_ALLOC_PARTITION_CONSOLIDATE) if `consolidate`; 0 back to first fit. TP_E_STATE while
+ * any model is resident, TP_E_INVAL for a size that is not a multiple. tph_arena_request
+ * reports no moves; tph_arena_moves gives the last request's. */
+TP_API tp_status tph_arena_set_partitioned(struct tph_arena* a, uint64_t partition_bytes, int32_t consolidate);
+/* The consolidation moves of the last tph_arena_request: up to `cap` (model, old offset, new
+ * offset) triples in the order made; *n receives their count. */
+TP_API tp_status tph_arena_moves(struct tph_arena* a, int32_t* model_id, uint64_t* from, uint64_t* to, uint32_t cap,
+                                 uint32_t* n);
 TP_API tp_status tph_arena_stats(struct tph_arena* a, tp_arena_stats_t* out);
 
 #ifdef __cplusplus

@@ -17,4 +17,4 @@ under a grouping (``pipeline``), and the SLO-aware queueing rules (``slo_queue``
 Precision: float64 by default (the paper fixes none); ``dt=np.float32`` gives the fp32
 variant. bf16 weights and inputs are widened exactly.
 """
-from . import ops, forward, arena_sim, chunks, pipeline, slo_queue  # noqa: F401
+from . import ops, forward, arena_sim, partition_sim, chunks, pipeline, slo_queue  # noqa: F401

@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libtorpor.so")
 HOST_LIB = os.path.join(PKG, "libtorpor_host.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-CORE = ["core/model.cpp", "core/arena.cpp", "core/sched.cpp", "core/plan_api.cpp", "core/errors.cpp"]
+CORE = ["core/model.cpp", "core/arena.cpp", "core/partition.cpp", "core/sched.cpp", "core/plan_api.cpp", "core/errors.cpp"]
 HIP_HOST = ["hip/runtime.cpp", "hip/executors.cpp", "hip/trace.cpp"]
 KERNELS = ["kernels/gemm_bf16.hip", "kernels/gemv_bf16.hip", "kernels/linear_f32.hip", "kernels/norm.hip", "kernels/attention.hip",
            "kernels/pool_copy.hip"]

@@ -10,12 +10,32 @@ tp_status Arena::add_model(int32_t id, uint64_t bytes, bool heavy) {
   r.bytes = (bytes + align_ - 1) / align_ * align_;
   r.heavy = heavy;
   models_[id] = r;
+  ++class_count_[r.bytes];
   return TP_OK;
 }
 
 void Arena::remove_model(int32_t id) {
   evict(id);
-  models_.erase(id);
+  auto it = models_.find(id);
+  if (it == models_.end()) return;
+  if (--class_count_[it->second.bytes] == 0) class_count_.erase(it->second.bytes);
+  models_.erase(it);
+}
+
+tp_status Arena::set_partitioned(uint64_t part_bytes, bool consolidate) {
+  if (!by_addr_.empty()) return TP_E_STATE;
+  if (part_bytes % align_) return TP_E_INVAL;
+  consolidate_ = consolidate && part_bytes;
+  if (part_bytes == 0)
+    parts_.reset();
+  else
+    parts_.reset(new Partitions(capacity_, part_bytes, align_));
+  return TP_OK;
+}
+
+bool Arena::place(int32_t id, uint64_t need, uint64_t* off) {
+  if (!parts_) return first_fit(need, off);
+  return parts_->place(id, need, class_count_.at(need) >= 2, off);
 }
 
 uint64_t Arena::used() const {
@@ -65,8 +85,28 @@ Arena::Decision Arena::request(int32_t id) {
   }
   ++misses_;
   uint64_t off = 0;
-  while (!first_fit(me.bytes, &off)) {
+  while (!place(id, me.bytes, &off)) {
+    if (consolidate_) {
+      std::vector<Partitions::Move> mv;
+      const bool moved = parts_->evacuate([&](int32_t m) { return models_.at(m).bytes; },
+                                          [&](int32_t m) { return class_count_.at(models_.at(m).bytes) >= 2; }, &mv);
+      if (moved) {
+        for (const auto& x : mv) {
+          models_.at(x.id).offset = x.to;
+          moved_ += models_.at(x.id).bytes;
+          d.moves.push_back(x);
+        }
+        std::sort(by_addr_.begin(), by_addr_.end(),
+                  [&](int32_t a, int32_t b) { return models_.at(a).offset < models_.at(b).offset; });
+        ++evacuations_;
+        continue;
+      }
+    }
     const int32_t victim = this->victim();
+    if (victim < 0) {               // nothing left to evict: only if !fits_at_all(id)
+      d.placed = false;
+      return d;
+    }
     if (capacity_ - used() >= me.bytes) ++frag_evictions_;
     evict(victim);
     ++evictions_;
@@ -87,6 +127,7 @@ void Arena::evict(int32_t id) {
   if (it == models_.end() || !it->second.resident) return;
   it->second.resident = false;
   by_addr_.erase(std::find(by_addr_.begin(), by_addr_.end(), id));
+  if (parts_) parts_->release(id);
 }
 
 void Arena::stats(tp_arena_stats_t* s) const {
@@ -107,6 +148,10 @@ void Arena::stats(tp_arena_stats_t* s) const {
   s->frag_evictions = frag_evictions_;
   s->bytes_swapped = swapped_;
   s->admit_calls = s->admit_ns_total = s->admit_ns_max = 0;   // timed by the runtime
+  s->evacuations = evacuations_;
+  s->bytes_moved = moved_;
+  s->partitions = parts_ ? parts_->count() : 0;
+  s->partitions_free = parts_ ? parts_->free_count() : 0;
 }
 
 }  // namespace tp

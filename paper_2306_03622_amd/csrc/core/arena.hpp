@@ -3,12 +3,16 @@
 // (invalidate only) one victim at a time until a gap fits: least recently used, or, under
 // the heaviness-aware policy, the least recently used light model while one is resident and
 // only then the least recently used heavy one. Host-only C++; the runtime attaches
-// device-side ordering (events) to the decisions made here.
+// device-side ordering (events) to the decisions made here. With partitioned placement
+// (set_partitioned) the offset comes from the two-tier partition scheme instead of first
+// fit; a size class is common while at least two registered models have it.
 #pragma once
 #include <cstdint>
+#include <memory>
 #include <unordered_map>
 #include <vector>
 
+#include "partition.hpp"
 #include "torpor.h"
 
 namespace tp {
@@ -20,14 +24,21 @@ class Arena {
 
   struct Decision {
     bool hit = false;
+    bool placed = true;             // false: the model cannot be placed even in an empty arena
     uint64_t offset = 0;
     std::vector<int32_t> victims;   // evicted by this request, in eviction order
+    std::vector<Partitions::Move> moves;   // consolidation moves, in the order made (before victims')
   };
 
   tp_status add_model(int32_t id, uint64_t bytes, bool heavy = false);
   void set_heavy(int32_t id, bool heavy) { models_.at(id).heavy = heavy; }
   bool heavy(int32_t id) const { return models_.at(id).heavy; }
   void set_policy(int policy) { policy_ = policy; }
+  // Switches placement to partitions of part_bytes (a multiple of the alignment; 0 turns
+  // partitioning off), with or without consolidation (partition evacuation before each
+  // eviction). TP_E_STATE while any model is resident, TP_E_INVAL for a bad size.
+  tp_status set_partitioned(uint64_t part_bytes, bool consolidate = false);
+  const Partitions* partitions() const { return parts_.get(); }
   void remove_model(int32_t id);               // also drops residency
   bool known(int32_t id) const { return models_.count(id) != 0; }
   bool fits_at_all(int32_t id) const { return models_.at(id).bytes <= capacity_; }
@@ -51,6 +62,7 @@ class Arena {
     bool heavy = false;
   };
   bool first_fit(uint64_t need, uint64_t* off) const;
+  bool place(int32_t id, uint64_t need, uint64_t* off);
   int32_t victim() const;
   uint64_t used() const;
 
@@ -58,8 +70,12 @@ class Arena {
   int policy_;
   uint64_t clock_ = 0;
   uint64_t hits_ = 0, misses_ = 0, evictions_ = 0, frag_evictions_ = 0, swapped_ = 0;
+  uint64_t evacuations_ = 0, moved_ = 0;
+  bool consolidate_ = false;
   std::unordered_map<int32_t, Rec> models_;
   std::vector<int32_t> by_addr_;                // resident ids sorted by offset
+  std::unique_ptr<Partitions> parts_;           // partitioned placement, else first fit
+  std::unordered_map<uint64_t, uint32_t> class_count_;   // registered models per size
 };
 
 }  // namespace tp

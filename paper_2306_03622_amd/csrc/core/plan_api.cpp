@@ -11,6 +11,7 @@ using namespace tp;
 
 struct tph_arena {
   Arena a;
+  std::vector<Partitions::Move> last_moves;
   tph_arena(uint64_t c, uint64_t al) : a(c, al) {}
 };
 
@@ -160,9 +161,12 @@ tp_status tph_arena_unregister(tph_arena* a, int32_t id) {
 tp_status tph_arena_request(tph_arena* a, int32_t id, int32_t* hit, uint64_t* offset, int32_t* victims,
                             uint32_t cap, uint32_t* n_victims) {
   if (!a) return fail(TP_E_INVAL, "NULL arena");
+  a->last_moves.clear();
   if (!a->a.known(id)) return fail(TP_E_NOENT, "unknown model id");
   if (!a->a.fits_at_all(id)) return fail(TP_E_NOSPC, "model larger than the arena");
   Arena::Decision d = a->a.request(id);
+  a->last_moves = d.moves;
+  if (!d.placed) return fail(TP_E_NOSPC, "model cannot be placed in the arena");
   if (hit) *hit = d.hit;
   if (offset) *offset = d.offset;
   if (n_victims) *n_victims = (uint32_t)d.victims.size();
@@ -188,6 +192,25 @@ tp_status tph_arena_set_heavy(tph_arena* a, int32_t id, int32_t heavy) {
   if (!a) return fail(TP_E_INVAL, "NULL arena");
   if (!a->a.known(id)) return fail(TP_E_NOENT, "unknown model id");
   a->a.set_heavy(id, heavy != 0);
+  return ok();
+}
+
+tp_status tph_arena_moves(tph_arena* a, int32_t* model_id, uint64_t* from, uint64_t* to, uint32_t cap, uint32_t* n) {
+  if (!a || !n) return fail(TP_E_INVAL, "NULL argument");
+  *n = (uint32_t)a->last_moves.size();
+  for (uint32_t i = 0; i < a->last_moves.size() && i < cap; ++i) {
+    if (model_id) model_id[i] = a->last_moves[i].id;
+    if (from) from[i] = a->last_moves[i].from;
+    if (to) to[i] = a->last_moves[i].to;
+  }
+  return ok();
+}
+
+tp_status tph_arena_set_partitioned(tph_arena* a, uint64_t partition_bytes, int32_t consolidate) {
+  if (!a) return fail(TP_E_INVAL, "NULL arena");
+  const tp_status s = a->a.set_partitioned(partition_bytes, consolidate != 0);
+  if (s == TP_E_STATE) return fail(s, "tph_arena_set_partitioned: models are resident");
+  if (s != TP_OK) return fail(s, "tph_arena_set_partitioned: partition size not a multiple of the alignment");
   return ok();
 }
 

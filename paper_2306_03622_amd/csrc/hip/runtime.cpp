@@ -157,12 +157,32 @@ hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
   return e;
 }
 
-// One request's admission: a hit, or victims invalidated and their readers waited for on
-// the primary copy stream; the chunk copies are then issued by the request's Waiter. On
-// failure the model is left non-resident.
+// A consolidation move of resident model `x` from arena offset `from` to `to`, on the primary
+// copy stream: after the destination's retired owners and x's own swap-in (its last chunk
+// on each copy stream), a device-to-device copy of x's image; x's last chunk event is then
+// recorded after the copy and x marked pending, so x's next request waits for it (settle).
+// The old extent is retired under x, like an eviction: whoever writes it next waits for x's
+// enqueued readers; the copy itself precedes any later write on the copy streams.
+tp_status move_extent(tp_ctx* c, Model* x, uint64_t from, uint64_t to) {
+  const uint64_t len = c->policy->bytes(x->id);
+  tp_status s = claim(c, to, len);
+  if (s != TP_OK) return s;
+  const size_t n = x->chunk_ev.size();
+  TP_HIP(hipStreamWaitEvent(c->copy[0], x->chunk_ev[n - 1], 0));
+  if (c->ncopy == 2 && n > 1) TP_HIP(hipStreamWaitEvent(c->copy[0], x->chunk_ev[n - 2], 0));
+  TP_HIP(hipMemcpyAsync(c->arena + to, c->arena + from, x->spec.host_bytes, hipMemcpyDeviceToDevice, c->copy[0]));
+  TP_HIP(hipEventRecord(x->chunk_ev.back(), c->copy[0]));
+  x->bg_pending = true;
+  return retire(c, x->id, from, len);
+}
+
+// One request's admission: a hit, or consolidation moves made and victims invalidated and
+// their readers waited for on the primary copy stream; the chunk copies are then issued by
+// the request's Waiter. On failure the model is left non-resident.
 tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   const auto t0 = std::chrono::steady_clock::now();
   Arena::Decision d = c->policy->request(m->id);
+  if (!d.placed) return fail(TP_E_NOSPC, "model cannot be placed in the arena");
   *swapped = !d.hit;
   if (d.hit) return ok();
   struct Timer {              // host time of this (missing) admission, on every return path
@@ -172,17 +192,26 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
       const uint64_t ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
                               std::chrono::steady_clock::now() - t0).count();
       ++c->admit_calls;
+      c->last_admit_ns = ns;
       c->admit_ns_total += ns;
       c->admit_ns_max = std::max(c->admit_ns_max, ns);
     }
   } timer{c, t0};
   m->bg_pending = false;         // a new swap supersedes an earlier one
   tp_status s = TP_OK;
+  for (const auto& mv : d.moves)
+    if (s == TP_OK) s = move_extent(c, find(c, mv.id), mv.from, mv.to);
   for (int32_t v : d.victims)
     if (s == TP_OK) s = retire(c, v, c->policy->offset(v), c->policy->bytes(v));
   if (s == TP_OK) s = claim(c, d.offset, m->spec.host_bytes);
   if (s != TP_OK) {
     const std::string msg = last_error();
+    for (const auto& mv : d.moves) {       // a move may not have been copied: drop the moved models
+      const uint64_t len = c->policy->bytes(mv.id);
+      c->policy->evict(mv.id);
+      (void)retire(c, mv.id, mv.from, len);
+      (void)retire(c, mv.id, mv.to, len);
+    }
     c->policy->evict(m->id);
     (void)retire(c, m->id, d.offset, m->spec.host_bytes);
     return fail(s, msg);
@@ -333,6 +362,9 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   if ((cfg->evict_policy != TP_EVICT_LRU && cfg->evict_policy != TP_EVICT_HEAVINESS) || !(cfg->heavy_ratio >= 0) ||
       cfg->heavy_ratio > 1e6)
     return fail(TP_E_INVAL, "tp_create: evict_policy or heavy_ratio out of range");
+  if (cfg->alloc < TP_ALLOC_FIRST_FIT || cfg->alloc > TP_ALLOC_PARTITION_CONSOLIDATE ||
+      (cfg->alloc != TP_ALLOC_FIRST_FIT && cfg->partition_bytes % 256))
+    return fail(TP_E_INVAL, "tp_create: alloc or partition_bytes out of range");
   std::unique_ptr<tp_ctx> c(new (std::nothrow) tp_ctx);
   if (!c) return fail(TP_E_NOSPC, "out of host memory");
   c->cfg = *cfg;
@@ -340,6 +372,12 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   c->arena = static_cast<char*>(cfg->arena_dev);
   c->work = static_cast<char*>(cfg->work_dev);
   c->policy.reset(new Arena(cfg->arena_bytes, 256, cfg->evict_policy));
+  if (cfg->alloc != TP_ALLOC_FIRST_FIT) {
+    uint64_t part = cfg->partition_bytes;
+    if (!part) part = std::max<uint64_t>(cfg->arena_bytes / 8 / (1u << 20) * (1u << 20), 256);
+    // nothing is resident yet and part is a multiple of 256: cannot fail
+    (void)c->policy->set_partitioned(part, cfg->alloc == TP_ALLOC_PARTITION_CONSOLIDATE);
+  }
   TP_HIP(hipGetDevice(&c->device));
   c->ncopy = cfg->copy_streams == 2 ? 2 : 1;
   hipError_t e = hipSuccess;

@@ -118,6 +118,7 @@ struct tp_ctx {
   bool any_request = false;
   std::vector<hipEvent_t> trace_ev;            // completion ring of tp_run_trace
   uint64_t admit_calls = 0, admit_ns_total = 0, admit_ns_max = 0;   // admissions that missed
+  uint64_t last_admit_ns = 0;                                         // the latest of them
   // extents invalidated but possibly still read by enqueued work of their old owner
   struct Retired {
     uint64_t off, len;

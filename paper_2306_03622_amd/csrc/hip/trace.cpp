@@ -89,7 +89,9 @@ extern "C" tp_status tp_run_trace(tp_ctx* c, const tp_request* reqs, uint32_t n,
     (void)tp_is_resident(c, reqs[i].model_id, &res);
     out[i].hit = res;
     out[i].issue_ns = since(t0);
+    const uint64_t calls = c->admit_calls;
     tp_status st = tp_infer(c, reqs[i].model_id, reqs[i].input_dev, reqs[i].batch, reqs[i].output_dev, stream);
+    out[i].admit_ns = c->admit_calls != calls ? c->last_admit_ns : 0;
     out[i].status = st;
     if (st == TP_OK) {
       hipError_t e = hipEventRecord(c->trace_ev[i % kRing], stream);
@@ -244,7 +246,9 @@ extern "C" tp_status tp_run_trace_sched(tp_ctx* c, const tp_request* reqs, uint3
     out[i].hit = res;
     out[i].issue_ns = since(t0);
     const uint32_t slot = issue_seq % kRing;
+    const uint64_t calls = c->admit_calls;
     tp_status st = tp_infer(c, reqs[i].model_id, reqs[i].input_dev, reqs[i].batch, reqs[i].output_dev, stream);
+    out[i].admit_ns = c->admit_calls != calls ? c->last_admit_ns : 0;
     if (st == TP_OK && hipEventRecord(c->trace_ev[slot], stream) != hipSuccess) st = TP_E_HIP;
     out[i].status = st;
     if (st != TP_OK) {

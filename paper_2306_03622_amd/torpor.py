@@ -28,6 +28,7 @@ TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_
 TP_PLAN_GREEDY, TP_PLAN_COST = 0, 1
 TP_EVICT_LRU, TP_EVICT_HEAVINESS = 0, 1
 TP_CLASS_AUTO, TP_CLASS_LIGHT, TP_CLASS_HEAVY = 0, 1, 2
+TP_ALLOC_FIRST_FIT, TP_ALLOC_PARTITION, TP_ALLOC_PARTITION_CONSOLIDATE = 0, 1, 2
 TP_QUEUE_FIFO, TP_QUEUE_SLO = 0, 1
 ROLES = {
     "w": 0, "b": 1,
@@ -61,7 +62,8 @@ class tp_config(C.Structure):
                 ("copy_method", C.c_int32), ("gather_wgs", C.c_int32), ("flags", C.c_int32),
                 ("throttle_us", C.c_int32), ("copy_streams", C.c_int32), ("direct_max_bytes", C.c_uint64),
                 ("plan", C.c_int32), ("plan_batch", C.c_int32), ("link_gbs", C.c_float), ("chunk_us", C.c_float),
-                ("evict_policy", C.c_int32), ("heavy_ratio", C.c_float)]
+                ("evict_policy", C.c_int32), ("heavy_ratio", C.c_float), ("alloc", C.c_int32),
+                ("partition_bytes", C.c_uint64)]
 
 
 class tp_arena_stats_t(C.Structure):
@@ -69,7 +71,8 @@ class tp_arena_stats_t(C.Structure):
                 ("resident", C.c_uint32), ("registered", C.c_uint32), ("hits", C.c_uint64),
                 ("misses", C.c_uint64), ("evictions", C.c_uint64), ("frag_evictions", C.c_uint64),
                 ("bytes_swapped", C.c_uint64), ("admit_calls", C.c_uint64), ("admit_ns_total", C.c_uint64),
-                ("admit_ns_max", C.c_uint64)]
+                ("admit_ns_max", C.c_uint64), ("partitions", C.c_uint32), ("partitions_free", C.c_uint32),
+                ("evacuations", C.c_uint64), ("bytes_moved", C.c_uint64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -90,7 +93,8 @@ class tp_request(C.Structure):
 
 
 class tp_request_result(C.Structure):
-    _fields_ = [("issue_ns", C.c_uint64), ("done_ns", C.c_uint64), ("hit", C.c_int32), ("status", C.c_int32)]
+    _fields_ = [("issue_ns", C.c_uint64), ("done_ns", C.c_uint64), ("hit", C.c_int32), ("status", C.c_int32),
+                ("admit_ns", C.c_uint64)]
 
 
 class tp_sched_config(C.Structure):
@@ -157,6 +161,9 @@ _SIGS = {
     "tph_arena_evict": [_P, C.c_int32],
     "tph_arena_set_policy": [_P, C.c_int32],
     "tph_arena_set_heavy": [_P, C.c_int32, C.c_int32],
+    "tph_arena_set_partitioned": [_P, C.c_uint64, C.c_int32],
+    "tph_arena_moves": [_P, C.POINTER(C.c_int32), C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.c_uint32,
+                        C.POINTER(C.c_uint32)],
     "tph_arena_stats": [_P, C.POINTER(tp_arena_stats_t)],
 }
 HOST_ONLY = [n for n in _SIGS if n.startswith("tph_")]
@@ -257,11 +264,11 @@ class ModelDesc:
 def tp_create(arena_dev, arena_bytes, work_dev, work_bytes, copy_stream=None, chunk_min_bytes=DEFAULT_CHUNK,
               copy_method=TP_COPY_MEMCPY, gather_wgs=0, flags=0, throttle_us=0, copy_streams=0, direct_max_bytes=0,
               plan=TP_PLAN_GREEDY, plan_batch=0, link_gbs=0.0, chunk_us=0.0, evict_policy=TP_EVICT_LRU,
-              heavy_ratio=0.0):
+              heavy_ratio=0.0, alloc=TP_ALLOC_FIRST_FIT, partition_bytes=0):
     L = lib()
     cfg = tp_config(_ptr(arena_dev), arena_bytes, _ptr(work_dev), work_bytes, _ptr(copy_stream), chunk_min_bytes,
                     copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes, plan, plan_batch,
-                    link_gbs, chunk_us, evict_policy, heavy_ratio)
+                    link_gbs, chunk_us, evict_policy, heavy_ratio, alloc, partition_bytes)
     ctx = _P()
     _check(L, L.tp_create(C.byref(cfg), C.byref(ctx)))
     return ctx
@@ -353,7 +360,7 @@ def tp_workspace_bytes(desc: ModelDesc, batch: int) -> int:
 def tp_run_trace(ctx, requests, stream=None):
     """requests: iterable of (model_id, batch, input_dev, output_dev, arrival_ns).
 
-    Returns a list of dicts (issue_ns, done_ns, hit, status). Raises if any request failed
+    Returns a list of dicts (issue_ns, done_ns, hit, status, admit_ns). Raises if any request failed
     (after the whole trace ran)."""
     reqs = list(requests)
     arr = (tp_request * len(reqs))()
@@ -361,7 +368,8 @@ def tp_run_trace(ctx, requests, stream=None):
         arr[i] = tp_request(mid, b, _ptr(x), _ptr(y), int(t))
     res = (tp_request_result * len(reqs))()
     st = lib().tp_run_trace(ctx, arr, len(reqs), _ptr(stream), res)
-    out = [{"issue_ns": r.issue_ns, "done_ns": r.done_ns, "hit": bool(r.hit), "status": r.status} for r in res]
+    out = [{"issue_ns": r.issue_ns, "done_ns": r.done_ns, "hit": bool(r.hit), "status": r.status,
+            "admit_ns": r.admit_ns} for r in res]
     _check(lib(), st)
     return out
 
@@ -379,7 +387,8 @@ def tp_run_trace_sched(ctx, requests, deadlines_ns, policy=TP_QUEUE_SLO, max_inf
     res = (tp_request_result * len(reqs))()
     st = tp_sched_stats()
     status = lib().tp_run_trace_sched(ctx, arr, len(reqs), _ptr(stream), C.byref(cfg), dl, res, C.byref(st))
-    out = [{"issue_ns": r.issue_ns, "done_ns": r.done_ns, "hit": bool(r.hit), "status": r.status} for r in res]
+    out = [{"issue_ns": r.issue_ns, "done_ns": r.done_ns, "hit": bool(r.hit), "status": r.status,
+            "admit_ns": r.admit_ns} for r in res]
     _check(lib(), status)
     return out, st.as_dict()
 
@@ -464,12 +473,28 @@ def tph_alpha_update(alpha, last_ratio, new_ratio, scalar=2.0, threshold=0.04, L
 class HostArena:
     """tph_arena_*: the arena bookkeeping without a device."""
 
-    def __init__(self, capacity: int, align: int = 256, L=None, policy: int = TP_EVICT_LRU):
+    def __init__(self, capacity: int, align: int = 256, L=None, policy: int = TP_EVICT_LRU, partition: int = 0,
+                 consolidate: bool = False):
         self.L = L or lib()
         self.h = _P()
         _check(self.L, self.L.tph_arena_create(capacity, align, C.byref(self.h)))
         if policy != TP_EVICT_LRU:
             _check(self.L, self.L.tph_arena_set_policy(self.h, policy))
+        self.consolidate = consolidate
+        if partition:
+            self.set_partitioned(partition, consolidate)
+
+    def set_partitioned(self, partition: int, consolidate: bool = False):
+        _check(self.L, self.L.tph_arena_set_partitioned(self.h, partition, int(consolidate)))
+        self.consolidate = consolidate and partition > 0
+
+    def moves(self):
+        """The last request's consolidation moves: [(model, old offset, new offset)]."""
+        n = C.c_uint32()
+        _check(self.L, self.L.tph_arena_moves(self.h, None, None, None, 0, C.byref(n)))
+        ids, fr, to = (C.c_int32 * n.value)(), (C.c_uint64 * n.value)(), (C.c_uint64 * n.value)()
+        _check(self.L, self.L.tph_arena_moves(self.h, ids, fr, to, n.value, C.byref(n)))
+        return [(ids[i], fr[i], to[i]) for i in range(n.value)]
 
     def __del__(self):
         if getattr(self, "h", None):
@@ -491,7 +516,10 @@ class HostArena:
         hit, off, n = C.c_int32(), C.c_uint64(), C.c_uint32()
         vict = (C.c_int32 * 1024)()
         _check(self.L, self.L.tph_arena_request(self.h, mid, C.byref(hit), C.byref(off), vict, 1024, C.byref(n)))
-        return {"hit": bool(hit.value), "offset": off.value, "evicted": [vict[i] for i in range(n.value)]}
+        out = {"hit": bool(hit.value), "offset": off.value, "evicted": [vict[i] for i in range(n.value)]}
+        if self.consolidate:
+            out["moved"] = self.moves()
+        return out
 
     def evict(self, mid):
         _check(self.L, self.L.tph_arena_evict(self.h, mid))
@@ -511,7 +539,8 @@ class Runtime:
                  copy_method: int = TP_COPY_MEMCPY, gather_wgs: int = 0, flags: int = 0, throttle_us: int = 0,
                  copy_stream=None, copy_streams: int = 0, direct_max_bytes: int = DEFAULT_DIRECT,
                  plan: int = TP_PLAN_GREEDY, plan_batch: int = 0, link_gbs: float = 0.0, chunk_us: float = 0.0,
-                 evict_policy: int = TP_EVICT_LRU, heavy_ratio: float = 0.0):
+                 evict_policy: int = TP_EVICT_LRU, heavy_ratio: float = 0.0, alloc: int = TP_ALLOC_FIRST_FIT,
+                 partition_bytes: int = 0):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("libtorpor needs a HIP device")
@@ -523,7 +552,7 @@ class Runtime:
         self.copy_stream = copy_stream
         self.ctx = tp_create(self.arena, arena_bytes, self.work, self.work.numel(), copy_stream, chunk_min_bytes,
                              copy_method, gather_wgs, flags, throttle_us, copy_streams, direct_max_bytes, plan,
-                             plan_batch, link_gbs, chunk_us, evict_policy, heavy_ratio)
+                             plan_batch, link_gbs, chunk_us, evict_policy, heavy_ratio, alloc, partition_bytes)
         self.descs = {}
 
     def close(self):

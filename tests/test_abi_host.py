@@ -12,6 +12,7 @@ import paper_2306_03622_amd as tp
 import synth
 from oracle import chunks as ref_chunks
 from oracle.arena_sim import ArenaSim, NoSpace
+from oracle.partition_sim import PartitionArenaSim
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -26,7 +27,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 35, sorted(names)
+    assert len(names) == 37, sorted(names)
     L = tp.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -134,6 +135,78 @@ def _replay(trace, sizes, cap, L, policy="lru", heavy=None):
     got = ha.stats()
     assert {k: got[k] for k in sim.stats()} == sim.stats() and got["registered"] == len(sizes)
     assert got["admit_calls"] == 0       # admissions are timed by the runtime, not the bookkeeping
+
+
+@settings(max_examples=80, deadline=None)
+@given(base=st.lists(st.integers(1, 90).map(lambda x: x * 100), min_size=1, max_size=4),
+       picks=st.lists(st.integers(0, 40), min_size=2, max_size=10),
+       ops=st.lists(st.tuples(st.sampled_from(["req"] * 6 + ["evict", "reg"]), st.integers(0, 9)), max_size=100),
+       part_units=st.integers(1, 40), n_parts=st.integers(1, 6), tail=st.integers(0, 5),
+       policy=st.sampled_from(["lru", "heaviness"]), bits=st.integers(0, 1023), consolidate=st.booleans())
+def test_partitioned_arena_matches_simulator(base, picks, ops, part_units, n_parts, tail, policy, bits,
+                                             consolidate):
+    """tph_arena with two-tier partitions, with and without consolidation, against the
+    oracle's partition simulator: offsets, victims, moves and counters, with models
+    registered and unregistered on the way (a size class is common only while two
+    registered models share it)."""
+    sizes = [base[p % len(base)] if p < 30 else p * 170 for p in picks]
+    part = part_units * 256
+    cap = n_parts * part + tail * 256
+    for L in (tp.lib(), tp.host_lib()):
+        sim = PartitionArenaSim(cap, part, 256, policy, consolidate=consolidate)
+        ha = tp.HostArena(cap, 256, L=L, partition=part, consolidate=consolidate,
+                          policy=tp.TP_EVICT_HEAVINESS if policy == "heaviness" else tp.TP_EVICT_LRU)
+        live = set()
+        for i, nb in enumerate(sizes):
+            sim.register(i, nb, bool(bits >> i & 1))
+            ha.register(i, nb, bool(bits >> i & 1))
+            live.add(i)
+        for op, k in ops:
+            k %= len(sizes)
+            if op == "reg":
+                if k in live:
+                    sim.unregister(k)
+                    ha.unregister(k)
+                    live.discard(k)
+                else:
+                    sim.register(k, sizes[k], bool(bits >> k & 1))
+                    ha.register(k, sizes[k], bool(bits >> k & 1))
+                    live.add(k)
+                continue
+            if k not in live:
+                continue
+            if op == "evict":
+                sim.evict(k)
+                ha.evict(k)
+                continue
+            try:
+                want = sim.request(k)
+            except NoSpace:
+                with pytest.raises(tp.TorporError) as e:
+                    ha.request(k)
+                assert e.value.status == tp.TP_E_NOSPC
+                continue
+            assert ha.request(k) == want
+        got, want = ha.stats(), sim.stats()
+        assert {k: got[k] for k in want} == want
+
+
+def test_partitioned_arena_errors():
+    ha = tp.HostArena(1 << 20, 256, L=tp.host_lib())
+    with pytest.raises(tp.TorporError) as e:
+        ha.set_partitioned(1000)                    # not a multiple of the alignment
+    assert e.value.status == tp.TP_E_INVAL
+    ha.register(0, 5000)
+    ha.request(0)
+    with pytest.raises(tp.TorporError) as e:
+        ha.set_partitioned(4096)                    # a model is resident
+    assert e.value.status == tp.TP_E_STATE
+    ha.evict(0)
+    ha.set_partitioned(4096)
+    assert ha.request(0)["offset"] == 0             # 5120 bytes > 4096: a run of two partitions, lowest first
+    st_ = ha.stats()
+    assert st_["partitions"] == 256 and st_["partitions_free"] == 254
+    assert st_["evacuations"] == 0 and st_["bytes_moved"] == 0
 
 
 @settings(max_examples=60, deadline=None)

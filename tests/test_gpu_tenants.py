@@ -11,6 +11,7 @@ import paper_2306_03622_amd as tp
 import synth
 from oracle import forward as oracle
 from oracle.arena_sim import ArenaSim
+from oracle.partition_sim import PartitionArenaSim
 from tests.common import log, out_shape, to_device, torch_dev
 
 pytestmark = pytest.mark.gpu
@@ -116,4 +117,67 @@ def test_scheduled_replay(policy):
         y = outs[r].cpu().numpy()
         err = oracle.normwise_error(y, oracle.forward(models[k], xs_np[r])).max()
         assert np.all(np.isfinite(y)) and err <= 2e-2, (k, err)
+    rt.close()
+
+
+@pytest.mark.parametrize("alloc", [tp.TP_ALLOC_PARTITION, tp.TP_ALLOC_PARTITION_CONSOLIDATE])
+def test_partitioned_arena_trace(alloc):
+    # The scaled workload on a 1100 MiB arena of two 512 MiB partitions and a short one:
+    # MLPs take runs of both full partitions, ResNet-50 and BERT-base slots of partitions of
+    # their class; with consolidation the trace makes 11 evacuations (1171 MiB moved) where
+    # the arena would otherwise evict. Retired extents are poisoned (NaN in bf16). Checks:
+    # hit flags and counters (moves included) equal the oracle's partition simulator, and
+    # every request's output equals the same request's on an arena that holds all models.
+    torch, dev = torch_dev()
+    specs = synth.tenant_models(9)
+    models = [m for _, m in synth.build_models(specs, workers=9)]
+    trace = synth.tenant_trace(120, n_models=9)
+    cap, part = 1100 << 20, 512 << 20
+    ws = max(tp.tp_workspace_bytes(tp.ModelDesc.of(m), 1) for m in models)
+    xs, outs, ref_outs = [], [], []
+    for r in range(len(trace.model)):
+        m = models[int(trace.model[r])]
+        xs.append(to_device(synth.request_input(m, int(trace.input_seed[r]))))
+        outs.append(torch.full(out_shape(m, 1), float("nan"), dtype=torch.float32, device=dev))
+        ref_outs.append(torch.full(out_shape(m, 1), float("nan"), dtype=torch.float32, device=dev))
+
+    def replay(rt, ys):
+        ids = [rt.register(tp.ModelDesc.of(m), m.blob()) for m in models]
+        reqs = [(ids[int(trace.model[r])], 1, xs[r], ys[r], int(trace.arrival_s[r] * 1e9))
+                for r in range(len(trace.model))]
+        torch.cuda.synchronize()
+        res = rt.run_trace(reqs)
+        torch.cuda.synchronize()
+        assert all(q["status"] == 0 for q in res)
+        return ids, res
+
+    big = sum(m.total_bytes for m in models) + (64 << 20)
+    rt = tp.Runtime(big // 256 * 256, ws)
+    replay(rt, ref_outs)
+    rt.close()
+
+    rt = tp.Runtime(cap, ws, alloc=alloc, partition_bytes=part, flags=tp.TP_FLAG_POISON)
+    ids, res = replay(rt, outs)
+    consolidate = alloc == tp.TP_ALLOC_PARTITION_CONSOLIDATE
+    sim = PartitionArenaSim(cap, part, 256, consolidate=consolidate)
+    for i, m in zip(ids, models):
+        sim.register(i, m.total_bytes)
+    want_hits = [sim.request(ids[int(k)])["hit"] for k in trace.model]
+    assert [q["hit"] for q in res] == want_hits
+    got, want = rt.stats(), sim.stats()
+    for k, v in want.items():
+        assert got[k] == v, (k, got[k], v)
+    if consolidate:
+        assert got["evacuations"] == 11
+    assert all((q["admit_ns"] > 0) == (not q["hit"]) for q in res)
+    log(f"alloc {alloc}: hit rate {np.mean(want_hits):.3f}, evictions {got['evictions']}, "
+        f"evacuations {got['evacuations']}, moved {got['bytes_moved'] >> 20} MiB")
+    worst = 0.0
+    for r in range(len(outs)):
+        y, ref = outs[r].cpu().numpy(), ref_outs[r].cpu().numpy()
+        assert np.all(np.isfinite(y)), r
+        err = float(np.abs(y - ref).max() / max(np.abs(ref).max(), 1e-30))
+        worst = max(worst, err)
+        assert err <= 1e-5, (r, int(trace.model[r]), err)
+    log(f"  largest relative difference from the all-resident run: {worst:.1e}")
     rt.close()
