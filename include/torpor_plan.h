@@ -91,12 +91,14 @@ TP_API tp_status tph_arena_set_heavy(struct tph_arena* a, int32_t model_id, int3
  * (torpor.h) with partitions of that size (a multiple of the alignment), with consolidation
  * (TP_ALLOC_PARTITION_CONSOLIDATE) if `consolidate`; 0 back to first fit. TP_E_STATE while
  * any model is resident, TP_E_INVAL for a size that is not a multiple. tph_arena_request
- * reports no moves; tph_arena_moves gives the last request's. */
+ * reports the victims alone; tph_arena_steps gives the last request's victims and moves in
+ * the order made. */
 TP_API tp_status tph_arena_set_partitioned(struct tph_arena* a, uint64_t partition_bytes, int32_t consolidate);
-/* The consolidation moves of the last tph_arena_request: up to `cap` (model, old offset, new
- * offset) triples in the order made; *n receives their count. */
-TP_API tp_status tph_arena_moves(struct tph_arena* a, int32_t* model_id, uint64_t* from, uint64_t* to, uint32_t cap,
-                                 uint32_t* n);
+/* The steps of the last tph_arena_request in the order made: up to `cap` entries of a model,
+ * whether it was moved (1; consolidation) or evicted (0), its old offset and (moves) its new
+ * one; *n receives the count. The device replays them in this order. */
+TP_API tp_status tph_arena_steps(struct tph_arena* a, int32_t* model_id, int32_t* moved, uint64_t* from, uint64_t* to,
+                                 uint32_t cap, uint32_t* n);
 TP_API tp_status tph_arena_stats(struct tph_arena* a, tp_arena_stats_t* out);
 
 #ifdef __cplusplus

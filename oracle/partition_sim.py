@@ -46,9 +46,9 @@ Readings (the paper gives neither sizes nor tie rules):
   occupants can all be placed, in increasing offset order and by the rules above, in other
   partitions of the same kind (slots of the same class, buddy blocks) without dedicating a
   free partition. It becomes free, and placement is tried again; only when no partition
-  can be evacuated is a victim evicted. Every move (model, old offset, new offset) is
-  reported with the request, in the order made; the device copies them before the
-  requester's weights land.
+  can be evacuated is a victim evicted. The request reports its evictions and moves
+  (model, old offset, new offset) interleaved in the order made; the device replays them
+  in that order before the requester's weights land.
 """
 from __future__ import annotations
 
@@ -254,16 +254,16 @@ class PartitionArenaSim(ArenaSim):
             self.hits += 1
             out = {"hit": True, "offset": self.where[mid], "evicted": []}
             if self.consolidate:
-                out["moved"] = []
+                out["steps"] = []
             return out
         self.misses += 1
-        evicted, moved = [], []
+        evicted, steps = [], []
         off = self.try_place(mid)
         while off is None:
             if self.consolidate:
                 mv = self.evacuate()
                 if mv is not None:
-                    moved += mv
+                    steps += [("move",) + m for m in mv]
                     off = self.try_place(mid)
                     continue
             victim = self.victim()
@@ -272,12 +272,13 @@ class PartitionArenaSim(ArenaSim):
             self.evict(victim)
             self.evictions += 1
             evicted.append(victim)
+            steps.append(("evict", victim))
             off = self.try_place(mid)
         self.where[mid] = off
         self.bytes_swapped += need
         out = {"hit": False, "offset": off, "evicted": evicted}
         if self.consolidate:
-            out["moved"] = moved
+            out["steps"] = steps
         return out
 
     def evict(self, mid: int) -> None:

@@ -95,6 +95,7 @@ Arena::Decision Arena::request(int32_t id) {
           models_.at(x.id).offset = x.to;
           moved_ += models_.at(x.id).bytes;
           d.moves.push_back(x);
+          d.steps.push_back({true, x.id, x.from, x.to});
         }
         std::sort(by_addr_.begin(), by_addr_.end(),
                   [&](int32_t a, int32_t b) { return models_.at(a).offset < models_.at(b).offset; });
@@ -108,6 +109,7 @@ Arena::Decision Arena::request(int32_t id) {
       return d;
     }
     if (capacity_ - used() >= me.bytes) ++frag_evictions_;
+    d.steps.push_back({false, victim, models_.at(victim).offset, 0});
     evict(victim);
     ++evictions_;
     d.victims.push_back(victim);

@@ -27,7 +27,15 @@ class Arena {
     bool placed = true;             // false: the model cannot be placed even in an empty arena
     uint64_t offset = 0;
     std::vector<int32_t> victims;   // evicted by this request, in eviction order
-    std::vector<Partitions::Move> moves;   // consolidation moves, in the order made (before victims')
+    std::vector<Partitions::Move> moves;   // consolidation moves, in the order made
+    // victims and moves interleaved in the order made (a move may fill a victim's range, a
+    // victim may be a model moved earlier in the same request): the device replays this
+    struct Step {
+      bool move;
+      int32_t id;
+      uint64_t from, to;      // move: old and new offset
+    };
+    std::vector<Step> steps;
   };
 
   tp_status add_model(int32_t id, uint64_t bytes, bool heavy = false);

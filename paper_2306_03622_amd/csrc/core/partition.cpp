@@ -134,12 +134,33 @@ bool Partitions::evacuate(const std::function<uint64_t(int32_t)>& bytes, const s
   for (const auto& cand : order) {
     const int i = cand.second;
     std::vector<std::pair<uint64_t, int32_t>> occ;   // (offset, model) in offset order
+    uint64_t need = 0;
+    bool irregular = true;                           // every occupant's class irregular now
     for (const auto& w : where_) {
       if (w.second.kind == kRun || (int)w.second.first != i) continue;
       const Part& p = parts_[i];
       occ.push_back({p.start + (w.second.kind == kSlab ? w.second.pos * p.cls : w.second.pos), w.first});
+      need += bytes(w.first);
+      irregular = irregular && !common(w.first);
     }
     std::sort(occ.begin(), occ.end());
+    // cheap rejections that never change the outcome: a slot partition whose class is still
+    // common needs as many free slots of its class elsewhere as it has occupants (exact); a
+    // buddy partition of irregular occupants needs at least their bytes free in other buddy
+    // partitions (occupants whose class has become common go to slots instead)
+    const Part& pi = parts_[i];
+    if (pi.kind == kSlab && common(occ.front().second)) {
+      uint64_t free_slots = 0;
+      for (int k = 0; k < (int)parts_.size(); ++k)
+        if (k != i && parts_[k].kind == kSlab && parts_[k].cls == pi.cls)
+          free_slots += parts_[k].size / pi.cls - parts_[k].slots.size();
+      if (free_slots < occ.size()) continue;
+    } else if (pi.kind == kBuddy && irregular) {
+      uint64_t free_bytes = 0;
+      for (int k = 0; k < (int)parts_.size(); ++k)
+        if (k != i && parts_[k].kind == kBuddy) free_bytes += parts_[k].size - parts_[k].used_bytes;
+      if (free_bytes < need) continue;
+    }
     const std::vector<Part> saved_parts = parts_;
     const std::unordered_map<int32_t, Where> saved_where = where_;
     std::vector<Move> mv;

@@ -11,7 +11,7 @@ using namespace tp;
 
 struct tph_arena {
   Arena a;
-  std::vector<Partitions::Move> last_moves;
+  std::vector<Arena::Decision::Step> last_steps;
   tph_arena(uint64_t c, uint64_t al) : a(c, al) {}
 };
 
@@ -161,11 +161,11 @@ tp_status tph_arena_unregister(tph_arena* a, int32_t id) {
 tp_status tph_arena_request(tph_arena* a, int32_t id, int32_t* hit, uint64_t* offset, int32_t* victims,
                             uint32_t cap, uint32_t* n_victims) {
   if (!a) return fail(TP_E_INVAL, "NULL arena");
-  a->last_moves.clear();
+  a->last_steps.clear();
   if (!a->a.known(id)) return fail(TP_E_NOENT, "unknown model id");
   if (!a->a.fits_at_all(id)) return fail(TP_E_NOSPC, "model larger than the arena");
   Arena::Decision d = a->a.request(id);
-  a->last_moves = d.moves;
+  a->last_steps = d.steps;
   if (!d.placed) return fail(TP_E_NOSPC, "model cannot be placed in the arena");
   if (hit) *hit = d.hit;
   if (offset) *offset = d.offset;
@@ -195,13 +195,16 @@ tp_status tph_arena_set_heavy(tph_arena* a, int32_t id, int32_t heavy) {
   return ok();
 }
 
-tp_status tph_arena_moves(tph_arena* a, int32_t* model_id, uint64_t* from, uint64_t* to, uint32_t cap, uint32_t* n) {
+tp_status tph_arena_steps(tph_arena* a, int32_t* model_id, int32_t* moved, uint64_t* from, uint64_t* to, uint32_t cap,
+                          uint32_t* n) {
   if (!a || !n) return fail(TP_E_INVAL, "NULL argument");
-  *n = (uint32_t)a->last_moves.size();
-  for (uint32_t i = 0; i < a->last_moves.size() && i < cap; ++i) {
-    if (model_id) model_id[i] = a->last_moves[i].id;
-    if (from) from[i] = a->last_moves[i].from;
-    if (to) to[i] = a->last_moves[i].to;
+  *n = (uint32_t)a->last_steps.size();
+  for (uint32_t i = 0; i < a->last_steps.size() && i < cap; ++i) {
+    const auto& st = a->last_steps[i];
+    if (model_id) model_id[i] = st.id;
+    if (moved) moved[i] = st.move;
+    if (from) from[i] = st.from;
+    if (to) to[i] = st.move ? st.to : 0;
   }
   return ok();
 }

@@ -176,9 +176,10 @@ tp_status move_extent(tp_ctx* c, Model* x, uint64_t from, uint64_t to) {
   return retire(c, x->id, from, len);
 }
 
-// One request's admission: a hit, or consolidation moves made and victims invalidated and
-// their readers waited for on the primary copy stream; the chunk copies are then issued by
-// the request's Waiter. On failure the model is left non-resident.
+// One request's admission: a hit, or consolidation moves made and victims invalidated, in
+// the arena's order, with their readers waited for on the primary copy stream; the chunk
+// copies are then issued by the request's Waiter. On failure the model is left
+// non-resident.
 tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   const auto t0 = std::chrono::steady_clock::now();
   Arena::Decision d = c->policy->request(m->id);
@@ -199,10 +200,10 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   } timer{c, t0};
   m->bg_pending = false;         // a new swap supersedes an earlier one
   tp_status s = TP_OK;
-  for (const auto& mv : d.moves)
-    if (s == TP_OK) s = move_extent(c, find(c, mv.id), mv.from, mv.to);
-  for (int32_t v : d.victims)
-    if (s == TP_OK) s = retire(c, v, c->policy->offset(v), c->policy->bytes(v));
+  for (const auto& st : d.steps) {         // in the order the arena made them
+    if (s != TP_OK) break;
+    s = st.move ? move_extent(c, find(c, st.id), st.from, st.to) : retire(c, st.id, st.from, c->policy->bytes(st.id));
+  }
   if (s == TP_OK) s = claim(c, d.offset, m->spec.host_bytes);
   if (s != TP_OK) {
     const std::string msg = last_error();

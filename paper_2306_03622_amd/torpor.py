@@ -162,8 +162,8 @@ _SIGS = {
     "tph_arena_set_policy": [_P, C.c_int32],
     "tph_arena_set_heavy": [_P, C.c_int32, C.c_int32],
     "tph_arena_set_partitioned": [_P, C.c_uint64, C.c_int32],
-    "tph_arena_moves": [_P, C.POINTER(C.c_int32), C.POINTER(C.c_uint64), C.POINTER(C.c_uint64), C.c_uint32,
-                        C.POINTER(C.c_uint32)],
+    "tph_arena_steps": [_P, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_uint64),
+                        C.POINTER(C.c_uint64), C.c_uint32, C.POINTER(C.c_uint32)],
     "tph_arena_stats": [_P, C.POINTER(tp_arena_stats_t)],
 }
 HOST_ONLY = [n for n in _SIGS if n.startswith("tph_")]
@@ -488,13 +488,15 @@ class HostArena:
         _check(self.L, self.L.tph_arena_set_partitioned(self.h, partition, int(consolidate)))
         self.consolidate = consolidate and partition > 0
 
-    def moves(self):
-        """The last request's consolidation moves: [(model, old offset, new offset)]."""
+    def steps(self):
+        """The last request's victims and consolidation moves in the order made:
+        [("evict", model)] and [("move", model, old offset, new offset)] entries."""
         n = C.c_uint32()
-        _check(self.L, self.L.tph_arena_moves(self.h, None, None, None, 0, C.byref(n)))
-        ids, fr, to = (C.c_int32 * n.value)(), (C.c_uint64 * n.value)(), (C.c_uint64 * n.value)()
-        _check(self.L, self.L.tph_arena_moves(self.h, ids, fr, to, n.value, C.byref(n)))
-        return [(ids[i], fr[i], to[i]) for i in range(n.value)]
+        _check(self.L, self.L.tph_arena_steps(self.h, None, None, None, None, 0, C.byref(n)))
+        ids, mv = (C.c_int32 * n.value)(), (C.c_int32 * n.value)()
+        fr, to = (C.c_uint64 * n.value)(), (C.c_uint64 * n.value)()
+        _check(self.L, self.L.tph_arena_steps(self.h, ids, mv, fr, to, n.value, C.byref(n)))
+        return [("move", ids[i], fr[i], to[i]) if mv[i] else ("evict", ids[i]) for i in range(n.value)]
 
     def __del__(self):
         if getattr(self, "h", None):
@@ -518,7 +520,7 @@ class HostArena:
         _check(self.L, self.L.tph_arena_request(self.h, mid, C.byref(hit), C.byref(off), vict, 1024, C.byref(n)))
         out = {"hit": bool(hit.value), "offset": off.value, "evicted": [vict[i] for i in range(n.value)]}
         if self.consolidate:
-            out["moved"] = self.moves()
+            out["steps"] = self.steps()
         return out
 
     def evict(self, mid):

@@ -191,6 +191,59 @@ def test_partitioned_arena_matches_simulator(base, picks, ops, part_units, n_par
         assert {k: got[k] for k in want} == want
 
 
+def test_partitioned_arena_seeded_sweep():
+    """3000 seeded traces against the oracle: registration churn makes size classes switch
+    between common and irregular while their models are resident (so evacuated models may
+    change tier), partitions of 1 to 64 units with and without a short tail, both eviction
+    policies, consolidation on half of them; every decision, move order and counter equal."""
+    import random
+    L = tp.host_lib()
+    evacuations = 0
+    for seed in range(3000):
+        r = random.Random(seed)
+        part = 256 * r.choice([1, 2, 3, 4, 8, 16, 12, 40, 64])
+        cap = part * r.randint(1, 6) + 256 * r.choice([0, 0, 1, 3, 7])
+        n = r.randint(2, 10)
+        base = [r.choice([1, 2, 3, 5, 8, 13, 20, 40, 70]) * 100 for _ in range(4)]
+        sizes = [r.choice(base) if r.random() < 0.6 else r.randint(1, 80) * 100 for _ in range(n)]
+        policy = r.choice(["lru", "heaviness"])
+        consolidate = r.random() < 0.5
+        heavy = [r.random() < 0.3 for _ in range(n)]
+        sim = PartitionArenaSim(cap, part, 256, policy, consolidate=consolidate)
+        ha = tp.HostArena(cap, 256, L=L, partition=part, consolidate=consolidate,
+                          policy=tp.TP_EVICT_HEAVINESS if policy == "heaviness" else tp.TP_EVICT_LRU)
+        live = set(range(n))
+        for i in range(n):
+            sim.register(i, sizes[i], heavy[i])
+            ha.register(i, sizes[i], heavy[i])
+        for _ in range(120):
+            op, k = r.choice(["req"] * 6 + ["evict", "reg"]), r.randrange(n)
+            if op == "reg":
+                if k in live:
+                    sim.unregister(k)
+                    ha.unregister(k)
+                    live.discard(k)
+                else:
+                    sim.register(k, sizes[k], heavy[k])
+                    ha.register(k, sizes[k], heavy[k])
+                    live.add(k)
+            elif k in live and op == "evict":
+                sim.evict(k)
+                ha.evict(k)
+            elif k in live:
+                try:
+                    want = sim.request(k)
+                except NoSpace:
+                    with pytest.raises(tp.TorporError):
+                        ha.request(k)
+                    continue
+                assert ha.request(k) == want, seed
+        got, want = ha.stats(), sim.stats()
+        assert {k: got[k] for k in want} == want, seed
+        evacuations += got["evacuations"]
+    assert evacuations > 100
+
+
 def test_partitioned_arena_errors():
     ha = tp.HostArena(1 << 20, 256, L=tp.host_lib())
     with pytest.raises(tp.TorporError) as e:

@@ -177,13 +177,13 @@ def test_consolidation_worked_example():
     first) instead of evicting anything."""
     pa = _consolidation_setup(True)
     r = pa.request(9)
-    assert r == {"hit": False, "offset": 0, "evicted": [], "moved": [(3, 2048 + 768, 4096)]}
+    assert r == {"hit": False, "offset": 0, "evicted": [], "steps": [("move", 3, 2048 + 768, 4096)]}
     assert pa.where[3] == 4096 and pa.evacuations == 1 and pa.bytes_moved == 768
     assert pa.evictions == 0 and pa.frag_evictions == 0
     # now partition 2 is full (models 3, 1) and nothing is free: evacuating it fails (no
     # other partition of the class), the state is restored, and the LRU model (1) goes
     r = pa.request(0)
-    assert r == {"hit": False, "offset": 4096 + 768, "evicted": [1], "moved": []}
+    assert r == {"hit": False, "offset": 4096 + 768, "evicted": [1], "steps": [("evict", 1)]}
     assert pa.where[3] == 4096 and pa.parts[2].kind == "slab" and pa.parts[2].slots == {0: 3, 1: 0}
     assert pa.frag_evictions == 1             # 6144 - (768 + 768 + 3072) = 1536 free before
     # the same start without consolidation: LRU evicts model 1 (partition 2 frees, but 0 and
@@ -191,6 +191,25 @@ def test_consolidation_worked_example():
     pb = _consolidation_setup(False)
     r = pb.request(9)
     assert r == {"hit": False, "offset": 0, "evicted": [1, 3]} and pb.frag_evictions == 2
+
+
+def test_consolidation_move_into_a_victims_slot():
+    """Derived by hand: the order of evictions and moves matters to the device (a move may
+    fill the slot a victim just left, whose readers must finish first), so the request
+    reports them interleaved. Three partitions of 2048, 768-byte models (two slots per
+    partition): partition 2 holds models 0 and 1, partition 1 model 2, partition 0 is free.
+    A 3072-byte model needs a run of two free partitions. Partition 1 cannot be evacuated
+    (partition 2 is full) nor partition 2 (one free slot for two models), so LRU evicts
+    model 0; now partition 1's model moves into the slot model 0 left, partition 1 is free,
+    and the run takes partitions 0 and 1."""
+    pa = PartitionArenaSim(3 * 2048, 2048, A, consolidate=True)
+    for i in range(3):
+        pa.register(i, 768)
+    pa.register(9, 3072)
+    assert [pa.request(i)["offset"] for i in range(3)] == [4096, 4096 + 768, 2048]
+    r = pa.request(9)
+    assert r == {"hit": False, "offset": 0, "evicted": [0], "steps": [("evict", 0), ("move", 2, 2048, 4096)]}
+    assert pa.where == {1: 4096 + 768, 2: 4096, 9: 0}
 
 
 @settings(max_examples=60, deadline=None)
