@@ -1,6 +1,8 @@
 // Row LayerNorm and the fused embedding gather + LayerNorm. One wave per row, each lane
 // holding D/64 elements in registers; mean and variance (two passes over the registers,
-// population variance) use butterfly wave reductions in fp32.
+// population variance) use butterfly wave reductions in fp32. When D/64 is a multiple of 4
+// a lane holds a contiguous run of the row (16-byte fp32 and 8-byte bf16 accesses);
+// otherwise element lane + 64 i.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -36,6 +38,44 @@ __device__ __forceinline__ void normalize(float (&v)[PER], int D, const uint16_t
   }
 }
 
+// The same for a row held as PER contiguous values per lane (element c = PER lane + i).
+template <int PER>
+__device__ __forceinline__ void normalize_runs(float (&v)[PER], int D, const uint16_t* g, const uint16_t* b,
+                                               float eps, int lane, void* out, size_t row_off, int out_f32) {
+  static_assert(PER % 4 == 0, "runs of 4");
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) s += v[i];
+  const float mean = wave_sum(s) / (float)D;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const float d = v[i] - mean;
+    q = fmaf(d, d, q);
+  }
+  const float var = wave_sum(q) / (float)D;
+  const float rstd = 1.f / sqrtf(var + eps);
+  const int c0 = lane * PER;
+#pragma unroll
+  for (int i = 0; i < PER; i += 4) {
+    const uint2 gg = *reinterpret_cast<const uint2*>(g + c0 + i);
+    const uint2 bb = *reinterpret_cast<const uint2*>(b + c0 + i);
+    float y[4];
+    y[0] = (v[i] - mean) * rstd * bf2f(gg.x & 0xffff) + bf2f(bb.x & 0xffff);
+    y[1] = (v[i + 1] - mean) * rstd * bf2f(gg.x >> 16) + bf2f(bb.x >> 16);
+    y[2] = (v[i + 2] - mean) * rstd * bf2f(gg.y & 0xffff) + bf2f(bb.y & 0xffff);
+    y[3] = (v[i + 3] - mean) * rstd * bf2f(gg.y >> 16) + bf2f(bb.y >> 16);
+    if (out_f32) {
+      *reinterpret_cast<float4*>(static_cast<float*>(out) + row_off + c0 + i) = make_float4(y[0], y[1], y[2], y[3]);
+    } else {
+      uint2 o;
+      o.x = (uint32_t)f2bf(y[0]) | ((uint32_t)f2bf(y[1]) << 16);
+      o.y = (uint32_t)f2bf(y[2]) | ((uint32_t)f2bf(y[3]) << 16);
+      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + row_off + c0 + i) = o;
+    }
+  }
+}
+
 template <int PER>
 __global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ x, int M,
                                                    const uint16_t* __restrict__ g, const uint16_t* __restrict__ b,
@@ -46,9 +86,18 @@ __global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ x, 
   if (row >= M) return;
   float v[PER];
   const float* xr = x + (size_t)row * D;
+  if constexpr (PER % 4 == 0) {
 #pragma unroll
-  for (int i = 0; i < PER; ++i) v[i] = xr[lane + 64 * i];
-  normalize<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, out_f32);
+    for (int i = 0; i < PER; i += 4) {
+      const float4 t = *reinterpret_cast<const float4*>(xr + lane * PER + i);
+      v[i] = t.x; v[i + 1] = t.y; v[i + 2] = t.z; v[i + 3] = t.w;
+    }
+    normalize_runs<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, out_f32);
+  } else {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) v[i] = xr[lane + 64 * i];
+    normalize<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, out_f32);
+  }
 }
 
 template <int PER>
@@ -64,12 +113,27 @@ __global__ __launch_bounds__(256) void k_embed_ln(const int32_t* __restrict__ id
   id = id < 0 ? 0 : (id >= vocab ? vocab - 1 : id);
   const int s = row % S;
   float v[PER];
+  if constexpr (PER % 4 == 0) {
 #pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = lane + 64 * i;
-    v[i] = bf2f(tok[(size_t)id * D + c]) + bf2f(pos[(size_t)s * D + c]) + bf2f(type[c]);
+    for (int i = 0; i < PER; i += 4) {
+      const int c = lane * PER + i;
+      const uint2 t = *reinterpret_cast<const uint2*>(tok + (size_t)id * D + c);
+      const uint2 p = *reinterpret_cast<const uint2*>(pos + (size_t)s * D + c);
+      const uint2 y = *reinterpret_cast<const uint2*>(type + c);
+      v[i] = bf2f(t.x & 0xffff) + bf2f(p.x & 0xffff) + bf2f(y.x & 0xffff);
+      v[i + 1] = bf2f(t.x >> 16) + bf2f(p.x >> 16) + bf2f(y.x >> 16);
+      v[i + 2] = bf2f(t.y & 0xffff) + bf2f(p.y & 0xffff) + bf2f(y.y & 0xffff);
+      v[i + 3] = bf2f(t.y >> 16) + bf2f(p.y >> 16) + bf2f(y.y >> 16);
+    }
+    normalize_runs<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, 0);
+  } else {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = lane + 64 * i;
+      v[i] = bf2f(tok[(size_t)id * D + c]) + bf2f(pos[(size_t)s * D + c]) + bf2f(type[c]);
+    }
+    normalize<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, 0);
   }
-  normalize<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, 0);
 }
 
 template <int PER>
