@@ -136,9 +136,11 @@ hipError_t run_bert(ExecCtx& x) {
     e2.res = h;
     e2.out = pre;
     e2.out_f32 = 1;
+    e2.ln_g = x.t<uint16_t>(l, TP_ROLE_LN1_G);
+    e2.ln_b = x.t<uint16_t>(l, TP_ROLE_LN1_B);
+    e2.ln_eps = eps;
+    e2.ln_out = h;
     TP_TRY(k::linear_bf16(att, M, d, x.t<uint16_t>(l, TP_ROLE_O_W), d, e2, x.split, x.stream));
-    TP_TRY(k::layernorm(pre, M, d, x.t<uint16_t>(l, TP_ROLE_LN1_G), x.t<uint16_t>(l, TP_ROLE_LN1_B), eps, h, 0,
-                        x.stream));
     k::Epilogue e3;
     e3.bias = x.t<uint16_t>(l, TP_ROLE_FFN1_B);
     e3.act = k::ACT_GELU;
@@ -149,10 +151,13 @@ hipError_t run_bert(ExecCtx& x) {
     e4.res = h;
     e4.out = pre;
     e4.out_f32 = 1;
-    TP_TRY(k::linear_bf16(ff, M, F, x.t<uint16_t>(l, TP_ROLE_FFN2_W), d, e4, x.split, x.stream));
     const bool last = l == L;
-    TP_TRY(k::layernorm(pre, M, d, x.t<uint16_t>(l, TP_ROLE_LN2_G), x.t<uint16_t>(l, TP_ROLE_LN2_B), eps,
-                        last ? x.out : static_cast<void*>(h), last ? 1 : 0, x.stream));
+    e4.ln_g = x.t<uint16_t>(l, TP_ROLE_LN2_G);
+    e4.ln_b = x.t<uint16_t>(l, TP_ROLE_LN2_B);
+    e4.ln_eps = eps;
+    e4.ln_out = last ? x.out : static_cast<void*>(h);
+    e4.ln_out_f32 = last ? 1 : 0;
+    TP_TRY(k::linear_bf16(ff, M, F, x.t<uint16_t>(l, TP_ROLE_FFN2_W), d, e4, x.split, x.stream));
   }
   return hipSuccess;
 }

@@ -66,6 +66,11 @@ __device__ __forceinline__ void store_row4(const GemmArgs& a, int m, int n0, f32
   }
 }
 
+// The reduction of a split contraction fused with the row LayerNorm of its result
+// (norm.hip); split_reduce_ln_fits tells whether it applies to width N.
+bool split_reduce_ln_fits(int N);
+hipError_t split_reduce_ln(const GemmArgs& a, hipStream_t s);
+
 // M <= 32 rows: the skinny kernel (gemv_bf16.hip)
 hipError_t launch_skinny(const GemmArgs& a, hipStream_t s);
 

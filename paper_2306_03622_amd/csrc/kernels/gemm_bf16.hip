@@ -523,12 +523,22 @@ __global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
   store_row4(a, m, n0, sum);
 }
 
-hipError_t reduce_splits(const GemmArgs& a, hipStream_t s) {
+// After the contraction: the reduction of a k split (fused with the epilogue's row
+// LayerNorm when the width allows), then the LayerNorm of an fp32 result if one is asked for
+// and not yet done.
+hipError_t finish(const GemmArgs& a, hipStream_t s) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   if (a.splits > 1) {
+    if (a.ep.ln_g && split_reduce_ln_fits(a.N)) return split_reduce_ln(a, s);
     const long groups = (long)a.M * ((a.N + 3) / 4);
     hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  return hipGetLastError();
+  if (a.ep.ln_g)
+    return layernorm(static_cast<const float*>(a.ep.out), a.M, a.N, a.ep.ln_g, a.ep.ln_b, a.ep.ln_eps, a.ep.ln_out,
+                     a.ep.ln_out_f32, s);
+  return hipSuccess;
 }
 
 template <int BN, int BM, int BK, int MODE, bool WVEC, int D>
@@ -553,11 +563,11 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   if constexpr (MODE == X_ROWS) {
     if (a.ep.w_packed) {
       hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, true, D>), grid, dim3(256), 0, s, a);
-      return reduce_splits(a, s);
+      return finish(a, s);
     }
   }
   hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, false, D>), grid, dim3(256), 0, s, a);
-  return reduce_splits(a, s);
+  return finish(a, s);
 }
 
 template <int MODE, bool WVEC>
@@ -571,7 +581,10 @@ hipError_t pick_tiled(const GemmArgs& a, const Split& sp, hipStream_t s) {
   return launch_tiled<64, 64, 64, MODE, WVEC, 2>(a, sp, s);
 }
 
-bool ep_ok(const Epilogue& ep) { return ep.out != nullptr && ep.act >= 0 && ep.act <= 2; }
+bool ep_ok(const Epilogue& ep) {
+  if (ep.ln_g && (!ep.ln_b || !ep.ln_out || !ep.out_f32)) return false;
+  return ep.out != nullptr && ep.act >= 0 && ep.act <= 2;
+}
 
 }  // namespace
 
@@ -581,14 +594,18 @@ hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N
   if (ep.w_packed && ((N & 15) || (K & 127))) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = x; a.w = w; a.M = M; a.N = N; a.K = K; a.ep = ep;
-  if (M <= 32) return launch_skinny(a, s);
+  if (M <= 32) {
+    a.splits = 1;
+    hipError_t e = launch_skinny(a, s);
+    return e == hipSuccess ? finish(a, s) : e;
+  }
   return pick_tiled<X_ROWS, true>(a, sp, s);
 }
 
 hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16_t* w, int O, int KH, int KW,
                      int stride, int pad, const Epilogue& ep, const Split& sp, hipStream_t s) {
   if (!x || !w || B < 1 || H < 1 || W < 1 || C < 1 || O < 1 || KH < 1 || KW < 1 || stride < 1 || pad < 0 ||
-      !ep_ok(ep))
+      !ep_ok(ep) || ep.ln_g)
     return hipErrorInvalidValue;
   const int Ho = (H + 2 * pad - KH) / stride + 1, Wo = (W + 2 * pad - KW) / stride + 1;
   if (Ho < 1 || Wo < 1) return hipErrorInvalidValue;

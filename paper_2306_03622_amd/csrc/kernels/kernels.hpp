@@ -20,6 +20,14 @@ struct Epilogue {
   void* out = nullptr;
   int out_f32 = 0;                  // out dtype: 0 bf16, 1 fp32
   int w_packed = 0;                 // weights in 16 x 128 blocks (N % 16 == 0, K % 128 == 0)
+  // optional row LayerNorm of the (fp32) result, written to ln_out (bf16 or fp32): then
+  // `out` must be fp32 [M][N] scratch, which a contraction split over k does not touch (the
+  // reduction normalises in registers when 256 <= N <= 1024 and N % 256 == 0)
+  const uint16_t* ln_g = nullptr;
+  const uint16_t* ln_b = nullptr;
+  float ln_eps = 0.f;
+  void* ln_out = nullptr;
+  int ln_out_f32 = 0;
 };
 
 // Scratch for splitting a contraction over k into fp32 partials (null disables splitting).

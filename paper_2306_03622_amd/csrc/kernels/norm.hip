@@ -4,6 +4,7 @@
 // a lane holds a contiguous run of the row (16-byte fp32 and 8-byte bf16 accesses);
 // otherwise element lane + 64 i.
 #include "common.hpp"
+#include "gemm_args.hpp"
 #include "kernels.hpp"
 
 namespace tp {
@@ -136,6 +137,51 @@ __global__ __launch_bounds__(256) void k_embed_ln(const int32_t* __restrict__ id
   }
 }
 
+// The reduction of a contraction split over k, fused with the row LayerNorm of its result:
+// one wave per row sums the fp32 partials in split order, applies the contraction's
+// epilogue arithmetic (bias, residual, activation: the same operations in the same order
+// as the plain reduction) and normalises the row in registers. Only the LayerNorm output is
+// written.
+template <int PER>
+__global__ __launch_bounds__(256) void k_split_reduce_ln(GemmArgs a) {
+  constexpr int D = 64 * PER;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.M) return;
+  const Epilogue& ep = a.ep;
+  const int c0 = lane * PER;
+  const size_t base = (size_t)row * D + c0, plane = (size_t)a.M * D;
+  float v[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) v[i] = 0.f;
+  for (int z = 0; z < a.splits; ++z) {
+#pragma unroll
+    for (int i = 0; i < PER; i += 4) {
+      const float4 t = *reinterpret_cast<const float4*>(a.partials + z * plane + base + i);
+      v[i] += t.x; v[i + 1] += t.y; v[i + 2] += t.z; v[i + 3] += t.w;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < PER; i += 4) {
+    if (ep.bias) {
+      const uint2 bb = *reinterpret_cast<const uint2*>(ep.bias + c0 + i);
+      v[i] += bf2f(bb.x & 0xffff); v[i + 1] += bf2f(bb.x >> 16); v[i + 2] += bf2f(bb.y & 0xffff); v[i + 3] += bf2f(bb.y >> 16);
+    }
+    if (ep.res) {
+      if (ep.res_f32) {
+        const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(ep.res) + base + i);
+        v[i] += r.x; v[i + 1] += r.y; v[i + 2] += r.z; v[i + 3] += r.w;
+      } else {
+        const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(ep.res) + base + i);
+        v[i] += bf2f(r.x & 0xffff); v[i + 1] += bf2f(r.x >> 16); v[i + 2] += bf2f(r.y & 0xffff); v[i + 3] += bf2f(r.y >> 16);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[i + e] = act_apply(v[i + e], ep.act);
+  }
+  normalize_runs<PER>(v, D, ep.ln_g, ep.ln_b, ep.ln_eps, lane, ep.ln_out, (size_t)row * D, ep.ln_out_f32);
+}
+
 template <int PER>
 hipError_t launch_ln(const float* x, int M, const uint16_t* g, const uint16_t* b, float eps, void* out, int out_f32,
                      hipStream_t s) {
@@ -153,6 +199,20 @@ hipError_t launch_embed(const int32_t* ids, int M, int S, int vocab, const uint1
 }
 
 }  // namespace
+
+bool split_reduce_ln_fits(int N) { return N >= 256 && N <= 64 * kMaxPer && N % 256 == 0; }
+
+hipError_t split_reduce_ln(const GemmArgs& a, hipStream_t s) {
+  if (!split_reduce_ln_fits(a.N) || !a.ep.ln_g || !a.ep.ln_b || !a.ep.ln_out || a.splits < 1) return hipErrorInvalidValue;
+  const dim3 grid((a.M + 3) / 4), block(256);
+  switch (a.N / 64) {
+    case 4: hipLaunchKernelGGL(k_split_reduce_ln<4>, grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL(k_split_reduce_ln<8>, grid, block, 0, s, a); break;
+    case 12: hipLaunchKernelGGL(k_split_reduce_ln<12>, grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL(k_split_reduce_ln<16>, grid, block, 0, s, a); break;
+  }
+  return hipGetLastError();
+}
 
 hipError_t layernorm(const float* x, int M, int D, const uint16_t* g, const uint16_t* b, float eps, void* out,
                      int out_f32, hipStream_t s) {
