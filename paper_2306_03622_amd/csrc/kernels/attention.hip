@@ -28,12 +28,31 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   const int D = H * 64, ld = 3 * D;
   const uint16_t* base = qkv + (size_t)b * S * ld;
 
-  for (int v = tid; v < S * 8; v += 256) {
-    const int key = v >> 3, d8 = (v & 7) << 3;
-    const uint16_t* row = base + (size_t)key * ld + h * 64 + d8;
-    *reinterpret_cast<uint4*>(&Ks[key * LDK + d8]) = *reinterpret_cast<const uint4*>(row + D);
-    const uint4 vv = *reinterpret_cast<const uint4*>(row + 2 * D);
-    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+  // this wave's queries first (independent of the staging); a wave past the sequence end
+  // loads row 0 and does nothing with it
+  const int q0 = blockIdx.x * 64 + wave * 16;
+  const bool active = q0 < S;
+  const uint16_t* qrow = base + (size_t)(active ? q0 + r : 0) * ld + h * 64 + (g << 3);
+  const uint4 qf0 = *reinterpret_cast<const uint4*>(qrow);
+  const uint4 qf1 = *reinterpret_cast<const uint4*>(qrow + 32);
+
+  // K and V of the head: every load of this thread issued before the first LDS store, so
+  // the round trips overlap (key = 32 i + tid / 8, 8 dims at (tid % 8) * 8)
+  constexpr int NV = SMAX * 8 / 256;
+  uint4 kv[NV], vv[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int key = (i * 256 + tid) >> 3, d8 = (tid & 7) << 3;
+    const uint16_t* row = base + (size_t)(key < S ? key : 0) * ld + h * 64 + d8;
+    kv[i] = *reinterpret_cast<const uint4*>(row + D);
+    vv[i] = *reinterpret_cast<const uint4*>(row + 2 * D);
+  }
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int key = (i * 256 + tid) >> 3, d8 = (tid & 7) << 3;
+    if (key >= S) continue;
+    *reinterpret_cast<uint4*>(&Ks[key * LDK + d8]) = kv[i];
+    const uint32_t w[4] = {vv[i].x, vv[i].y, vv[i].z, vv[i].w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       Vt[(d8 + 2 * e) * LDV + key] = (uint16_t)(w[e] & 0xffff);
@@ -42,12 +61,8 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   }
   __syncthreads();
 
-  const int q0 = blockIdx.x * 64 + wave * 16;
-  if (q0 >= S) return;
+  if (!active) return;
   const int nt = S >> 4;
-  const uint16_t* qrow = base + (size_t)(q0 + r) * ld + h * 64 + (g << 3);
-  const uint4 qf0 = *reinterpret_cast<const uint4*>(qrow);
-  const uint4 qf1 = *reinterpret_cast<const uint4*>(qrow + 32);
 
   f32x4 sc[NT];
 #pragma unroll
