@@ -66,6 +66,28 @@ def out_shape(m, b):
     return (b, m.dims["seq"], m.dims["d"])
 
 
+def link_rates(torch, dev):
+    """(bound rate, copy-engine rate, gather-kernel rate) of the host link in GB/s: the
+    best single 1 GiB pinned copy and the best 1 GiB kernel gather from pinned memory; the
+    bound uses the higher."""
+    import paper_2306_03622_amd as tp
+    memcpy = link_peak(torch, dev)
+    gather = tp.probe_gather_h2d(1 << 30, 1024, 5)
+    return max(memcpy, gather), memcpy, gather
+
+
+def machine_peaks():
+    """Measured matrix-core and HBM peaks next to the published ones."""
+    import paper_2306_03622_amd as tp
+    tflops, clock = tp.probe_mfma_bf16(1024, 2048, 5)
+    hbm = tp.probe_hbm_read(4 << 30, 2048, 5)
+    return {"mfma_bf16_tflops": round(tflops, 1), "shader_clock_ghz": round(clock, 3),
+            "hbm_read_gbs": round(hbm, 1),
+            "published": {"mfma_bf16_tflops": BF16_PEAK_TFLOPS, "hbm_gbs": HBM_PEAK_GBS, "clock_ghz": 2.4},
+            "probe": "1024 workgroups x 4 waves x 2048 x 8 independent bf16 16x16x32 MFMAs; 4 GiB non-temporal "
+                     "read by 2048 workgroups; best of 5 each"}
+
+
 def link_peak(torch, dev, reps=10, nbytes=1 << 30):
     """Best-of-`reps` single pinned host->device copy of 1 GiB (GB/s)."""
     h = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
@@ -375,13 +397,16 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                        "partition_mib": (partition_mib or (arena_gib << 10) // 8) if alloc != "first-fit" else None}}
 
 
-def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, link, steps, warmup, trace):
-    """Cold, warm and swap-only latencies of workload `cfg` at batches `bts` (one context)."""
+def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, link, steps, warmup, trace,
+                     plan_link=None, cpu=False):
+    """Cold, warm and swap-only latencies of workload `cfg` at batches `bts` (one context);
+    `link` sets the bound, `plan_link` (default `link`) the cost-model plan; with `cpu` the
+    oracle's time at each batch too."""
     import paper_2306_03622_amd as tp
     import synth
     m = synth.config_model(cfg)
     out = {}
-    bb = Bench(torch, dev, m, bts, method, chunk, copy_streams, plan=plan, link_gbs=link,
+    bb = Bench(torch, dev, m, bts, method, chunk, copy_streams, plan=plan, link_gbs=plan_link or link,
                flags=tp.TP_FLAG_TRACE if trace else 0)
     for bt in bts:
         rr = measure(bb, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt), steps, warmup, max(4 * steps, 100))
@@ -406,6 +431,11 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
             "warm_tflops": round(fl / (fwd * 1e-3) / 1e12, 2),
             "mfma_util": round(fl / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5)}
     bb.close()
+    if cpu:
+        for bt in bts:
+            log(f"  CPU oracle, workload {cfg} batch {bt}")
+            out[f"cfg{cfg}_b{bt}"]["cpu_oracle"] = cpu_baseline(m, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt),
+                                                                budget_s=8.0, max_runs=50 if cfg == 1 else 5)
     m.drop_blob()
     return out
 
@@ -542,7 +572,8 @@ def main():
             cmd = [sys.executable, os.path.abspath(__file__), "--workload", str(cfg), "--batches",
                    ",".join(map(str, bts)), "--steps", str(a.steps), "--warmup", str(a.warmup), "--method",
                    "memcpy" if a.method == "auto" else a.method, "--chunk", str(a.chunk), "--copy-streams",
-                   str(a.copy_streams), "--plan", a.plan] + (["--trace"] if a.trace else [])
+                   str(a.copy_streams), "--plan", a.plan] + (["--trace"] if a.trace else []) + \
+                  (["--no-cpu"] if a.no_cpu else [])
             out = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)     # its log goes to our stderr
             if out.returncode != 0:
                 raise SystemExit(f"workload {cfg} failed with status {out.returncode}")
@@ -586,14 +617,15 @@ def main():
         return
 
     import paper_2306_03622_amd as tp
-    log("measuring host-link peak (1 GiB pinned H2D, best of 10)")
-    link = link_peak(torch, dev)
-    log(f"  link peak {link:.1f} GB/s")
+    log("measuring host-link peak (1 GiB pinned H2D copies and kernel gathers, best of 10 / 5)")
+    link, link_copy, link_gather = link_rates(torch, dev)
+    log(f"  link peak {link:.1f} GB/s (copy engine {link_copy:.1f}, gather kernel {link_gather:.1f})")
     if a.workload:
         bts = [int(v) for v in a.batches.split(",")]
         chunk = tp.DEFAULT_CHUNK if a.chunk in ("default", "elbow") else int(a.chunk)
         res = measure_workload(torch, dev, a.workload, bts, a.method, chunk, a.copy_streams, a.plan, link, a.steps,
-                               a.warmup, a.trace)
+                               a.warmup, a.trace, plan_link=link_copy if a.method != "gather" else link_gather,
+                               cpu=not a.no_cpu)
         for v in res.values():
             if "cold_p50_ms" in v:
                 v["link_peak_gbs"] = round(link, 2)
@@ -622,7 +654,8 @@ def main():
     if method == "auto":
         rates = {}
         for meth in ("memcpy", "gather"):
-            b = Bench(torch, dev, model, batches, meth, a.chunk, a.copy_streams, plan=a.plan, link_gbs=link)
+            b = Bench(torch, dev, model, batches, meth, a.chunk, a.copy_streams, plan=a.plan,
+                      link_gbs=link_gather if meth == "gather" else link_copy)
             b.swap_only()
             rates[meth] = model.total_bytes / (p50([b.swap_only() for _ in range(5)]) / 1e3) / 1e9
             b.close()
@@ -630,7 +663,8 @@ def main():
         extra["swap_rate_by_method_gbs"] = {k: round(v, 2) for k, v in rates.items()}
         log(f"  swap rates {rates} -> {method}")
 
-    b = Bench(torch, dev, model, batches, method, a.chunk, a.copy_streams, plan=a.plan, link_gbs=link)
+    b = Bench(torch, dev, model, batches, method, a.chunk, a.copy_streams, plan=a.plan,
+              link_gbs=link_gather if method == "gather" else link_copy)
     n_chunks = len(b.rt.chunks(b.mid))
     results = {}
     for bt in batches:
@@ -680,6 +714,8 @@ def main():
     if not a.no_cpu:
         log("CPU oracle baseline")
         cpu = cpu_baseline(model, B, 10200 + B)
+    log("matrix-core and HBM peak probes")
+    peaks = machine_peaks()
 
     line = {
         "metric": "cold-start p50 latency (swap+exec)",
@@ -692,7 +728,9 @@ def main():
                    "chunk_min_bytes": a.chunk if a.plan == "greedy" else None, "copy_streams": a.copy_streams or 1,
                    "direct_max_bytes": tp.DEFAULT_DIRECT},
         "bound_ms": round(bound, 3), "cold_over_bound": round(cold_p50 / bound, 4),
-        "swap_gbs": round(swap_gbs, 2), "link_peak_gbs": round(link, 2), "link_theoretical_gbs": PCIE5_X16_GBS,
+        "swap_gbs": round(swap_gbs, 2), "link_peak_gbs": round(link, 2), "link_copy_engine_gbs": round(link_copy, 2),
+        "link_gather_kernel_gbs": round(link_gather, 2), "link_theoretical_gbs": PCIE5_X16_GBS,
+        "peaks": peaks,
         "warm_p50_ms": round(warm_p50, 4), "roofline": roofline, "cpu_baseline": cpu, "elbow_sweep": sweep,
         "extra": extra,
     }

@@ -3,7 +3,8 @@
     python -m paper_2306_03622_amd.build [--jobs N] [--sanitize]
 
 ``libtorpor.so`` holds the C ABI of include/torpor.h and include/torpor_plan.h with all
-kernels. ``libtorpor_host.so`` is the same host-side bookkeeping (validation, chunk
+kernels; ``libtorpor_probe.so`` the peak probes of include/torpor_probe.h that the
+benchmark measures its rooflines against. ``libtorpor_host.so`` is the same host-side bookkeeping (validation, chunk
 plan, arena) compiled with g++ alone, optionally with ASan/UBSan, for host-only tests.
 """
 from __future__ import annotations
@@ -20,18 +21,24 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtorpor.so")
 HOST_LIB = os.path.join(PKG, "libtorpor_host.so")
+PROBE_LIB = os.path.join(PKG, "libtorpor_probe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 CORE = ["core/model.cpp", "core/arena.cpp", "core/partition.cpp", "core/sched.cpp", "core/plan_api.cpp", "core/errors.cpp"]
 HIP_HOST = ["hip/runtime.cpp", "hip/executors.cpp", "hip/trace.cpp"]
+PROBE = ["probe/peaks.hip"]
 KERNELS = ["kernels/gemm_bf16.hip", "kernels/gemv_bf16.hip", "kernels/linear_f32.hip", "kernels/norm.hip", "kernels/attention.hip",
            "kernels/pool_copy.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall", f"-I{os.path.join(ROOT, 'include')}"]
 # host translation units that use the HIP runtime API only
 HOST_HIP = ["-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
-# device code: gfx950 only; packed-fp32 instructions disabled
-DEVICE = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# device code: gfx950 only; packed-fp32 instructions disabled; MFMA accumulators in ordinary
+# VGPRs (the default accumulation-register form made the register allocator shuffle
+# accumulators between register files inside the GEMM and attention loops: ~2,400 and ~700
+# extra moves per instantiation set; the matrix-core probe ran at half rate because of it)
+DEVICE = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def _run(cmd):
@@ -52,7 +59,7 @@ def build(jobs: int = 8, sanitize: bool = False, verbose: bool = False) -> str:
     cmds = []
     for src in CORE + HIP_HOST:
         cmds.append([HIPCC, *COMMON, *HOST_HIP, "-x", "c++", "-c", os.path.join(CSRC, src), "-o", _obj(src)])
-    for src in KERNELS:
+    for src in KERNELS + PROBE:
         cmds.append([HIPCC, *COMMON, *DEVICE, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", _obj(src)])
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         for msg in ex.map(_run, cmds):
@@ -62,6 +69,10 @@ def build(jobs: int = 8, sanitize: bool = False, verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", *DEVICE, "-o", tmp, *objs, "-lpthread"])
     os.replace(tmp, LIB)
+    # peak probes of the benchmark (a library of their own, no part of the serving path)
+    ptmp = PROBE_LIB + ".tmp"
+    _run([HIPCC, "-shared", "-fPIC", *DEVICE, "-o", ptmp, *[_obj(s) for s in PROBE]])
+    os.replace(ptmp, PROBE_LIB)
     # host-only planning library
     san = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer"] if sanitize else []
     htmp = HOST_LIB + ".tmp"

@@ -18,6 +18,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtorpor.so")
 HOST_LIB_PATH = os.path.join(_HERE, "libtorpor_host.so")
+PROBE_LIB_PATH = os.path.join(_HERE, "libtorpor_probe.so")
 
 TP_OK, TP_E_INVAL, TP_E_NOENT, TP_E_NOSPC, TP_E_HIP, TP_E_STATE = 0, -1, -2, -3, -4, -5
 TP_F32, TP_BF16 = 0, 1
@@ -468,6 +469,51 @@ def tph_alpha_update(alpha, last_ratio, new_ratio, scalar=2.0, threshold=0.04, L
     out = C.c_double()
     _check(L, L.tph_alpha_update(alpha, last_ratio, new_ratio, scalar, threshold, C.byref(out)))
     return out.value
+
+
+_probe = None
+
+
+def probe_lib():
+    """libtorpor_probe.so (include/torpor_probe.h): the machine's measured peaks."""
+    global _probe
+    if _probe is None:
+        if not os.path.exists(PROBE_LIB_PATH):
+            raise ImportError(f"{PROBE_LIB_PATH} is not built; run python -m paper_2306_03622_amd.build")
+        L = C.CDLL(PROBE_LIB_PATH)
+        L.tpp_mfma_bf16.argtypes = [C.c_int, C.c_int, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_double)]
+        L.tpp_hbm_read.argtypes = [C.c_uint64, C.c_int, C.c_int, C.POINTER(C.c_double)]
+        L.tpp_gather_h2d.argtypes = [C.c_uint64, C.c_int, C.c_int, C.POINTER(C.c_double)]
+        for f in (L.tpp_mfma_bf16, L.tpp_hbm_read, L.tpp_gather_h2d):
+            f.restype = C.c_int
+        _probe = L
+    return _probe
+
+
+def _probe_check(rc, what):
+    if rc != 0:
+        raise RuntimeError(f"{what}: HIP error {rc}")
+
+
+def probe_mfma_bf16(wgs=1024, iters=2048, reps=5):
+    """(TFLOP/s, shader clock GHz) of back-to-back bf16 16x16x32 MFMAs on every CU."""
+    t, c = C.c_double(), C.c_double()
+    _probe_check(probe_lib().tpp_mfma_bf16(wgs, iters, reps, C.byref(t), C.byref(c)), "tpp_mfma_bf16")
+    return t.value, c.value
+
+
+def probe_hbm_read(nbytes=4 << 30, wgs=2048, reps=5):
+    """GB/s of a streaming read of nbytes of device memory."""
+    g = C.c_double()
+    _probe_check(probe_lib().tpp_hbm_read(nbytes, wgs, reps, C.byref(g)), "tpp_hbm_read")
+    return g.value
+
+
+def probe_gather_h2d(nbytes=1 << 30, wgs=1024, reps=5):
+    """GB/s of a kernel copying pinned host memory to the device."""
+    g = C.c_double()
+    _probe_check(probe_lib().tpp_gather_h2d(nbytes, wgs, reps, C.byref(g)), "tpp_gather_h2d")
+    return g.value
 
 
 class HostArena:

@@ -38,6 +38,17 @@ def test_library_exports_every_declared_symbol():
     assert set(re.findall(r" T (tph?_\w+)", host)) == {n for n in names if n.startswith("tph_")} | {"tp_last_error"}
 
 
+def test_probe_library_exports_its_header():
+    src = open(os.path.join(ROOT, "include", "torpor_probe.h")).read()
+    declared = set(re.findall(r"^TPP_API\s+[\w\s\*]+?\b(tpp_\w+)\s*\(", src, re.M))
+    assert declared == {"tpp_mfma_bf16", "tpp_hbm_read", "tpp_gather_h2d"}
+    out = subprocess.run(["nm", "-D", "--defined-only", tp.torpor.PROBE_LIB_PATH], capture_output=True, text=True).stdout
+    assert set(re.findall(r" T (tpp_\w+)", out)) == declared
+    L = tp.torpor.probe_lib()
+    for n in declared:
+        assert hasattr(L, n)
+
+
 def _desc(model, mutate=None, dims=None, dtype=None):
     tensors = [[t.layer, t.role, t.offset, t.nbytes, list(t.shape)] for t in model.tensors]
     if mutate:
