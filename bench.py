@@ -441,12 +441,15 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
 
 
 def kernel_fingerprint():
-    """First 16 hex digits of sha256 over the skinny-GEMM kernel sources."""
+    """First 16 hex digits of sha256 over the skinny-GEMM kernel sources and the device
+    compile flags."""
     import hashlib
+    from paper_2306_03622_amd import build as tp_build
     h = hashlib.sha256()
     for f in ("gemv_bf16.hip", "gemm_args.hpp", "common.hpp", "kernels.hpp"):
         with open(os.path.join(ROOT, "paper_2306_03622_amd", "csrc", "kernels", f), "rb") as fh:
             h.update(fh.read())
+    h.update(" ".join(tp_build.DEVICE).encode())
     return h.hexdigest()[:16]
 
 
