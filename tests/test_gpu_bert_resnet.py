@@ -18,6 +18,22 @@ def test_bert_small(seq, batch):
     rt.close()
 
 
+@pytest.mark.parametrize("d", [128, 256, 512])
+def test_bert_split_reduction_with_layernorm(d):
+    # FFN2 (K = 2048: 32 k-stages over 2 x d/64 tiles) is split over k here, so the second
+    # LayerNorm of each layer runs with its reduction: in registers for widths 256 and 512,
+    # as the plain reduction followed by a LayerNorm launch for width 128. Cold and warm
+    # requests agree bitwise; both match the oracle.
+    m = synth.bert(seed=45, layers=2, d=d, heads=d // 64, ffn=2048, seq=64, vocab=500, maxpos=64)
+    ids = synth.bert_input(2, 46, seq=64, vocab=500)
+    rt, (mid,) = make_runtime([m], batch_max=2)
+    log(f"bert d {d}: split FFN2 with LayerNorm")
+    cold = infer(rt, mid, m, ids)
+    assert np.array_equal(cold, infer(rt, mid, m, ids))
+    check_parity(cold, m, ids, 2e-2)
+    rt.close()
+
+
 def test_bert_out_of_range_ids_are_clamped():
     m = synth.bert(seed=43, layers=1, d=64, heads=1, ffn=64, seq=32, vocab=50, maxpos=32)
     ids = synth.bert_input(1, 44, seq=32, vocab=50)
