@@ -211,22 +211,32 @@ __device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k, bool& 
 // every split stores its fp32 partial to a.partials and k_split_reduce (the next launch on
 // the stream) sums the partials in split order, which is fixed, so results are
 // bit-reproducible.
-// 64 x 64 tiles are capped at 128 VGPRs, so four workgroups (16 waves) fit a CU as the LDS
-// allows, instead of two at the uncapped register count (the element-gather loader would
-// spill under the cap and keeps it off).
-template <int BN, int BM, int BK, int MODE, bool WVEC, bool PK, int D>
-__global__ __launch_bounds__(256, (BM == 64 && MODE != X_CONV1) ? 4 : 1) void k_gemm(GemmArgs a) {
+// WGN x WGM waves (64 WGN WGM threads) share a tile, each owning a (BN / WGN) x (BM / WGM)
+// block of it. 64 x 64 tiles of 2 x 2 waves are capped at 128 VGPRs, so four workgroups (16
+// waves) fit a CU as the LDS allows, instead of two at the uncapped register count (the
+// element-gather loader would spill under the cap and keeps it off); 8-wave tiles are capped
+// the same way for two workgroups per CU.
+template <int BN, int BM, int MODE>
+constexpr int gemm_min_waves_per_simd(int nt) {
+  return MODE == X_CONV1 ? 1 : (nt == 256 && BN == 64 && BM == 64) ? 4 : nt == 512 ? 4 : 1;
+}
+
+template <int BN, int BM, int BK, int MODE, bool WVEC, bool PK, int D, int WGN = 2, int WGM = 2>
+__global__ __launch_bounds__(64 * WGN * WGM, (gemm_min_waves_per_simd<BN, BM, MODE>(64 * WGN * WGM)))
+void k_gemm(GemmArgs a) {
+  constexpr int NT = 64 * WGN * WGM;            // threads
   constexpr int LDK = BK + 8;
   constexpr int KV = BK / 8;                    // 16-byte vectors per row and stage
-  constexpr int RSTEP = 256 / KV;               // rows covered by one pass of 256 threads
+  constexpr int RSTEP = NT / KV;                // rows covered by one pass of all threads
   constexpr int VA = BN / RSTEP, VB = BM / RSTEP;
-  constexpr int NB = BN / 32, MB = BM / 32;     // 16 x 16 blocks per wave (wave tile BN/2 x BM/2)
-  static_assert(VA >= 1 && VB >= 1 && BK % 32 == 0 && D >= 2 && D % 2 == 0, "tile shape");
+  constexpr int NB = BN / WGN / 16, MB = BM / WGM / 16;   // 16 x 16 blocks per wave
+  static_assert(VA >= 1 && VB >= 1 && BN % RSTEP == 0 && BM % RSTEP == 0 && NB >= 1 && MB >= 1 &&
+                    BK % 32 == 0 && D >= 2 && D % 2 == 0, "tile shape");
   static_assert(MODE != X_CONV64 || BK == 64, "X_CONV64 steps one 64-deep stage per tap position");
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * (BN + BM) * LDK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave & 1, wm = wave >> 1;
+  const int wn = wave % WGN, wm = wave / WGN;
   const int n_base = blockIdx.x * BN, m_base = blockIdx.y * BM;
   const int row0 = tid / KV, kq = (tid % KV) * 8;
 
@@ -275,10 +285,10 @@ __global__ __launch_bounds__(256, (BM == 64 && MODE != X_CONV1) ? 4 : 1) void k_
       uint4 fa[NB], fb[MB];
 #pragma unroll
       for (int i = 0; i < NB; ++i)
-        fa[i] = *reinterpret_cast<const uint4*>(&As[(wn * (BN / 2) + i * 16 + (lane & 15)) * LDK + kk + ((lane >> 4) << 3)]);
+        fa[i] = *reinterpret_cast<const uint4*>(&As[(wn * (BN / WGN) + i * 16 + (lane & 15)) * LDK + kk + ((lane >> 4) << 3)]);
 #pragma unroll
       for (int j = 0; j < MB; ++j)
-        fb[j] = *reinterpret_cast<const uint4*>(&Bs[(wm * (BM / 2) + j * 16 + (lane & 15)) * LDK + kk + ((lane >> 4) << 3)]);
+        fb[j] = *reinterpret_cast<const uint4*>(&Bs[(wm * (BM / WGM) + j * 16 + (lane & 15)) * LDK + kk + ((lane >> 4) << 3)]);
 #pragma unroll
       for (int i = 0; i < NB; ++i)
 #pragma unroll
@@ -334,13 +344,13 @@ __global__ __launch_bounds__(256, (BM == 64 && MODE != X_CONV1) ? 4 : 1) void k_
   for (int i = 0; i < NB; ++i)
 #pragma unroll
     for (int j = 0; j < MB; ++j) {
-      const int ml = wm * (BM / 2) + j * 16 + (lane & 15);
-      const int nl = wn * (BN / 2) + i * 16 + ((lane >> 4) << 2);
+      const int ml = wm * (BM / WGM) + j * 16 + (lane & 15);
+      const int nl = wn * (BN / WGN) + i * 16 + ((lane >> 4) << 2);
       const f32x4 v = acc[i][j];
       *reinterpret_cast<float4*>(&T[ml * TS + nl]) = make_float4(v[0], v[1], v[2], v[3]);
     }
   __syncthreads();
-  constexpr int TPR = BN / 16, RPI = 256 / TPR;
+  constexpr int TPR = BN / 16, RPI = NT / TPR;
   const int nl = (tid % TPR) * 16;
   const int n0 = n_base + nl;
   const bool vec = n0 + 15 < a.N && (a.N & 3) == 0;
@@ -541,7 +551,7 @@ hipError_t finish(const GemmArgs& a, hipStream_t s) {
   return hipSuccess;
 }
 
-template <int BN, int BM, int BK, int MODE, bool WVEC, int D>
+template <int BN, int BM, int BK, int MODE, bool WVEC, int D, int WGN = 2, int WGM = 2>
 hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   const int tn = (a.N + BN - 1) / BN, tm = (a.M + BM - 1) / BM, tiles = tn * tm;
   const int nst = (a.K + BK - 1) / BK;
@@ -562,11 +572,11 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   dim3 grid(tn, tm, a.splits);
   if constexpr (MODE == X_ROWS) {
     if (a.ep.w_packed) {
-      hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, true, D>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, true, D, WGN, WGM>), grid, dim3(64 * WGN * WGM), 0, s, a);
       return finish(a, s);
     }
   }
-  hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, false, D>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, false, D, WGN, WGM>), grid, dim3(64 * WGN * WGM), 0, s, a);
   return finish(a, s);
 }
 
