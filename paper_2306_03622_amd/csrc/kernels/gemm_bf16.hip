@@ -225,7 +225,11 @@ template <int BN, int BM, int BK, int MODE, bool WVEC, bool PK, int D, int WGN =
 __global__ __launch_bounds__(64 * WGN * WGM, (gemm_min_waves_per_simd<BN, BM, MODE>(64 * WGN * WGM)))
 void k_gemm(GemmArgs a) {
   constexpr int NT = 64 * WGN * WGM;            // threads
-  constexpr int LDK = BK + 8;
+  // LDS row stride of the operand tiles: 80 bf16 (160 B). With 72 (144 B) the 16-byte
+  // fragment reads and stores conflicted on banks (rocprofv3 SQ_LDS_BANK_CONFLICT: 1.18 M
+  // cycles per BERT-base FFN1 launch at batch 8, 2.5 per LDS instruction); 80 measured zero
+  // conflicts (88 and 104 did not help), 4.5% off BERT-base's warm forward
+  constexpr int LDK = BK + 16;
   constexpr int KV = BK / 8;                    // 16-byte vectors per row and stage
   constexpr int RSTEP = NT / KV;                // rows covered by one pass of all threads
   constexpr int VA = BN / RSTEP, VB = BM / RSTEP;
