@@ -570,6 +570,11 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
     while (want > 1 && per_split * want > sp.partial_bytes) --want;
     splits = max(want, 1);
   }
+  // a row LayerNorm epilogue costs a launch of its own unless a split reduction carries it
+  // (BERT-base's attention output projection: warm forward -1.9% at batch 1)
+  if (splits == 1 && sp.partials && a.ep.ln_g && split_reduce_ln_fits(a.N) && nst >= 2 &&
+      (size_t)a.M * a.N * 4 * 2 <= sp.partial_bytes)
+    splits = 2;
   a.kst = (nst + splits - 1) / splits;
   a.splits = (nst + a.kst - 1) / a.kst;        // no empty split
   a.partials = sp.partials;
