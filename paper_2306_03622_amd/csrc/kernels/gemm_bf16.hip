@@ -516,25 +516,57 @@ __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
   }
 }
 
-// y = epilogue(sum over splits z = 0, 1, ... of P[z]) for four consecutive outputs per thread
+// y = epilogue(sum over splits z = 0, 1, ... of P[z]) for four consecutive outputs per thread.
+// A thread fetches the epilogue's inputs and ZG partials before it adds any (a launch that
+// waited for each partial in turn spent ~5 us on a few MB: one memory round trip per split);
+// the additions keep split order, so results are the same as summing one split at a time.
+template <int ZG, int RES>
 __global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
   const long q = (long)blockIdx.x * 256 + threadIdx.x;       // index of a group of 4 outputs
   const int groups_per_row = (a.N + 3) >> 2;
   const long total = (long)a.M * groups_per_row;
   if (q >= total) return;
   const int m = (int)(q / groups_per_row), n0 = (int)(q - (long)m * groups_per_row) * 4;
-  const size_t plane = (size_t)a.M * a.N;
+  const size_t plane = (size_t)a.M * a.N, base = (size_t)m * a.N + n0;
   f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int z = 0; z < a.splits; ++z) {
-    const float* p = a.partials + z * plane + (size_t)m * a.N + n0;
-    if (n0 + 3 < a.N && (a.N & 3) == 0) {
-      const float4 v = *reinterpret_cast<const float4*>(p);
-      sum += f32x4{v.x, v.y, v.z, v.w};
-    } else {
-      for (int e = 0; e < 4 && n0 + e < a.N; ++e) sum[e] += p[e];
+  if (n0 + 3 < a.N && (a.N & 3) == 0) {
+    const Ep4In in = ep4_fetch<RES>(a.ep, base, n0);
+    for (int z0 = 0; z0 < a.splits; z0 += ZG) {
+      float4 t[ZG];
+#pragma unroll
+      for (int u = 0; u < ZG; ++u)
+        if (z0 + u < a.splits) t[u] = *reinterpret_cast<const float4*>(a.partials + (z0 + u) * plane + base);
+#pragma unroll
+      for (int u = 0; u < ZG; ++u)
+        if (z0 + u < a.splits) sum += f32x4{t[u].x, t[u].y, t[u].z, t[u].w};
     }
+    float v[4] = {sum[0], sum[1], sum[2], sum[3]};
+    ep4_apply<RES>(a.ep, in, v);
+    ep4_store(a.ep, base, v);
+    return;
+  }
+  for (int z = 0; z < a.splits; ++z) {
+    const float* p = a.partials + z * plane + base;
+    for (int e = 0; e < 4 && n0 + e < a.N; ++e) sum[e] += p[e];
   }
   store_row4(a, m, n0, sum);
+}
+
+template <int RES>
+void launch_split_reduce_res(const GemmArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+  switch (split_group(a.splits)) {
+    case 2: hipLaunchKernelGGL((k_split_reduce<2, RES>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_split_reduce<4, RES>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_split_reduce<8, RES>), grid, block, 0, s, a); break;
+  }
+}
+
+void launch_split_reduce(const GemmArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+  switch (res_kind(a.ep)) {
+    case 0: launch_split_reduce_res<0>(a, grid, block, s); break;
+    case 1: launch_split_reduce_res<1>(a, grid, block, s); break;
+    default: launch_split_reduce_res<2>(a, grid, block, s); break;
+  }
 }
 
 // After the contraction: the reduction of a k split (fused with the epilogue's row
@@ -546,7 +578,8 @@ hipError_t finish(const GemmArgs& a, hipStream_t s) {
   if (a.splits > 1) {
     if (a.ep.ln_g && split_reduce_ln_fits(a.N)) return split_reduce_ln(a, s);
     const long groups = (long)a.M * ((a.N + 3) / 4);
-    hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, s, a);
+    const dim3 grid((unsigned)((groups + 255) / 256)), block(256);
+    launch_split_reduce(a, grid, block, s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (a.ep.ln_g)
@@ -562,10 +595,14 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   int splits = 1;
   if (sp.partials && tiles < 512) {
     // aim for about 512 workgroups (two per CU), at least 8 k-stages per split, within
-    // the scratch
+    // the scratch; 4 k-stages once the contraction is split anyway, its fp32 partials are
+    // at most 512 KiB per split and no LayerNorm rides on the reduction (ResNet-50 at batch
+    // 1: forward -5.5%; ResNet-50 at batch 8 with its larger partials, BERT-base's FFN2 at
+    // batch 1, or also splitting contractions that 8 stages leave whole: 3-10% slower)
     const size_t per_split = (size_t)a.M * a.N * 4;
     int want = (512 + tiles - 1) / tiles;
-    want = min(want, max(nst / 8, 1));
+    const int min_stages = (nst / 8 >= 2 && per_split <= (512u << 10) && !a.ep.ln_g) ? 4 : 8;
+    want = min(want, max(nst / min_stages, 1));
     want = min(want, 16);
     while (want > 1 && per_split * want > sp.partial_bytes) --want;
     splits = max(want, 1);

@@ -39,10 +39,24 @@ __device__ __forceinline__ void normalize(float (&v)[PER], int D, const uint16_t
   }
 }
 
+// gamma and beta of a lane's run of PER contiguous elements (c = PER lane + i), raw bf16
+// bits, fetched before the row so that their loads overlap the row's
+template <int PER>
+struct LnAffine {
+  uint2 g[PER / 4], b[PER / 4];
+  __device__ __forceinline__ void fetch(const uint16_t* gp, const uint16_t* bp, int c0) {
+#pragma unroll
+    for (int i = 0; i < PER / 4; ++i) {
+      g[i] = *reinterpret_cast<const uint2*>(gp + c0 + 4 * i);
+      b[i] = *reinterpret_cast<const uint2*>(bp + c0 + 4 * i);
+    }
+  }
+};
+
 // The same for a row held as PER contiguous values per lane (element c = PER lane + i).
 template <int PER>
-__device__ __forceinline__ void normalize_runs(float (&v)[PER], int D, const uint16_t* g, const uint16_t* b,
-                                               float eps, int lane, void* out, size_t row_off, int out_f32) {
+__device__ __forceinline__ void normalize_runs(float (&v)[PER], int D, const LnAffine<PER>& af, float eps, int lane,
+                                               void* out, size_t row_off, int out_f32) {
   static_assert(PER % 4 == 0, "runs of 4");
   float s = 0.f;
 #pragma unroll
@@ -59,8 +73,7 @@ __device__ __forceinline__ void normalize_runs(float (&v)[PER], int D, const uin
   const int c0 = lane * PER;
 #pragma unroll
   for (int i = 0; i < PER; i += 4) {
-    const uint2 gg = *reinterpret_cast<const uint2*>(g + c0 + i);
-    const uint2 bb = *reinterpret_cast<const uint2*>(b + c0 + i);
+    const uint2 gg = af.g[i / 4], bb = af.b[i / 4];
     float y[4];
     y[0] = (v[i] - mean) * rstd * bf2f(gg.x & 0xffff) + bf2f(bb.x & 0xffff);
     y[1] = (v[i + 1] - mean) * rstd * bf2f(gg.x >> 16) + bf2f(bb.x >> 16);
@@ -88,12 +101,14 @@ __global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ x, 
   float v[PER];
   const float* xr = x + (size_t)row * D;
   if constexpr (PER % 4 == 0) {
+    LnAffine<PER> af;
+    af.fetch(g, b, lane * PER);
 #pragma unroll
     for (int i = 0; i < PER; i += 4) {
       const float4 t = *reinterpret_cast<const float4*>(xr + lane * PER + i);
       v[i] = t.x; v[i + 1] = t.y; v[i + 2] = t.z; v[i + 3] = t.w;
     }
-    normalize_runs<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, out_f32);
+    normalize_runs<PER>(v, D, af, eps, lane, out, (size_t)row * D, out_f32);
   } else {
 #pragma unroll
     for (int i = 0; i < PER; ++i) v[i] = xr[lane + 64 * i];
@@ -115,6 +130,8 @@ __global__ __launch_bounds__(256) void k_embed_ln(const int32_t* __restrict__ id
   const int s = row % S;
   float v[PER];
   if constexpr (PER % 4 == 0) {
+    LnAffine<PER> af;
+    af.fetch(g, b, lane * PER);
 #pragma unroll
     for (int i = 0; i < PER; i += 4) {
       const int c = lane * PER + i;
@@ -126,7 +143,7 @@ __global__ __launch_bounds__(256) void k_embed_ln(const int32_t* __restrict__ id
       v[i + 2] = bf2f(t.y & 0xffff) + bf2f(p.y & 0xffff) + bf2f(y.y & 0xffff);
       v[i + 3] = bf2f(t.y >> 16) + bf2f(p.y >> 16) + bf2f(y.y >> 16);
     }
-    normalize_runs<PER>(v, D, g, b, eps, lane, out, (size_t)row * D, 0);
+    normalize_runs<PER>(v, D, af, eps, lane, out, (size_t)row * D, 0);
   } else {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
@@ -141,45 +158,66 @@ __global__ __launch_bounds__(256) void k_embed_ln(const int32_t* __restrict__ id
 // one wave per row sums the fp32 partials in split order, applies the contraction's
 // epilogue arithmetic (bias, residual, activation: the same operations in the same order
 // as the plain reduction) and normalises the row in registers. Only the LayerNorm output is
-// written.
-template <int PER>
+// written. The epilogue's inputs, gamma, beta and ZG partials are all fetched before the
+// first addition, so the row costs one memory round trip per ZG splits.
+template <int PER, int ZG, int RES>
 __global__ __launch_bounds__(256) void k_split_reduce_ln(GemmArgs a) {
-  constexpr int D = 64 * PER;
+  constexpr int D = 64 * PER, R = PER / 4;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= a.M) return;
   const Epilogue& ep = a.ep;
   const int c0 = lane * PER;
   const size_t base = (size_t)row * D + c0, plane = (size_t)a.M * D;
+  Ep4In in[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) in[i] = ep4_fetch<RES>(ep, base + 4 * i, c0 + 4 * i);
+  LnAffine<PER> af;
+  af.fetch(ep.ln_g, ep.ln_b, c0);
   float v[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) v[i] = 0.f;
-  for (int z = 0; z < a.splits; ++z) {
+  for (int z0 = 0; z0 < a.splits; z0 += ZG) {
+    float4 t[ZG][R];
 #pragma unroll
-    for (int i = 0; i < PER; i += 4) {
-      const float4 t = *reinterpret_cast<const float4*>(a.partials + z * plane + base + i);
-      v[i] += t.x; v[i + 1] += t.y; v[i + 2] += t.z; v[i + 3] += t.w;
-    }
+    for (int u = 0; u < ZG; ++u)
+#pragma unroll
+      for (int i = 0; i < R; ++i)
+        if (z0 + u < a.splits) t[u][i] = *reinterpret_cast<const float4*>(a.partials + (z0 + u) * plane + base + 4 * i);
+#pragma unroll
+    for (int u = 0; u < ZG; ++u)
+#pragma unroll
+      for (int i = 0; i < R; ++i)
+        if (z0 + u < a.splits) {
+          v[4 * i] += t[u][i].x; v[4 * i + 1] += t[u][i].y; v[4 * i + 2] += t[u][i].z; v[4 * i + 3] += t[u][i].w;
+        }
   }
 #pragma unroll
-  for (int i = 0; i < PER; i += 4) {
-    if (ep.bias) {
-      const uint2 bb = *reinterpret_cast<const uint2*>(ep.bias + c0 + i);
-      v[i] += bf2f(bb.x & 0xffff); v[i + 1] += bf2f(bb.x >> 16); v[i + 2] += bf2f(bb.y & 0xffff); v[i + 3] += bf2f(bb.y >> 16);
-    }
-    if (ep.res) {
-      if (ep.res_f32) {
-        const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(ep.res) + base + i);
-        v[i] += r.x; v[i + 1] += r.y; v[i + 2] += r.z; v[i + 3] += r.w;
-      } else {
-        const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(ep.res) + base + i);
-        v[i] += bf2f(r.x & 0xffff); v[i + 1] += bf2f(r.x >> 16); v[i + 2] += bf2f(r.y & 0xffff); v[i + 3] += bf2f(r.y >> 16);
-      }
-    }
+  for (int i = 0; i < R; ++i) {
+    float w[4] = {v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
+    ep4_apply<RES>(ep, in[i], w);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[i + e] = act_apply(v[i + e], ep.act);
+    for (int e = 0; e < 4; ++e) v[4 * i + e] = w[e];
   }
-  normalize_runs<PER>(v, D, ep.ln_g, ep.ln_b, ep.ln_eps, lane, ep.ln_out, (size_t)row * D, ep.ln_out_f32);
+  normalize_runs<PER>(v, D, af, ep.ln_eps, lane, ep.ln_out, (size_t)row * D, ep.ln_out_f32);
+}
+
+template <int PER, int RES>
+void launch_split_reduce_ln_res(const GemmArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+  switch (split_group(a.splits)) {
+    case 2: hipLaunchKernelGGL((k_split_reduce_ln<PER, 2, RES>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_split_reduce_ln<PER, 4, RES>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_split_reduce_ln<PER, 8, RES>), grid, block, 0, s, a); break;
+  }
+}
+
+template <int PER>
+void launch_split_reduce_ln(const GemmArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+  switch (res_kind(a.ep)) {
+    case 0: launch_split_reduce_ln_res<PER, 0>(a, grid, block, s); break;
+    case 1: launch_split_reduce_ln_res<PER, 1>(a, grid, block, s); break;
+    default: launch_split_reduce_ln_res<PER, 2>(a, grid, block, s); break;
+  }
 }
 
 template <int PER>
@@ -206,10 +244,10 @@ hipError_t split_reduce_ln(const GemmArgs& a, hipStream_t s) {
   if (!split_reduce_ln_fits(a.N) || !a.ep.ln_g || !a.ep.ln_b || !a.ep.ln_out || a.splits < 1) return hipErrorInvalidValue;
   const dim3 grid((a.M + 3) / 4), block(256);
   switch (a.N / 64) {
-    case 4: hipLaunchKernelGGL(k_split_reduce_ln<4>, grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL(k_split_reduce_ln<8>, grid, block, 0, s, a); break;
-    case 12: hipLaunchKernelGGL(k_split_reduce_ln<12>, grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL(k_split_reduce_ln<16>, grid, block, 0, s, a); break;
+    case 4: launch_split_reduce_ln<4>(a, grid, block, s); break;
+    case 8: launch_split_reduce_ln<8>(a, grid, block, s); break;
+    case 12: launch_split_reduce_ln<12>(a, grid, block, s); break;
+    default: launch_split_reduce_ln<16>(a, grid, block, s); break;
   }
   return hipGetLastError();
 }
