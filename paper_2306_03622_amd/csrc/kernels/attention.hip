@@ -16,10 +16,13 @@ namespace tp {
 namespace k {
 namespace {
 
-template <int SMAX>
-__global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ qkv, int S, int H,
+// FULL: S == SMAX, so every key tile is valid at compile time (with a run-time tile count
+// the conditional MFMA accumulators compiled to hundreds of register copies)
+template <int SMAX, bool FULL>
+__global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ qkv, int S_arg, int H,
                                                    uint16_t* __restrict__ out) {
   constexpr int LDK = 72, LDV = SMAX + 8, NT = SMAX / 16;
+  const int S = FULL ? SMAX : S_arg;
   __shared__ __attribute__((aligned(16))) uint16_t Ks[SMAX * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[64 * LDV];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -133,8 +136,10 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
 hipError_t attention(const uint16_t* qkv, int B, int S, int H, uint16_t* out, hipStream_t s) {
   if (!qkv || !out || B < 1 || H < 1 || S < 32 || (S & 31) || S > 256) return hipErrorInvalidValue;
   dim3 grid((S + 63) / 64, H, B);
-  if (S <= 128) hipLaunchKernelGGL((k_attention<128>), grid, dim3(256), 0, s, qkv, S, H, out);
-  else hipLaunchKernelGGL((k_attention<256>), grid, dim3(256), 0, s, qkv, S, H, out);
+  if (S == 128) hipLaunchKernelGGL((k_attention<128, true>), grid, dim3(256), 0, s, qkv, S, H, out);
+  else if (S < 128) hipLaunchKernelGGL((k_attention<128, false>), grid, dim3(256), 0, s, qkv, S, H, out);
+  else if (S == 256) hipLaunchKernelGGL((k_attention<256, true>), grid, dim3(256), 0, s, qkv, S, H, out);
+  else hipLaunchKernelGGL((k_attention<256, false>), grid, dim3(256), 0, s, qkv, S, H, out);
   return hipGetLastError();
 }
 

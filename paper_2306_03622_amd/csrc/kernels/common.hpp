@@ -14,17 +14,34 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float((uint32_t)u << 16); }
 
-// float -> bf16 bits, round to nearest even; NaN stays NaN
+// float -> bf16 bits, round to nearest even; NaN stays NaN (quiet). Written as a select, not
+// an early return: as a branch it compiled to a divergent if per conversion (exec-mask
+// saves and restores around every element of an epilogue)
 __device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t quiet_nan = (u >> 16) | 0x40u;
+  return (uint16_t)((u & 0x7fffffffu) > 0x7f800000u ? quiet_nan : rounded);
+}
+
+// erf(x) by Abramowitz and Stegun, Handbook of Mathematical Functions, formula 7.1.26:
+// 1 - (a1 t + ... + a5 t^5) exp(-x^2) with t = 1 / (1 + p |x|), odd in x, absolute error at
+// most 1.5e-7 (plus the hardware reciprocal's and exponential's rounding). Branch-free: the
+// library erff chose between two evaluations per element, a divergent branch in every
+// GELU epilogue.
+__device__ __forceinline__ float erf_as7126(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.f));
+  float p = fmaf(1.061405429f, t, -1.453152027f);
+  p = fmaf(p, t, 1.421413741f);
+  p = fmaf(p, t, -0.284496736f);
+  p = fmaf(p, t, 0.254829592f);
+  return copysignf(1.f - p * t * __expf(-ax * ax), x);
 }
 
 __device__ __forceinline__ float act_apply(float v, int act) {
   if (act == ACT_RELU) return v > 0.f ? v : 0.f;
-  if (act == ACT_GELU) return 0.5f * v * (1.f + erff(v * 0.70710678118654752f));
+  if (act == ACT_GELU) return 0.5f * v * (1.f + erf_as7126(v * 0.70710678118654752f));
   return v;
 }
 
