@@ -40,7 +40,11 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
   const uint4 qf1 = *reinterpret_cast<const uint4*>(qrow + 32);
 
   // K and V of the head: every load of this thread issued before the first LDS store, so
-  // the round trips overlap (key = 32 i + tid / 8, 8 dims at (tid % 8) * 8)
+  // the round trips overlap. K: key = 32 i + tid / 8, 8 dims at (tid % 8) * 8 (a key's 128
+  // bytes per 8 lanes). V: pair p = 256 i + tid covers key p % SMAX and dims 8 (p / SMAX)
+  // .. +8, so the 64 lanes of a wave hold 64 consecutive keys of the same 8 dims and each
+  // 2-byte store of the transposed copy hits 32 consecutive LDS words (with the K mapping,
+  // 8 lanes of different dims shared one bank: 4-way conflicts on every store)
   constexpr int NV = SMAX * 8 / 256;
   uint4 kv[NV], vv[NV];
 #pragma unroll
@@ -48,18 +52,22 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
     const int key = (i * 256 + tid) >> 3, d8 = (tid & 7) << 3;
     const uint16_t* row = base + (size_t)(key < S ? key : 0) * ld + h * 64 + d8;
     kv[i] = *reinterpret_cast<const uint4*>(row + D);
-    vv[i] = *reinterpret_cast<const uint4*>(row + 2 * D);
+    const int p = i * 256 + tid, vkey = p % SMAX, vd8 = (p / SMAX) << 3;
+    const uint16_t* vrow = base + (size_t)(vkey < S ? vkey : 0) * ld + h * 64 + vd8;
+    vv[i] = *reinterpret_cast<const uint4*>(vrow + 2 * D);
   }
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int key = (i * 256 + tid) >> 3, d8 = (tid & 7) << 3;
-    if (key >= S) continue;
-    *reinterpret_cast<uint4*>(&Ks[key * LDK + d8]) = kv[i];
-    const uint32_t w[4] = {vv[i].x, vv[i].y, vv[i].z, vv[i].w};
+    if (key < S) *reinterpret_cast<uint4*>(&Ks[key * LDK + d8]) = kv[i];
+    const int p = i * 256 + tid, vkey = p % SMAX, vd8 = (p / SMAX) << 3;
+    if (vkey < S) {
+      const uint32_t w[4] = {vv[i].x, vv[i].y, vv[i].z, vv[i].w};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      Vt[(d8 + 2 * e) * LDV + key] = (uint16_t)(w[e] & 0xffff);
-      Vt[(d8 + 2 * e + 1) * LDV + key] = (uint16_t)(w[e] >> 16);
+      for (int e = 0; e < 4; ++e) {
+        Vt[(vd8 + 2 * e) * LDV + vkey] = (uint16_t)(w[e] & 0xffff);
+        Vt[(vd8 + 2 * e + 1) * LDV + vkey] = (uint16_t)(w[e] >> 16);
+      }
     }
   }
   __syncthreads();
@@ -93,7 +101,8 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
     if (t < nt)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p = expf((sc[t][e] - mx) * 0.125f);
+        // exp((s - max) / sqrt(64)) as one hardware base-2 exponential
+        const float p = __builtin_amdgcn_exp2f((sc[t][e] - mx) * (0.125f * 1.44269504088896341f));
         sc[t][e] = p;
         sum += p;
       }
