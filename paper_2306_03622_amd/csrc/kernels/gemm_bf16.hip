@@ -134,33 +134,39 @@ struct TapPos {
   }
 };
 
-// The loaders below return the raw 16 bytes of an always-in-bounds load (clamped address)
-// and report in `ok` whether they are real operand data; the caller zeroes invalid ones
-// when it stores them to LDS, stages later. Masking right after the load would make every
-// wave wait for each load as soon as it is issued.
-__device__ __forceinline__ uint4 load_x_tap(const GemmArgs& a, const RowInfo& ri, const TapPos& tp, int kq, bool& ok) {
+// 16 zero bytes in device memory: a loader whose operand lies outside the matrix or the
+// image reads them instead, so invalid data is zero as loaded. (Zeroing it after the load
+// instead, when stored to LDS, made the compiler compute every ring slot's masks at the
+// top of the main loop, and so wait there for every load in flight, including those just
+// issued for later stages: a ring of any depth then hid one stage of latency.)
+__device__ uint4 g_zero16[1];
+
+__device__ __forceinline__ uint4 load_or_zero(const uint16_t* p, bool ok) {
+  return *(ok ? reinterpret_cast<const uint4*>(p) : static_cast<const uint4*>(g_zero16));
+}
+
+__device__ __forceinline__ uint4 load_x_tap(const GemmArgs& a, const RowInfo& ri, const TapPos& tp, int kq) {
   const int ih = ri.ih0 + tp.kh, iw = ri.iw0 + tp.kw;
-  ok = ri.valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+  const bool ok = ri.valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
   const size_t off = ri.base + ((size_t)tp.kh * a.W + tp.kw) * a.C + tp.c0 + kq;
-  return *reinterpret_cast<const uint4*>(a.x + (ok ? off : 0));
+  return load_or_zero(a.x + (ok ? off : 0), ok);
 }
 
 template <int MODE>
-__device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, int k, bool& ok) {
+__device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, int k) {
   if (MODE == X_ROWS) {
-    ok = ri.valid && k < a.K;
-    return *reinterpret_cast<const uint4*>(a.x + (size_t)ri.b * a.K + (ok ? k : 0));
+    const bool ok = ri.valid && k < a.K;
+    return load_or_zero(a.x + (size_t)ri.b * a.K + (ok ? k : 0), ok);
   }
   if (MODE == X_CONV8) {
     const int tap = k / a.C, c = k - tap * a.C;
     const int kh = tap / a.KW, kw = tap - kh * a.KW;
     const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
-    ok = ri.valid && k < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+    const bool ok = ri.valid && k < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
     const size_t off = ok ? (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c : 0;
-    return *reinterpret_cast<const uint4*>(a.x + off);
+    return load_or_zero(a.x + off, ok);
   }
-  ok = true;                                   // element-wise gather: already zero-filled
-  uint32_t v[8];
+  uint32_t v[8];                               // element-wise gather, zero-filled
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int kk = k + e;
@@ -175,25 +181,24 @@ __device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, i
 }
 
 // weights in 16 x 128 blocks (N % 16 == 0, K % 128 == 0): element (n, k) of an 8-run
-__device__ __forceinline__ uint4 load_w8_packed(const GemmArgs& a, int n, int k, bool& ok) {
-  ok = n < a.N && k < a.K;
+__device__ __forceinline__ uint4 load_w8_packed(const GemmArgs& a, int n, int k) {
+  const bool ok = n < a.N && k < a.K;
   const int nn = ok ? n : 0, kk = ok ? k : 0;
   const size_t off = ((((size_t)(nn >> 4) * (a.K >> 7) + (kk >> 7)) * 4 + ((kk >> 5) & 3)) * 512) +
                      ((((kk >> 3) & 3) << 4) + (nn & 15)) * 8;
-  return *reinterpret_cast<const uint4*>(a.w + off);
+  return load_or_zero(a.w + off, ok);
 }
 
 template <bool WVEC, bool PK>
-__device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k, bool& ok) {
-  if (PK) return load_w8_packed(a, n, k, ok);
+__device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
+  if (PK) return load_w8_packed(a, n, k);
   const bool row_ok = n < a.N;
   const uint16_t* p = a.w + (size_t)(row_ok ? n : 0) * a.K;
   if (WVEC) {
-    ok = row_ok && k < a.K;
-    return *reinterpret_cast<const uint4*>(p + (ok ? k : 0));
+    const bool ok = row_ok && k < a.K;
+    return load_or_zero(p + (ok ? k : 0), ok);
   }
-  ok = true;                                   // element-wise: already zero-filled
-  uint32_t v[8];
+  uint32_t v[8];                               // element-wise, zero-filled
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const bool ok = row_ok && k + e < a.K;
@@ -206,8 +211,8 @@ __device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k, bool& 
 // global loads of a stage are issued D stages before its multiplications, into a ring of D
 // register sets, so D memory round trips overlap (the tiles are small and the contractions
 // short, so latency, not bandwidth, bounds these kernels); LDS is double-buffered, one
-// barrier per stage. Invalid operand data (outside the matrix or the image) is zeroed only
-// when it is stored to LDS, so no wave waits for a load when it issues it. With a.splits > 1
+// barrier per stage. Invalid operand data (outside the matrix or the image) is loaded from a
+// zero block, so a stage's LDS store waits only for that stage's loads. With a.splits > 1
 // every split stores its fp32 partial to a.partials and k_split_reduce (the next launch on
 // the stream) sums the partials in split order, which is fixed, so results are
 // bit-reproducible.
@@ -258,28 +263,27 @@ void k_gemm(GemmArgs a) {
   const int s0 = blockIdx.z * a.kst;
   const int n = min(s0 + a.kst, nst) - s0;      // stages of this split (>= 1: no empty split)
   uint4 ra[D][VA], rb[D][VB];
-  bool oka[D][VA], okb[D][VB];
-  auto load = [&](int s, uint4 (&A)[VA], bool (&OA)[VA], uint4 (&Bv)[VB], bool (&OB)[VB]) {
+  auto load = [&](int s, uint4 (&A)[VA], uint4 (&Bv)[VB]) {
     const int k = s * BK + kq;
 #pragma unroll
-    for (int p = 0; p < VA; ++p) A[p] = load_w8<WVEC, PK>(a, n_base + row0 + RSTEP * p, k, OA[p]);
+    for (int p = 0; p < VA; ++p) A[p] = load_w8<WVEC, PK>(a, n_base + row0 + RSTEP * p, k);
     if (MODE == X_CONV64) {
       TapPos tap;
       tap.init(a, s * BK);
 #pragma unroll
-      for (int p = 0; p < VB; ++p) Bv[p] = load_x_tap(a, ri[p], tap, kq, OB[p]);
+      for (int p = 0; p < VB; ++p) Bv[p] = load_x_tap(a, ri[p], tap, kq);
     } else {
 #pragma unroll
-      for (int p = 0; p < VB; ++p) Bv[p] = load_x8<MODE>(a, ri[p], k, OB[p]);
+      for (int p = 0; p < VB; ++p) Bv[p] = load_x8<MODE>(a, ri[p], k);
     }
   };
-  auto store = [&](int buf, const uint4 (&A)[VA], const bool (&OA)[VA], const uint4 (&Bv)[VB], const bool (&OB)[VB]) {
+  auto store = [&](int buf, const uint4 (&A)[VA], const uint4 (&Bv)[VB]) {
     uint16_t* As = lds + buf * (BN + BM) * LDK;
     uint16_t* Bs = As + BN * LDK;
 #pragma unroll
-    for (int p = 0; p < VA; ++p) *reinterpret_cast<uint4*>(&As[(row0 + RSTEP * p) * LDK + kq]) = mask_u4(A[p], OA[p]);
+    for (int p = 0; p < VA; ++p) *reinterpret_cast<uint4*>(&As[(row0 + RSTEP * p) * LDK + kq]) = A[p];
 #pragma unroll
-    for (int p = 0; p < VB; ++p) *reinterpret_cast<uint4*>(&Bs[(row0 + RSTEP * p) * LDK + kq]) = mask_u4(Bv[p], OB[p]);
+    for (int p = 0; p < VB; ++p) *reinterpret_cast<uint4*>(&Bs[(row0 + RSTEP * p) * LDK + kq]) = Bv[p];
   };
   auto compute = [&](int buf) {
     const uint16_t* As = lds + buf * (BN + BM) * LDK;
@@ -305,9 +309,9 @@ void k_gemm(GemmArgs a) {
   // then stage D into the freed slot 0
 #pragma unroll
   for (int i = 0; i < D; ++i)
-    if (i < n) load(s0 + i, ra[i], oka[i], rb[i], okb[i]);
-  store(0, ra[0], oka[0], rb[0], okb[0]);
-  if (D < n) load(s0 + D, ra[0], oka[0], rb[0], okb[0]);
+    if (i < n) load(s0 + i, ra[i], rb[i]);
+  store(0, ra[0], rb[0]);
+  if (D < n) load(s0 + D, ra[0], rb[0]);
   __syncthreads();
   // Stage j sits in ring slot j % D and LDS buffer j % 2; the loops are unrolled by D (even),
   // so every slot and buffer index is a constant. Steady state: trips whose loads are all
@@ -319,8 +323,8 @@ void k_gemm(GemmArgs a) {
     for (int u = 0; u < D; ++u) {
       const int nx = (u + 1) % D;
       compute(u & 1);
-      store((u + 1) & 1, ra[nx], oka[nx], rb[nx], okb[nx]);        // stage j0+u+1
-      load(s0 + j0 + u + 1 + D, ra[nx], oka[nx], rb[nx], okb[nx]);  // stage j0+u+1+D
+      store((u + 1) & 1, ra[nx], rb[nx]);        // stage j0+u+1
+      load(s0 + j0 + u + 1 + D, ra[nx], rb[nx]);  // stage j0+u+1+D
       __syncthreads();
     }
   }
@@ -330,8 +334,8 @@ void k_gemm(GemmArgs a) {
       const int j = j0 + u, nx = (u + 1) % D;
       if (j < n) {
         compute(u & 1);
-        if (j + 1 < n) store((u + 1) & 1, ra[nx], oka[nx], rb[nx], okb[nx]);
-        if (j + 1 + D < n) load(s0 + j + 1 + D, ra[nx], oka[nx], rb[nx], okb[nx]);
+        if (j + 1 < n) store((u + 1) & 1, ra[nx], rb[nx]);
+        if (j + 1 + D < n) load(s0 + j + 1 + D, ra[nx], rb[nx]);
         __syncthreads();
       }
     }
