@@ -145,6 +145,20 @@ __device__ __forceinline__ uint4 load_or_zero(const uint16_t* p, bool ok) {
   return *(ok ? reinterpret_cast<const uint4*>(p) : static_cast<const uint4*>(g_zero16));
 }
 
+// Buffer loads of a row-major operand: one buffer resource per matrix (base, size in bytes
+// < 2^31), a 32-bit byte offset per load; an offset at or beyond the size reads zero, so an
+// invalid operand costs an offset select and no address arithmetic in 64 bits.
+constexpr uint32_t kOffNone = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ uint4 load_x_tap(const GemmArgs& a, const RowInfo& ri, const TapPos& tp, int kq) {
   const int ih = ri.ih0 + tp.kh, iw = ri.iw0 + tp.kw;
   const bool ok = ri.valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
@@ -263,11 +277,36 @@ void k_gemm(GemmArgs a) {
   const int s0 = blockIdx.z * a.kst;
   const int n = min(s0 + a.kst, nst) - s0;      // stages of this split (>= 1: no empty split)
   uint4 ra[D][VA], rb[D][VB];
+  // row-major operands through buffer loads: per-thread byte offsets of k = 0
+  constexpr bool BUFW = WVEC && !PK, BUFX = MODE == X_ROWS;
+  const __amdgpu_buffer_rsrc_t rw = buffer_of(a.w, BUFW ? (uint32_t)((size_t)a.N * a.K * 2) : 0u);
+  const __amdgpu_buffer_rsrc_t rx = buffer_of(a.x, BUFX ? (uint32_t)((size_t)a.M * a.K * 2) : 0u);
+  uint32_t offw[VA], offx[VB];
+  if constexpr (BUFW) {
+#pragma unroll
+    for (int p = 0; p < VA; ++p) {
+      const int nn = n_base + row0 + RSTEP * p;
+      offw[p] = nn < a.N ? (uint32_t)(((size_t)nn * a.K + kq) * 2) : kOffNone;
+    }
+  }
+  if constexpr (BUFX) {
+#pragma unroll
+    for (int p = 0; p < VB; ++p) offx[p] = ri[p].valid ? (uint32_t)(((size_t)ri[p].b * a.K + kq) * 2) : kOffNone;
+  }
   auto load = [&](int s, uint4 (&A)[VA], uint4 (&Bv)[VB]) {
     const int k = s * BK + kq;
+    const bool kin = k < a.K;
+    if constexpr (BUFW) {
 #pragma unroll
-    for (int p = 0; p < VA; ++p) A[p] = load_w8<WVEC, PK>(a, n_base + row0 + RSTEP * p, k);
-    if (MODE == X_CONV64) {
+      for (int p = 0; p < VA; ++p) A[p] = buffer_load16(rw, kin ? offw[p] + (uint32_t)(s * BK * 2) : kOffNone);
+    } else {
+#pragma unroll
+      for (int p = 0; p < VA; ++p) A[p] = load_w8<WVEC, PK>(a, n_base + row0 + RSTEP * p, k);
+    }
+    if constexpr (BUFX) {
+#pragma unroll
+      for (int p = 0; p < VB; ++p) Bv[p] = buffer_load16(rx, kin ? offx[p] + (uint32_t)(s * BK * 2) : kOffNone);
+    } else if (MODE == X_CONV64) {
       TapPos tap;
       tap.init(a, s * BK);
 #pragma unroll
@@ -659,6 +698,8 @@ hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N
     hipError_t e = launch_skinny(a, s);
     return e == hipSuccess ? finish(a, s) : e;
   }
+  // the tiled kernel addresses x and w through 32-bit buffer offsets
+  if ((size_t)M * K * 2 >= (1u << 31) || (size_t)N * K * 2 >= (1u << 31)) return hipErrorInvalidValue;
   return pick_tiled<X_ROWS, true>(a, sp, s);
 }
 

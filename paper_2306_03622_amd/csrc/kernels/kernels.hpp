@@ -36,12 +36,14 @@ struct Split {
   size_t partial_bytes = 0;
 };
 
-// y[M][N] = x[M][K] * w[N][K]^T with the epilogue; bf16 in, fp32 accumulate. K % 8 == 0.
+// y[M][N] = x[M][K] * w[N][K]^T with the epilogue; bf16 in, fp32 accumulate. K % 8 == 0;
+// for M > 32, x and w each below 2 GiB (M K 2 and N K 2 bytes < 2^31).
 hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N, const Epilogue& ep,
                        const Split& sp, hipStream_t s);
 
 // Implicit-GEMM convolution: x NHWC [B][H][W][C] bf16, w OHWI [O][KH][KW][C] bf16,
-// y NHWC [B][Ho][Wo][O] via the epilogue (M = B*Ho*Wo rows of N = O).
+// y NHWC [B][Ho][Wo][O] via the epilogue (M = B*Ho*Wo rows of N = O). A 1x1 stride-1
+// convolution is a linear layer and has its size limits.
 hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16_t* w, int O, int KH, int KW,
                      int stride, int pad, const Epilogue& ep, const Split& sp, hipStream_t s);
 
