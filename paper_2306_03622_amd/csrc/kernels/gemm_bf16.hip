@@ -278,9 +278,13 @@ void k_gemm(GemmArgs a) {
   const int n = min(s0 + a.kst, nst) - s0;      // stages of this split (>= 1: no empty split)
   uint4 ra[D][VA], rb[D][VB];
   // row-major operands through buffer loads: per-thread byte offsets of k = 0
-  constexpr bool BUFW = WVEC && !PK, BUFX = MODE == X_ROWS;
+  // (X_CONV64: the input image, offsets of each row's top-left tap, wrapping modulo 2^32 where
+  // the window starts in the padding; a valid tap brings them back inside the image)
+  constexpr bool BUFW = WVEC && !PK, BUFX = MODE == X_ROWS, BUFC = MODE == X_CONV64;
   const __amdgpu_buffer_rsrc_t rw = buffer_of(a.w, BUFW ? (uint32_t)((size_t)a.N * a.K * 2) : 0u);
-  const __amdgpu_buffer_rsrc_t rx = buffer_of(a.x, BUFX ? (uint32_t)((size_t)a.M * a.K * 2) : 0u);
+  const uint32_t xbytes = BUFX ? (uint32_t)((size_t)a.M * a.K * 2)
+                          : BUFC ? (uint32_t)((size_t)(a.M / (a.Ho * a.Wo)) * a.H * a.W * a.C * 2) : 0u;
+  const __amdgpu_buffer_rsrc_t rx = buffer_of(a.x, xbytes);
   uint32_t offw[VA], offx[VB];
   if constexpr (BUFW) {
 #pragma unroll
@@ -292,6 +296,10 @@ void k_gemm(GemmArgs a) {
   if constexpr (BUFX) {
 #pragma unroll
     for (int p = 0; p < VB; ++p) offx[p] = ri[p].valid ? (uint32_t)(((size_t)ri[p].b * a.K + kq) * 2) : kOffNone;
+  }
+  if constexpr (BUFC) {
+#pragma unroll
+    for (int p = 0; p < VB; ++p) offx[p] = (uint32_t)((ri[p].base + kq) * 2);
   }
   auto load = [&](int s, uint4 (&A)[VA], uint4 (&Bv)[VB]) {
     const int k = s * BK + kq;
@@ -306,6 +314,16 @@ void k_gemm(GemmArgs a) {
     if constexpr (BUFX) {
 #pragma unroll
       for (int p = 0; p < VB; ++p) Bv[p] = buffer_load16(rx, kin ? offx[p] + (uint32_t)(s * BK * 2) : kOffNone);
+    } else if constexpr (BUFC) {
+      TapPos tap;
+      tap.init(a, s * BK);
+      const uint32_t toff = (uint32_t)(((tap.kh * a.W + tap.kw) * a.C + tap.c0) * 2);
+#pragma unroll
+      for (int p = 0; p < VB; ++p) {
+        const int ih = ri[p].ih0 + tap.kh, iw = ri[p].iw0 + tap.kw;
+        const bool ok = ri[p].valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+        Bv[p] = buffer_load16(rx, ok ? offx[p] + toff : kOffNone);
+      }
     } else if (MODE == X_CONV64) {
       TapPos tap;
       tap.init(a, s * BK);
@@ -717,6 +735,8 @@ hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16
   a.H = H; a.W = W; a.C = C; a.KW = KW; a.stride = stride; a.pad = pad; a.Ho = Ho; a.Wo = Wo;
   a.ep = ep;
   a.ep.w_packed = 0;
+  if ((size_t)B * H * W * C * 2 >= (1u << 31) || (size_t)O * KH * KW * C * 2 >= (1u << 31))
+    return hipErrorInvalidValue;   // the tiled kernel addresses x and w through 32-bit buffer offsets
   if (C <= SC_MAXC && KH <= SC_MAXK && KW <= SC_MAXK && stride <= SC_MAXS && O <= 64 && (O & 15) == 0 &&
       a.K <= SC_KP) {
     // enough workgroups to fill the chip, each reusing its staged weights over `rows` rows

@@ -42,8 +42,8 @@ hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N
                        const Split& sp, hipStream_t s);
 
 // Implicit-GEMM convolution: x NHWC [B][H][W][C] bf16, w OHWI [O][KH][KW][C] bf16,
-// y NHWC [B][Ho][Wo][O] via the epilogue (M = B*Ho*Wo rows of N = O). A 1x1 stride-1
-// convolution is a linear layer and has its size limits.
+// y NHWC [B][Ho][Wo][O] via the epilogue (M = B*Ho*Wo rows of N = O). x and w each below
+// 2 GiB; a 1x1 stride-1 convolution is a linear layer and has its size limits too.
 hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16_t* w, int O, int KH, int KW,
                      int stride, int pad, const Epilogue& ep, const Split& sp, hipStream_t s);
 
