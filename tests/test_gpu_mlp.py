@@ -71,3 +71,16 @@ def test_cfg2_full(batch):
     assert np.array_equal(cold, warm)
     check_parity(cold, m, x, 2e-2)
     rt.close()
+
+
+@pytest.mark.parametrize("width,batch", [(2000, 8200), (2048, 8192)])
+def test_mlp_bf16_large_tiles(width, batch):
+    # ceil(width/128) * ceil(batch/128) >= 1024 tiles of 128 x 128: the contraction takes the
+    # 128 x 128 tile kernel; width 2000 (row-major weights, ragged in both tile dimensions)
+    # and 2048 (blocked weights)
+    m = synth.mlp(2, width, "bf16", "gelu", seed=23)
+    x = synth.mlp_input(batch, width, "bf16", 500 + width)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"mlp bf16 width {width} batch {batch}: 128 x 128 tiles")
+    check_parity(infer(rt, mid, m, x), m, x, 2e-2)
+    rt.close()
