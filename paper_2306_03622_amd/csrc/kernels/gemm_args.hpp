@@ -8,8 +8,8 @@ namespace tp {
 namespace k {
 
 // activation loaders: row-major matrix; NHWC im2col with C % 64 == 0 (a 64-deep k-stage
-// then lies inside one filter tap); NHWC im2col with C % 8 == 0; element-wise im2col
-enum { X_ROWS = 0, X_CONV8 = 1, X_CONV1 = 2, X_CONV64 = 3 };
+// then lies inside one filter tap)
+enum { X_ROWS = 0, X_CONV64 = 3 };
 
 struct GemmArgs {
   const uint16_t* x;

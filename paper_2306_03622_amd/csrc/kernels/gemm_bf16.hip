@@ -134,8 +134,8 @@ struct TapPos {
   }
 };
 
-// 16 zero bytes in device memory: a loader whose operand lies outside the matrix or the
-// image reads them instead, so invalid data is zero as loaded. (Zeroing it after the load
+// 16 zero bytes in device memory: the blocked-weight loader (not read through buffer loads)
+// reads them for an operand outside the matrix, so invalid data is zero as loaded. (Zeroing it after the load
 // instead, when stored to LDS, made the compiler compute every ring slot's masks at the
 // top of the main loop, and so wait there for every load in flight, including those just
 // issued for later stages: a ring of any depth then hid one stage of latency.)
@@ -159,41 +159,6 @@ __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-__device__ __forceinline__ uint4 load_x_tap(const GemmArgs& a, const RowInfo& ri, const TapPos& tp, int kq) {
-  const int ih = ri.ih0 + tp.kh, iw = ri.iw0 + tp.kw;
-  const bool ok = ri.valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
-  const size_t off = ri.base + ((size_t)tp.kh * a.W + tp.kw) * a.C + tp.c0 + kq;
-  return load_or_zero(a.x + (ok ? off : 0), ok);
-}
-
-template <int MODE>
-__device__ __forceinline__ uint4 load_x8(const GemmArgs& a, const RowInfo& ri, int k) {
-  if (MODE == X_ROWS) {
-    const bool ok = ri.valid && k < a.K;
-    return load_or_zero(a.x + (size_t)ri.b * a.K + (ok ? k : 0), ok);
-  }
-  if (MODE == X_CONV8) {
-    const int tap = k / a.C, c = k - tap * a.C;
-    const int kh = tap / a.KW, kw = tap - kh * a.KW;
-    const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
-    const bool ok = ri.valid && k < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-    const size_t off = ok ? (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c : 0;
-    return load_or_zero(a.x + off, ok);
-  }
-  uint32_t v[8];                               // element-wise gather, zero-filled
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int kk = k + e;
-    const int tap = kk / a.C, c = kk - tap * a.C;
-    const int kh = tap / a.KW, kw = tap - kh * a.KW;
-    const int ih = ri.ih0 + kh, iw = ri.iw0 + kw;
-    const bool ok = ri.valid && kk < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-    const size_t off = ok ? (((size_t)ri.b * a.H + ih) * a.W + iw) * a.C + c : 0;
-    v[e] = ok ? (uint32_t)a.x[off] : 0u;
-  }
-  return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
-}
-
 // weights in 16 x 128 blocks (N % 16 == 0, K % 128 == 0): element (n, k) of an 8-run
 __device__ __forceinline__ uint4 load_w8_packed(const GemmArgs& a, int n, int k) {
   const bool ok = n < a.N && k < a.K;
@@ -201,24 +166,6 @@ __device__ __forceinline__ uint4 load_w8_packed(const GemmArgs& a, int n, int k)
   const size_t off = ((((size_t)(nn >> 4) * (a.K >> 7) + (kk >> 7)) * 4 + ((kk >> 5) & 3)) * 512) +
                      ((((kk >> 3) & 3) << 4) + (nn & 15)) * 8;
   return load_or_zero(a.w + off, ok);
-}
-
-template <bool WVEC, bool PK>
-__device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
-  if (PK) return load_w8_packed(a, n, k);
-  const bool row_ok = n < a.N;
-  const uint16_t* p = a.w + (size_t)(row_ok ? n : 0) * a.K;
-  if (WVEC) {
-    const bool ok = row_ok && k < a.K;
-    return load_or_zero(p + (ok ? k : 0), ok);
-  }
-  uint32_t v[8];                               // element-wise, zero-filled
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const bool ok = row_ok && k + e < a.K;
-    v[e] = ok ? (uint32_t)p[ok ? k + e : 0] : 0u;
-  }
-  return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
 // One BN x BM output tile over the k-stages [s0, s0 + n) of this split (blockIdx.z). The
@@ -237,7 +184,7 @@ __device__ __forceinline__ uint4 load_w8(const GemmArgs& a, int n, int k) {
 // the same way for two workgroups per CU.
 template <int BN, int BM, int MODE>
 constexpr int gemm_min_waves_per_simd(int nt) {
-  return MODE == X_CONV1 ? 1 : (nt == 256 && BN == 64 && BM == 64) ? 4 : nt == 512 ? 4 : 1;
+  return (nt == 256 && BN == 64 && BM == 64) ? 4 : nt == 512 ? 4 : 1;
 }
 
 template <int BN, int BM, int BK, int MODE, bool WVEC, bool PK, int D, int WGN = 2, int WGM = 2>
@@ -308,13 +255,15 @@ void k_gemm(GemmArgs a) {
 #pragma unroll
       for (int p = 0; p < VA; ++p) A[p] = buffer_load16(rw, kin ? offw[p] + (uint32_t)(s * BK * 2) : kOffNone);
     } else {
+      static_assert(PK && WVEC, "weights: row-major (buffer loads) or blocked");
 #pragma unroll
-      for (int p = 0; p < VA; ++p) A[p] = load_w8<WVEC, PK>(a, n_base + row0 + RSTEP * p, k);
+      for (int p = 0; p < VA; ++p) A[p] = load_w8_packed(a, n_base + row0 + RSTEP * p, k);
     }
     if constexpr (BUFX) {
 #pragma unroll
       for (int p = 0; p < VB; ++p) Bv[p] = buffer_load16(rx, kin ? offx[p] + (uint32_t)(s * BK * 2) : kOffNone);
-    } else if constexpr (BUFC) {
+    } else {
+      static_assert(BUFC, "activation modes: rows or 64-channel convolution taps");
       TapPos tap;
       tap.init(a, s * BK);
       const uint32_t toff = (uint32_t)(((tap.kh * a.W + tap.kw) * a.C + tap.c0) * 2);
@@ -324,14 +273,6 @@ void k_gemm(GemmArgs a) {
         const bool ok = ri[p].valid && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
         Bv[p] = buffer_load16(rx, ok ? offx[p] + toff : kOffNone);
       }
-    } else if (MODE == X_CONV64) {
-      TapPos tap;
-      tap.init(a, s * BK);
-#pragma unroll
-      for (int p = 0; p < VB; ++p) Bv[p] = load_x_tap(a, ri[p], tap, kq);
-    } else {
-#pragma unroll
-      for (int p = 0; p < VB; ++p) Bv[p] = load_x8<MODE>(a, ri[p], k);
     }
   };
   auto store = [&](int buf, const uint4 (&A)[VA], const uint4 (&Bv)[VB]) {
@@ -752,9 +693,7 @@ hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16
     return hipGetLastError();
   }
   if ((C & 63) == 0) return pick_tiled<X_CONV64, true>(a, sp, s);
-  if ((C & 7) == 0) return pick_tiled<X_CONV8, true>(a, sp, s);
-  if ((a.K & 7) == 0) return pick_tiled<X_CONV1, true>(a, sp, s);
-  return pick_tiled<X_CONV1, false>(a, sp, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace k

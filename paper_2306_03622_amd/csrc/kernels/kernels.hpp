@@ -42,8 +42,11 @@ hipError_t linear_bf16(const uint16_t* x, int M, int K, const uint16_t* w, int N
                        const Split& sp, hipStream_t s);
 
 // Implicit-GEMM convolution: x NHWC [B][H][W][C] bf16, w OHWI [O][KH][KW][C] bf16,
-// y NHWC [B][Ho][Wo][O] via the epilogue (M = B*Ho*Wo rows of N = O). x and w each below
-// 2 GiB; a 1x1 stride-1 convolution is a linear layer and has its size limits too.
+// y NHWC [B][Ho][Wo][O] via the epilogue (M = B*Ho*Wo rows of N = O). C % 64 == 0 (implicit
+// GEMM), or C <= 4 with O <= 64, O % 16 == 0 and a filter of at most 7 x 7, stride <= 2 (the
+// small-channel kernel of a network's stem); other channel counts return
+// hipErrorInvalidValue. x and w each below 2 GiB; a 1x1 stride-1 convolution is a linear
+// layer and has its size limits too.
 hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16_t* w, int O, int KH, int KW,
                      int stride, int pad, const Epilogue& ep, const Split& sp, hipStream_t s);
 
