@@ -387,7 +387,7 @@ void k_gemm(GemmArgs a) {
 
 // ------------------------------------------------------------------ few input channels
 
-// Convolutions whose input has fewer than 8 channels (the ResNet stem: 7 x 7, stride 2,
+// Convolutions whose input has at most 4 channels (the ResNet stem: 7 x 7, stride 2,
 // 3 channels), where an im2col row is not made of 16-byte runs. A workgroup owns all
 // (<= 64) output channels and SC_W consecutive output pixels of `rows` output rows of one
 // sample. The weights are brought in once per workgroup as 16-byte loads of the flat
