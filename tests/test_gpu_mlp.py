@@ -51,8 +51,10 @@ def test_mlp_bf16_blocked_weights(batch):
     rt.close()
 
 
-@pytest.mark.parametrize("act", ["relu", "none"])
+@pytest.mark.parametrize("act", ["relu", "none", "gelu"])
 def test_mlp_f32_acts(act):
+    # gelu: the kernels' fp32 erf (Abramowitz-Stegun 7.1.26, |error| <= 1.5e-7) against the
+    # oracle's exact one at the fp32 tolerance
     m = synth.mlp(2, 264, "f32", act, seed=3, bias_std=0.1)
     x = synth.mlp_input(3, 264, "f32", 4)
     rt, (mid,) = make_runtime([m], batch_max=3)
