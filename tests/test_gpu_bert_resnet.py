@@ -57,7 +57,7 @@ def test_cfg4_full(batch):
     rt.close()
 
 
-@pytest.mark.parametrize("image,batch", [(32, 1), (64, 3)])
+@pytest.mark.parametrize("image,batch", [(32, 1), (64, 3), (96, 2), (160, 1)])
 def test_resnet_small_images(image, batch):
     m = synth.resnet50(seed=51, classes=10, image=image)
     x = synth.resnet_input(batch, 52, image=image)
