@@ -1,4 +1,6 @@
 """Helpers shared by the GPU tests: run a synthetic model through the C ABI and compare."""
+import json
+import os
 import sys
 
 import numpy as np
@@ -56,11 +58,30 @@ def infer(rt, mid, model, x_np, stream=None):
     return out.cpu().numpy()
 
 
+# every parity check appends its achieved error here (one JSON object per line), so a GPU
+# run leaves a record of the errors behind its pass/fail verdicts
+PARITY_LOG = os.environ.get("TP_PARITY_LOG", os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(
+    __file__))), "gpurun_out", "parity_errors.jsonl"))
+
+
+def record_parity(model, batch, err, tol):
+    rec = {"test": os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0], "arch": model.arch,
+           "dtype": model.dtype, "dims": {k: v for k, v in model.dims.items() if isinstance(v, (int, str))},
+           "batch": int(batch), "max_normwise_error": float(err), "tol": tol}
+    try:
+        os.makedirs(os.path.dirname(PARITY_LOG), exist_ok=True)
+        with open(PARITY_LOG, "a") as f:
+            f.write(json.dumps(rec) + "\n")
+    except OSError as e:          # a read-only tree must not fail the check itself
+        log(f"  (parity record not written: {e})")
+
+
 def check_parity(got, model, x_np, tol):
     ref = oracle_forward.forward(model, x_np)
     err = oracle_forward.normwise_error(got, ref)
     log(f"  normwise error per sample: max {err.max():.3e} (tol {tol})")
     assert np.all(np.isfinite(got)), "non-finite output"
+    record_parity(model, x_np.shape[0], err.max(), tol)
     assert err.max() <= tol, (err.max(), tol)
     return err
 

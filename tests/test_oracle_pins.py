@@ -273,3 +273,47 @@ def test_oracle_fp32_matches_fp64(cfg):
     err = forward.normwise_error(y32, y64).max()
     assert err <= 1e-5, err
     m.drop_blob()
+
+
+# ---------------------------------------------------------------- the parity metric
+
+def test_normwise_error_hand_computed():
+    # Reading of "max relative error" for whole outputs: per sample (first axis),
+    # ||got - ref||_inf / ||ref||_inf. Values below are worked by hand.
+    ref = np.array([[1.0, -4.0, 2.0],          # sample 0: ||ref||_inf = 4 (a negative entry)
+                    [0.5, 0.25, -0.125]])      # sample 1: ||ref||_inf = 0.5
+    got = np.array([[1.5, -4.0, 2.0],          # |diff| max 0.5  -> 0.5 / 4   = 0.125
+                    [0.5, 0.0, -0.125]])       # |diff| max 0.25 -> 0.25 / 0.5 = 0.5
+    err = forward.normwise_error(got, ref)
+    assert err.shape == (2,)
+    assert err.tolist() == [0.125, 0.5]
+    # a per-tensor denominator (4 for both samples) would give 0.0625 for sample 1,
+    # and a signed maximum of ref (2 for sample 0) would give 0.25 for sample 0
+    assert err[1] != 0.25 / 4.0 and err[0] != 0.5 / 2.0
+    # errors of opposite sign count by magnitude: got below ref by 1 in sample 0
+    got2 = ref.copy()
+    got2[0, 1] = -5.0
+    assert forward.normwise_error(got2, ref).tolist() == [0.25, 0.0]
+    # exact agreement is exactly zero
+    assert forward.normwise_error(ref, ref).tolist() == [0.0, 0.0]
+
+
+def test_normwise_error_flattens_all_but_the_sample_axis():
+    # [2][2][3] outputs (a BERT-like [batch][seq][d]); each sample's norm is over all its
+    # elements, not per row. Sample 0: ||ref|| = 8, largest |diff| 2 -> 0.25. Sample 1:
+    # ||ref|| = 3 (at -3), largest |diff| 0.75 in its second row -> 0.25.
+    ref = np.zeros((2, 2, 3))
+    ref[0, 0] = [8.0, 1.0, 1.0]
+    ref[0, 1] = [1.0, 1.0, 1.0]
+    ref[1, 0] = [1.0, -3.0, 1.0]
+    ref[1, 1] = [0.5, 0.5, 0.5]
+    got = ref.copy()
+    got[0, 1, 2] += 2.0
+    got[1, 1, 0] -= 0.75
+    assert forward.normwise_error(got, ref).tolist() == [0.25, 0.25]
+    # a per-row reading would have divided sample 0's error by 1 (its second row's norm)
+    # and sample 1's by 0.5
+    assert forward.normwise_error(got.reshape(4, 3), ref.reshape(4, 3)).tolist() == [0.0, 2.0, 0.0, 1.5]
+    # float32 inputs (the GPU's outputs) are widened before the difference
+    g32 = np.float32(1.0) + np.float32(2.0 ** -23)
+    assert forward.normwise_error(np.array([[g32]], np.float32), np.array([[1.0]])).tolist() == [2.0 ** -23]
