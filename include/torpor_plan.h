@@ -67,8 +67,10 @@ TP_API tp_status tph_rrc(uint64_t n, uint64_t m, double p, double* out);
 TP_API tp_status tph_sched_pick(uint32_t n_funcs, const uint64_t* n, const uint64_t* m, double p, double alpha,
                          uint32_t n_pending, const int32_t* pending_func, int32_t* pick, uint8_t* high_out);
 
-/* One step of the alpha auto-configuration: alpha * scalar (at most 1) if new_ratio - last_ratio
- * > |threshold|, alpha / scalar if it is < -|threshold|, else alpha. scalar > 1. */
+/* One period of the alpha auto-configuration (appendix "Function request prioritization"):
+ * *out = min(alpha * scalar^d, 1), where d is +1 when the compliant share rose by more than
+ * |threshold| (new_ratio - last_ratio), -1 when it fell by more than |threshold|, else 0.
+ * alpha in (0, 1], scalar > 1; TP_E_INVAL otherwise. */
 TP_API tp_status tph_alpha_update(double alpha, double last_ratio, double new_ratio, double scalar, double threshold,
                            double* out);
 

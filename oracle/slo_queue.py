@@ -10,9 +10,10 @@ request prioritization":
   integer with sum_{j<=k} max(RRC_j, 0) <= alpha * sum_i max(RRC_i, 0).
 * Requests of the high-priority group run first, in reverse order of RRC (largest first);
   those of the low-priority group in order of RRC (smallest first).
-* alpha is adjusted periodically from the ratio of SLO-compliant functions: multiplied by
-  `scalar` (at most 1) when the ratio rose by more than |threshold| since the last period,
-  divided by `scalar` when it fell by more than |threshold|, otherwise kept.
+* alpha is adjusted periodically from the share of SLO-compliant functions, in the manner
+  of TCP congestion control (the appendix's alpha auto-configuration): a rise of the share
+  by more than |threshold| since the last period grows alpha by the factor `scalar`, a fall
+  by more than |threshold| shrinks it by the same factor, and alpha never exceeds 1.
 
 Readings where the paper is silent: ties in RRC go to the lower function index, both when
 sorting and when choosing; within a function, requests run in arrival order; the sums run
@@ -54,9 +55,7 @@ def pick(rrcs, high, pending_func):
 
 def alpha_update(alpha: float, last_ratio: float, new_ratio: float, scalar: float = 2.0,
                  threshold: float = 0.04) -> float:
+    band = abs(threshold)
     change = new_ratio - last_ratio
-    if change > abs(threshold):
-        return min(alpha * scalar, 1.0)
-    if change < -abs(threshold):
-        return alpha / scalar
-    return alpha
+    direction = (change > band) - (change < -band)     # +1 grow, -1 shrink, 0 hold
+    return min(alpha * scalar ** direction, 1.0)

@@ -50,10 +50,11 @@ int32_t sched_pick(const std::vector<double>& r, const std::vector<uint8_t>& hig
 }
 
 double alpha_update(double alpha, double last_ratio, double new_ratio, double scalar, double threshold) {
-  const double d = new_ratio - last_ratio, t = std::fabs(threshold);
-  if (d > t) return std::min(alpha * scalar, 1.0);
-  if (d < -t) return alpha / scalar;
-  return alpha;
+  // TCP-like: the change in the compliant share, outside a dead band of +-|threshold|, sets
+  // the direction; alpha moves one factor of `scalar` that way and stays at most 1
+  const double band = std::fabs(threshold), change = new_ratio - last_ratio;
+  const int direction = (change > band) - (change < -band);
+  return std::min(alpha * std::pow(scalar, direction), 1.0);
 }
 
 }  // namespace tp

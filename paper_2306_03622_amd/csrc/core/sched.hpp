@@ -26,9 +26,10 @@ std::vector<uint8_t> high_group(const std::vector<double>& rrc, double alpha);
 int32_t sched_pick(const std::vector<double>& rrc, const std::vector<uint8_t>& high,
                    const std::vector<int32_t>& pending_func);
 
-// Periodic alpha update: multiply by scalar (capped at 1) when the ratio of SLO-compliant
-// functions rose by more than |threshold| since the last period, divide by scalar when it fell
-// by more than |threshold|, else keep it.
+// The periodic alpha auto-configuration (appendix "Function request prioritization", the
+// algorithm of that name): when the share of SLO-compliant functions moved by more than
+// |threshold| since the last period, alpha is scaled by scalar in the direction of the move
+// (up when compliance improved, down when it worsened), never above 1; otherwise unchanged.
 double alpha_update(double alpha, double last_ratio, double new_ratio, double scalar, double threshold);
 
 }  // namespace tp
