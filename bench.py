@@ -27,14 +27,6 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-# Overlapping the swap with the forward pass needs the copy stream and the request's stream
-# on different hardware queues. HIP spreads a process's streams over GPU_MAX_HW_QUEUES
-# queues (4 by default), and with torch's streams in the same process some contexts then
-# land in an arrangement where chunk copies and layer kernels execute in lockstep (measured:
-# BERT-base cold 4.8-5.0 ms instead of 4.0 ms in about one context in ten); with 8 queues
-# none did. It must be set before the HIP runtime starts, so before torch is imported.
-os.environ.setdefault("GPU_MAX_HW_QUEUES", "8")
-
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 PCIE5_X16_GBS = 63.0

@@ -105,7 +105,9 @@ enum {
   TP_FLAG_PER_TENSOR = 16,/* transfer groups close at tensor boundaries, not layer boundaries;
                            * with chunk_min_bytes = 0 every tensor is its own transfer (the
                            * parameter-level pipeline of Sec. 6.1) */
-  TP_FLAG_TRACE = 32      /* cold requests record timing events per chunk (tp_last_timeline) */
+  TP_FLAG_TRACE = 32,     /* cold requests record timing events per chunk (tp_last_timeline) */
+  TP_FLAG_CALLER_STREAM = 64 /* cold requests run their kernels on the caller's stream instead
+                              * of the library's execution stream (see tp_config) */
 };
 
 /* Context configuration. arena_dev/work_dev are caller-owned device buffers that must
@@ -124,8 +126,14 @@ enum {
  * host-mapped pinned memory with gather_wgs workgroups (0 = default). throttle_us:
  * delay per chunk under TP_FLAG_THROTTLE. Warm requests of models whose forward pass
  * launches at least 16 kernels replay an instantiated HIP graph of it, cached per (model,
- * batch, input, output), unless TP_FLAG_NO_GRAPH is set; shorter forward passes are
- * launched kernel by kernel, which is faster for them. direct_max_bytes (0 = never): a cold request for a model of
+ * batch, extent, workspace; up to 4 per model), unless TP_FLAG_NO_GRAPH is set; a request
+ * whose input or output buffer differs from the graph's repoints the graph's kernels that
+ * read the input or write the output (no new capture); shorter forward passes are
+ * launched kernel by kernel, which is faster for them. A cold request's kernels run on an
+ * execution stream the library creates (with a hardware queue of its own, like the copy
+ * streams), forked from the caller's stream by an event and joined back to it by another;
+ * so whatever hardware queue the caller's stream maps to, the chunk copies overlap the
+ * kernels (TP_FLAG_CALLER_STREAM: on the caller's stream instead). direct_max_bytes (0 = never): a cold request for a model of
  * at most this many bytes runs its kernels on the pinned host copy over the host link
  * (direct host access, the alternative to swapping that Sec. 8 cites) instead of waiting
  * for its first chunk, and the copy stream swaps the model in behind it; the next request
@@ -210,6 +218,9 @@ typedef struct {
   uint64_t admit_calls, admit_ns_total, admit_ns_max;
   uint32_t partitions, partitions_free;   /* TP_ALLOC_PARTITION*: partitions in all, unoccupied */
   uint64_t evacuations, bytes_moved;      /* TP_ALLOC_PARTITION_CONSOLIDATE: partitions freed by moves, bytes moved */
+  /* warm-request graphs: forward passes captured and instantiated, and graph launches whose
+   * kernel nodes were repointed at a request's input and output buffers instead */
+  uint64_t graph_captures, graph_repoints;
 } tp_arena_stats_t;
 
 typedef struct {
@@ -370,6 +381,13 @@ TP_API tp_status tp_run_trace_sched(struct tp_ctx* ctx, const tp_request* reques
                                     const tp_sched_config* cfg, const uint64_t* deadline_ns,
                                     tp_request_result* results, tp_sched_stats* stats);
 
+/* Test hook for the error paths (fault handling is Sec. 4.5's concern; this checks the
+ * library's own rollback): the nth copy the context enqueues from now on (1 = the next;
+ * chunk copies of swaps and consolidation moves) fails as if the HIP runtime had rejected
+ * it, with nothing enqueued for it; 0 disarms. The request then fails like any enqueue
+ * failure: TP_E_HIP, the model left non-resident, its extent retired. Host-side only: no
+ * device work fails. Errors: TP_E_INVAL (NULL context, nth < 0). */
+TP_API tp_status tp_debug_fail_copy(struct tp_ctx* ctx, int32_t nth);
 /* Thread-local message describing the last non-OK status ("" if none). */
 TP_API const char* tp_last_error(void);
 

@@ -16,10 +16,12 @@
 
 using namespace tp;
 
+thread_local std::vector<tp::k::LaunchRecord>* tp::k::launch_log = nullptr;
+
 namespace {
 
-tp_status hip_fail(hipError_t e, const char* what) {
-  return fail(TP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+tp_status hip_fail(hipError_t e, const std::string& what) {
+  return fail(TP_E_HIP, what + ": " + hipGetErrorString(e));
 }
 
 #define TP_HIP(call)                                  \
@@ -60,6 +62,9 @@ hipError_t sync_copies(tp_ctx* c) {
 
 void destroy_streams(tp_ctx* c) {
   if (c->own_copy && c->copy[0]) (void)hipStreamDestroy(c->copy[0]);
+  if (c->exec) (void)hipStreamDestroy(c->exec);
+  if (c->exec_fork) (void)hipEventDestroy(c->exec_fork);
+  if (c->exec_join) (void)hipEventDestroy(c->exec_join);
   if (c->copy[1]) (void)hipStreamDestroy(c->copy[1]);
   if (c->capture) (void)hipStreamDestroy(c->capture);
   if (c->req_done) (void)hipEventDestroy(c->req_done);
@@ -73,19 +78,28 @@ void destroy_streams(tp_ctx* c) {
     if (e) (void)hipEventDestroy(e);
 }
 
-k::Split make_split(tp_ctx* c, const Model* m, int batch) {
+k::Split make_split(char* work, const Model* m, int batch) {
   k::Split sp;
   if (m->spec.dtype != TP_BF16) return sp;
-  sp.partials = reinterpret_cast<float*>(c->work + activation_bytes(m->spec, batch));
+  sp.partials = reinterpret_cast<float*>(work + activation_bytes(m->spec, batch));
   sp.partial_bytes = kSplitScratch;
   return sp;
 }
 
+void destroy_graph(GraphEntry& g) {
+  if (g.exec) (void)hipGraphExecDestroy(g.exec);
+  if (g.graph) (void)hipGraphDestroy(g.graph);
+  g.exec = nullptr;
+  g.graph = nullptr;
+}
+
 void drop_graphs(Model* m) {
-  for (auto& g : m->graphs)
-    if (g.exec) (void)hipGraphExecDestroy(g.exec);
+  for (auto& g : m->graphs) destroy_graph(g);
   m->graphs.clear();
 }
+
+// tp_debug_fail_copy: true when the copy about to be enqueued is the one chosen to fail
+bool injected_failure(tp_ctx* c) { return c->fail_copy > 0 && --c->fail_copy == 0; }
 
 void free_model(Model* m) {
   drop_graphs(m);
@@ -129,6 +143,7 @@ tp_status claim(tp_ctx* c, uint64_t off, uint64_t len) {
 
 // Enqueues the copy of chunk i of `m` into the extent at arena offset `off`, then its event.
 hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
+  if (injected_failure(c)) return hipErrorInvalidValue;     // nothing enqueued for this chunk
   const size_t n = m->chunks.size();
   const int ns = (c->ncopy == 2 && n > 1) ? 2 : 1;
   hipError_t e = hipSuccess;
@@ -152,8 +167,10 @@ hipError_t enqueue_chunk(tp_ctx* c, const Model* m, uint64_t off, size_t i) {
     else
       e = hipMemcpyAsync(dst, static_cast<char*>(m->host) + ch.begin, nb, hipMemcpyHostToDevice, s);
   }
-  if (e == hipSuccess) e = hipEventRecord(m->chunk_ev[i], s);
+  // the traced end precedes the chunk's event, so that a kernel released by that event
+  // starts after the recorded end
   if (e == hipSuccess && traced) e = hipEventRecord(c->tl.copy_end[i], s);
+  if (e == hipSuccess) e = hipEventRecord(m->chunk_ev[i], s);
   return e;
 }
 
@@ -168,6 +185,7 @@ tp_status move_extent(tp_ctx* c, Model* x, uint64_t from, uint64_t to) {
   tp_status s = claim(c, to, len);
   if (s != TP_OK) return s;
   const size_t n = x->chunk_ev.size();
+  if (injected_failure(c)) return hip_fail(hipErrorInvalidValue, "consolidation move (injected)");
   TP_HIP(hipStreamWaitEvent(c->copy[0], x->chunk_ev[n - 1], 0));
   if (c->ncopy == 2 && n > 1) TP_HIP(hipStreamWaitEvent(c->copy[0], x->chunk_ev[n - 2], 0));
   TP_HIP(hipMemcpyAsync(c->arena + to, c->arena + from, x->spec.host_bytes, hipMemcpyDeviceToDevice, c->copy[0]));
@@ -183,7 +201,6 @@ tp_status move_extent(tp_ctx* c, Model* x, uint64_t from, uint64_t to) {
 tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   const auto t0 = std::chrono::steady_clock::now();
   Arena::Decision d = c->policy->request(m->id);
-  if (!d.placed) return fail(TP_E_NOSPC, "model cannot be placed in the arena");
   *swapped = !d.hit;
   if (d.hit) return ok();
   struct Timer {              // host time of this (missing) admission, on every return path
@@ -200,10 +217,13 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
   } timer{c, t0};
   m->bg_pending = false;         // a new swap supersedes an earlier one
   tp_status s = TP_OK;
-  for (const auto& st : d.steps) {         // in the order the arena made them
+  // the arena's victims and moves, in the order it made them; also when it then found no
+  // placement, so that the extents it invalidated are retired like any other
+  for (const auto& st : d.steps) {
     if (s != TP_OK) break;
     s = st.move ? move_extent(c, find(c, st.id), st.from, st.to) : retire(c, st.id, st.from, c->policy->bytes(st.id));
   }
+  if (s == TP_OK && !d.placed) return fail(TP_E_NOSPC, "model cannot be placed in the arena");
   if (s == TP_OK) s = claim(c, d.offset, m->spec.host_bytes);
   if (s != TP_OK) {
     const std::string msg = last_error();
@@ -213,8 +233,10 @@ tp_status admit(tp_ctx* c, Model* m, bool* swapped) {
       (void)retire(c, mv.id, mv.from, len);
       (void)retire(c, mv.id, mv.to, len);
     }
-    c->policy->evict(m->id);
-    (void)retire(c, m->id, d.offset, m->spec.host_bytes);
+    if (d.placed) {
+      c->policy->evict(m->id);
+      (void)retire(c, m->id, d.offset, m->spec.host_bytes);
+    }
     return fail(s, msg);
   }
   return ok();
@@ -244,10 +266,11 @@ hipError_t run_forward(ExecCtx& x) {
   return hipErrorInvalidValue;
 }
 
-// Warm request: replay the model's forward pass as one graph launch. The graph is
-// captured from the same kernel sequence (on a private stream, nothing executes) the
-// first time a (batch, input, output, extent) combination is seen; up to kGraphs
-// combinations stay instantiated per model. If capture fails the model falls back to
+// Warm request: replay the model's forward pass as one graph launch. A graph is captured
+// from the same kernel sequence (on a private stream, nothing executes) the first time a
+// (batch, extent, workspace) combination is seen; up to kGraphs combinations stay
+// instantiated per model. A request with other input or output buffers than the graph's
+// nodes hold repoints those nodes in place. If capture fails the model falls back to
 // launching its kernels one by one, which computes the same bits.
 constexpr size_t kGraphs = 4;
 
@@ -264,39 +287,139 @@ int forward_launches(const ModelSpec& s) {
   }
 }
 
-hipError_t launch_graph(tp_ctx* c, Model* m, char* base, const void* in, int batch, void* out, hipStream_t stream) {
+// The kernel nodes of a captured single-stream graph in launch order: the graph must be one
+// chain of `n` kernel nodes whose kernels are those of the recorded launches.
+bool chain_nodes(hipGraph_t g, const std::vector<k::LaunchRecord>& rec, std::vector<hipGraphNode_t>* out) {
+  size_t n = 0;
+  if (hipGraphGetRootNodes(g, nullptr, &n) != hipSuccess || n != 1) return false;
+  hipGraphNode_t cur = nullptr;
+  if (hipGraphGetRootNodes(g, &cur, &n) != hipSuccess) return false;
+  out->clear();
+  while (cur) {
+    hipGraphNodeType t;
+    if (hipGraphNodeGetType(cur, &t) != hipSuccess || t != hipGraphNodeTypeKernel) return false;
+    if (out->size() >= rec.size()) return false;
+    hipKernelNodeParams p{};
+    if (hipGraphKernelNodeGetParams(cur, &p) != hipSuccess || p.func != rec[out->size()].func) return false;
+    out->push_back(cur);
+    size_t nd = 0;
+    if (hipGraphNodeGetDependentNodes(cur, nullptr, &nd) != hipSuccess || nd > 1) return false;
+    hipGraphNode_t next = nullptr;
+    if (nd == 1 && hipGraphNodeGetDependentNodes(cur, &next, &nd) != hipSuccess) return false;
+    cur = nd == 1 ? next : nullptr;
+  }
+  return out->size() == rec.size();
+}
+
+// Points the graph's nodes that held the captured request's input and output at `in` and
+// `out`: each such kernel's recorded arguments with those two addresses replaced.
+hipError_t repoint(GraphEntry& g, const void* in, void* out) {
+  for (uint32_t i : g.io) {
+    const k::LaunchRecord& r = g.launches[i];
+    std::vector<uint8_t> b = r.bytes;
+    for (uint32_t at : r.ptr_at) {
+      uintptr_t v;
+      std::memcpy(&v, b.data() + at, sizeof v);
+      if (v == (uintptr_t)g.cap_in) v = (uintptr_t)in;
+      else if (v == (uintptr_t)g.cap_out) v = (uintptr_t)out;
+      else continue;
+      std::memcpy(b.data() + at, &v, sizeof v);
+    }
+    std::vector<void*> argv(r.arg_at.size());
+    for (size_t j = 0; j < argv.size(); ++j) argv[j] = b.data() + r.arg_at[j];
+    hipKernelNodeParams p{};
+    p.func = const_cast<void*>(r.func);
+    p.gridDim = r.grid;
+    p.blockDim = r.block;
+    p.sharedMemBytes = r.shmem;
+    p.kernelParams = argv.data();
+    p.extra = nullptr;
+    const hipError_t e = hipGraphExecKernelNodeSetParams(g.exec, g.nodes[i], &p);
+    if (e != hipSuccess) return e;
+  }
+  g.cur_in = in;
+  g.cur_out = out;
+  return hipSuccess;
+}
+
+// Captures and instantiates the forward pass of `m` into `g` (its key fields set).
+hipError_t capture_graph(tp_ctx* c, Model* m, GraphEntry& g) {
+  Waiter w;
+  w.m = m;
+  char* base = const_cast<char*>(g.base);
+  char* work = const_cast<char*>(g.work);
+  ExecCtx x{m, base, work, g.cap_in, g.cap_out, g.batch, c->capture, &w, make_split(work, m, g.batch)};
+  g.launches.clear();
+  k::launch_log = &g.launches;
+  hipError_t e = hipStreamBeginCapture(c->capture, hipStreamCaptureModeThreadLocal);
+  if (e == hipSuccess) {
+    hipError_t er = run_forward(x);
+    e = hipStreamEndCapture(c->capture, &g.graph);
+    if (er != hipSuccess) e = er;
+  }
+  k::launch_log = nullptr;
+  if (e == hipSuccess) e = hipGraphInstantiate(&g.exec, g.graph, nullptr, nullptr, 0);
+  if (e != hipSuccess) {
+    destroy_graph(g);
+    return e;
+  }
+  ++c->graph_captures;
+  g.cur_in = g.cap_in;
+  g.cur_out = g.cap_out;
+  g.patchable = chain_nodes(g.graph, g.launches, &g.nodes);
+  g.io.clear();
+  for (uint32_t i = 0; g.patchable && i < g.launches.size(); ++i) {
+    const k::LaunchRecord& r = g.launches[i];
+    for (uint32_t at : r.ptr_at) {
+      uintptr_t v;
+      std::memcpy(&v, r.bytes.data() + at, sizeof v);
+      if (v == (uintptr_t)g.cap_in || v == (uintptr_t)g.cap_out) {
+        g.io.push_back(i);
+        break;
+      }
+    }
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_graph(tp_ctx* c, Model* m, char* base, char* work, const void* in, int batch, void* out,
+                        hipStream_t stream) {
   GraphEntry* hit = nullptr;
   for (auto& g : m->graphs)
-    if (g.batch == batch && g.in == in && g.out == out && g.base == base) hit = &g;
-  if (!hit) {
-    Waiter w;
-    w.m = m;
-    ExecCtx x{m, base, c->work, in, out, batch, c->capture, &w, make_split(c, m, batch)};
-    hipGraph_t graph = nullptr;
-    hipGraphExec_t exec = nullptr;
-    hipError_t e = hipStreamBeginCapture(c->capture, hipStreamCaptureModeThreadLocal);
+    if (g.batch == batch && g.base == base && g.work == work) hit = &g;
+  if (hit && (hit->cur_in != in || hit->cur_out != out)) {
+    hipError_t e = hit->patchable ? repoint(*hit, in, out) : hipErrorNotSupported;
     if (e == hipSuccess) {
-      hipError_t er = run_forward(x);
-      e = hipStreamEndCapture(c->capture, &graph);
-      if (er != hipSuccess) e = er;
+      ++c->graph_repoints;
+    } else {
+      (void)hipGetLastError();
+      destroy_graph(*hit);                 // captured again below, for these buffers
+      m->graphs.erase(m->graphs.begin() + (hit - m->graphs.data()));
+      hit = nullptr;
     }
-    if (e == hipSuccess) e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
-    if (graph) (void)hipGraphDestroy(graph);
-    if (e != hipSuccess) {
+  }
+  if (!hit) {
+    if (m->graphs.size() >= kGraphs) {
+      auto oldest = std::min_element(m->graphs.begin(), m->graphs.end(),
+                                     [](const GraphEntry& a, const GraphEntry& b) { return a.stamp < b.stamp; });
+      destroy_graph(*oldest);
+      m->graphs.erase(oldest);
+    }
+    GraphEntry g;
+    g.batch = batch;
+    g.base = base;
+    g.work = work;
+    g.cap_in = in;
+    g.cap_out = out;
+    if (capture_graph(c, m, g) != hipSuccess) {
       (void)hipGetLastError();
       m->graph_failed = true;
       Waiter w2;
       w2.m = m;
-      ExecCtx x2{m, base, c->work, in, out, batch, stream, &w2, make_split(c, m, batch)};
+      ExecCtx x2{m, base, work, in, out, batch, stream, &w2, make_split(work, m, batch)};
       return run_forward(x2);
     }
-    if (m->graphs.size() >= kGraphs) {
-      auto oldest = std::min_element(m->graphs.begin(), m->graphs.end(),
-                                     [](const GraphEntry& a, const GraphEntry& b) { return a.stamp < b.stamp; });
-      (void)hipGraphExecDestroy(oldest->exec);
-      m->graphs.erase(oldest);
-    }
-    m->graphs.push_back({batch, in, out, base, exec, 0});
+    m->graphs.push_back(std::move(g));
     hit = &m->graphs.back();
   }
   hit->stamp = ++c->graph_clock;
@@ -340,6 +463,122 @@ tp_status check_request(tp_ctx* c, int32_t id, Model** out) {
                                 std::to_string(c->cfg.arena_bytes) + " bytes");
   *out = m;
   return ok();
+}
+
+// One request (tp_infer and its variants), with the workspace `work` of `work_bytes`.
+tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, void* output_dev,
+                        hipStream_t stream, char* work, uint64_t work_bytes, const char* who) {
+  Model* m = nullptr;
+  tp_status s = check_request(c, id, &m);
+  if (s != TP_OK) return s;
+  if (batch < 1 || !input_dev || !output_dev) return fail(TP_E_INVAL, std::string(who) + ": batch < 1 or NULL buffer");
+  const uint64_t need = workspace_bytes(m->spec, batch);
+  if (need > work_bytes)
+    return fail(TP_E_NOSPC, std::string(who) + ": workspace of " + std::to_string(work_bytes) + " bytes, need " +
+                                std::to_string(need));
+  if ((s = begin_request(c, stream)) != TP_OK) return s;
+  if (c->cfg.copy_method == TP_COPY_ZERO && !c->policy->resident(id)) {
+    // direct host access: the kernels read the weights from the pinned host copy
+    Waiter w;
+    w.m = m;
+    ExecCtx x{m, static_cast<char*>(m->host_dev), work, input_dev, output_dev, batch, stream, &w,
+              make_split(work, m, batch)};
+    hipError_t e = run_forward(x);
+    if (e != hipSuccess) {
+      (void)end_request(c, m, stream);
+      return hip_fail(e, std::string(who) + ": kernel launch");
+    }
+    return end_request(c, m, stream);
+  }
+  const bool direct = c->cfg.direct_max_bytes && m->spec.host_bytes <= c->cfg.direct_max_bytes &&
+                      !c->policy->resident(id) && c->ncopy == 1 &&
+                      (c->cfg.copy_method == TP_COPY_MEMCPY || c->cfg.copy_method == TP_COPY_GATHER);
+  bool swapped = false;
+  if ((s = admit(c, m, &swapped)) != TP_OK) return s;
+  const uint64_t off = c->policy->offset(id);
+  const bool graphs =
+      !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed && forward_launches(m->spec) >= kGraphMinLaunches;
+  // a swapping request's kernels run on the library's execution stream (see tp_create)
+  const bool forked = swapped && !direct && c->exec;
+  hipError_t e = swapped ? hipSuccess : settle(m, stream);
+  if (e != hipSuccess) {
+    // fall through to the failure handling below
+  } else if (direct) {
+    // The request's kernels read the host copy and own the host link while they run; the
+    // swap is enqueued after the request's completion event, on the copy stream that
+    // waits for it, so neither the link nor (when the runtime maps both streams onto one
+    // hardware queue) the caller's synchronisation waits for the copy.
+    char* host = static_cast<char*>(m->host_dev);
+    if (graphs) {
+      e = launch_graph(c, m, host, work, input_dev, batch, output_dev, stream);
+    } else {
+      Waiter w;
+      w.m = m;
+      ExecCtx x{m, host, work, input_dev, output_dev, batch, stream, &w, make_split(work, m, batch)};
+      e = run_forward(x);
+    }
+    if (e == hipSuccess && (s = end_request(c, m, stream)) == TP_OK) {
+      Waiter bg;
+      bg.m = m;
+      bg.ctx = c;
+      bg.base_off = off;
+      e = hipStreamWaitEvent(c->copy[0], c->req_done, 0);
+      if (e == hipSuccess) e = bg.issue_through((int)m->chunks.size() - 1);
+      if (e == hipSuccess) {
+        m->bg_pending = true;
+        return ok();
+      }
+      c->policy->evict(id);
+      (void)retire(c, id, off, m->spec.host_bytes);
+      return hip_fail(e, std::string(who) + ": swap enqueue");
+    }
+    if (s != TP_OK) {
+      c->policy->evict(id);
+      (void)retire(c, id, off, m->spec.host_bytes);
+      return s;
+    }
+  } else if (!swapped && graphs) {
+    e = launch_graph(c, m, c->arena + off, work, input_dev, batch, output_dev, stream);
+  } else {
+    const hipStream_t xs = forked ? c->exec : stream;
+    Waiter w;
+    w.m = m;
+    w.stream = xs;
+    w.swapping = swapped;
+    w.ctx = c;
+    w.base_off = off;
+    ExecCtx x{m, c->arena + off, work, input_dev, output_dev, batch, xs, &w, make_split(work, m, batch)};
+    if (swapped && (c->cfg.flags & TP_FLAG_TRACE)) {
+      c->tl.active = true;
+      c->tl.valid = false;
+      c->tl.n = (uint32_t)m->chunks.size();
+      e = hipEventRecord(c->tl.start, stream);
+    }
+    if (e == hipSuccess && forked) {
+      e = hipEventRecord(c->exec_fork, stream);
+      if (e == hipSuccess) e = hipStreamWaitEvent(c->exec, c->exec_fork, 0);
+    }
+    // swap, then execute: every chunk is waited for before the first kernel
+    if (e == hipSuccess && swapped && (c->cfg.flags & TP_FLAG_SERIAL)) e = w.need(m->spec.n_layers - 1);
+    if (e == hipSuccess) e = run_forward(x);
+    // every layer asks for its chunk; issue any the forward pass did not reach
+    if (e == hipSuccess && swapped) e = w.issue_through((int)m->chunks.size() - 1);
+    if (forked) {
+      // join whatever was enqueued on the execution stream, also after a failure, so that
+      // the request's completion (and the model's last use) covers it
+      hipError_t ej = hipEventRecord(c->exec_join, c->exec);
+      if (ej == hipSuccess) ej = hipStreamWaitEvent(stream, c->exec_join, 0);
+      if (e == hipSuccess) e = ej;
+    }
+  }
+  if (e != hipSuccess) {
+    // keep the ordering intact, then leave the model non-resident
+    (void)end_request(c, m, stream);
+    c->policy->evict(id);
+    (void)retire(c, id, off, m->spec.host_bytes);
+    return hip_fail(e, std::string(who) + ": enqueue");
+  }
+  return end_request(c, m, stream);
 }
 
 }  // namespace
@@ -389,6 +628,14 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
     c->own_copy = e == hipSuccess;
   }
   if (e == hipSuccess && c->ncopy == 2) e = create_copy_stream(c->device, &c->copy[1]);
+  if (e == hipSuccess && !(cfg->flags & TP_FLAG_CALLER_STREAM)) {
+    // the execution stream of swapping requests: a hardware queue of its own, like the copy
+    // streams, so that whatever queue the caller's stream lands on, chunk copies and layer
+    // kernels are never serialised behind each other in one queue
+    e = create_copy_stream(c->device, &c->exec);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->exec_fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->exec_join, hipEventDisableTiming);
+  }
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming);
@@ -405,6 +652,7 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
 tp_status tp_destroy(tp_ctx* c) {
   if (!c) return fail(TP_E_INVAL, "NULL context");
   hipError_t e = sync_copies(c);
+  if (e == hipSuccess && c->exec) e = hipStreamSynchronize(c->exec);
   if (e == hipSuccess && c->any_request) e = hipEventSynchronize(c->req_done);
   for (auto& kv : c->models) {
     if (kv.second->used) (void)hipEventSynchronize(kv.second->last_use);
@@ -518,104 +766,9 @@ tp_status tp_unregister_model(tp_ctx* c, int32_t id) {
 }
 
 tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, void* output_dev, void* stream_) {
-  Model* m = nullptr;
-  tp_status s = check_request(c, id, &m);
-  if (s != TP_OK) return s;
-  if (batch < 1 || !input_dev || !output_dev) return fail(TP_E_INVAL, "tp_infer: batch < 1 or NULL buffer");
-  const uint64_t need = workspace_bytes(m->spec, batch);
-  if (need > c->cfg.work_bytes)
-    return fail(TP_E_NOSPC, "tp_infer: workspace of " + std::to_string(c->cfg.work_bytes) + " bytes, need " +
-                                std::to_string(need));
-  hipStream_t stream = static_cast<hipStream_t>(stream_);
-  if ((s = begin_request(c, stream)) != TP_OK) return s;
-  if (c->cfg.copy_method == TP_COPY_ZERO && !c->policy->resident(id)) {
-    // direct host access: the kernels read the weights from the pinned host copy
-    Waiter w;
-    w.m = m;
-    ExecCtx x{m, static_cast<char*>(m->host_dev), c->work, input_dev, output_dev, batch, stream, &w,
-              make_split(c, m, batch)};
-    hipError_t e = run_forward(x);
-    if (e != hipSuccess) {
-      (void)end_request(c, m, stream);
-      return hip_fail(e, "tp_infer: kernel launch");
-    }
-    return end_request(c, m, stream);
-  }
-  const bool direct = c->cfg.direct_max_bytes && m->spec.host_bytes <= c->cfg.direct_max_bytes &&
-                      !c->policy->resident(id) && c->ncopy == 1 &&
-                      (c->cfg.copy_method == TP_COPY_MEMCPY || c->cfg.copy_method == TP_COPY_GATHER);
-  bool swapped = false;
-  if ((s = admit(c, m, &swapped)) != TP_OK) return s;
-  const uint64_t off = c->policy->offset(id);
-  const bool graphs =
-      !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed && forward_launches(m->spec) >= kGraphMinLaunches;
-  hipError_t e = swapped ? hipSuccess : settle(m, stream);
-  if (e != hipSuccess) {
-    // fall through to the failure handling below
-  } else if (direct) {
-    // The request's kernels read the host copy and own the host link while they run; the
-    // swap is enqueued after the request's completion event, on the copy stream that
-    // waits for it, so neither the link nor (when the runtime maps both streams onto one
-    // hardware queue) the caller's synchronisation waits for the copy.
-    char* host = static_cast<char*>(m->host_dev);
-    if (graphs) {
-      e = launch_graph(c, m, host, input_dev, batch, output_dev, stream);
-    } else {
-      Waiter w;
-      w.m = m;
-      ExecCtx x{m, host, c->work, input_dev, output_dev, batch, stream, &w, make_split(c, m, batch)};
-      e = run_forward(x);
-    }
-    if (e == hipSuccess && (s = end_request(c, m, stream)) == TP_OK) {
-      Waiter bg;
-      bg.m = m;
-      bg.ctx = c;
-      bg.base_off = off;
-      e = hipStreamWaitEvent(c->copy[0], c->req_done, 0);
-      if (e == hipSuccess) e = bg.issue_through((int)m->chunks.size() - 1);
-      if (e == hipSuccess) {
-        m->bg_pending = true;
-        return ok();
-      }
-      c->policy->evict(id);
-      (void)retire(c, id, off, m->spec.host_bytes);
-      return hip_fail(e, "tp_infer: swap enqueue");
-    }
-    if (s != TP_OK) {
-      c->policy->evict(id);
-      (void)retire(c, id, off, m->spec.host_bytes);
-      return s;
-    }
-  } else if (!swapped && graphs) {
-    e = launch_graph(c, m, c->arena + off, input_dev, batch, output_dev, stream);
-  } else {
-    Waiter w;
-    w.m = m;
-    w.stream = stream;
-    w.swapping = swapped;
-    w.ctx = c;
-    w.base_off = off;
-    ExecCtx x{m, c->arena + off, c->work, input_dev, output_dev, batch, stream, &w, make_split(c, m, batch)};
-    if (swapped && (c->cfg.flags & TP_FLAG_TRACE)) {
-      c->tl.active = true;
-      c->tl.valid = false;
-      c->tl.n = (uint32_t)m->chunks.size();
-      e = hipEventRecord(c->tl.start, stream);
-    }
-    // swap, then execute: every chunk is waited for before the first kernel
-    if (swapped && (c->cfg.flags & TP_FLAG_SERIAL)) e = w.need(m->spec.n_layers - 1);
-    if (e == hipSuccess) e = run_forward(x);
-    // every layer asks for its chunk; issue any the forward pass did not reach
-    if (e == hipSuccess && swapped) e = w.issue_through((int)m->chunks.size() - 1);
-  }
-  if (e != hipSuccess) {
-    // keep the ordering intact, then leave the model non-resident
-    (void)end_request(c, m, stream);
-    c->policy->evict(id);
-    (void)retire(c, id, off, m->spec.host_bytes);
-    return hip_fail(e, "tp_infer: kernel launch");
-  }
-  return end_request(c, m, stream);
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  return infer_request(c, id, input_dev, batch, output_dev, static_cast<hipStream_t>(stream_), c->work,
+                       c->cfg.work_bytes, "tp_infer");
 }
 
 tp_status tp_swap_in(tp_ctx* c, int32_t id, void* stream_) {
@@ -683,6 +836,15 @@ tp_status tp_arena_stats(tp_ctx* c, tp_arena_stats_t* out) {
   out->admit_calls = c->admit_calls;
   out->admit_ns_total = c->admit_ns_total;
   out->admit_ns_max = c->admit_ns_max;
+  out->graph_captures = c->graph_captures;
+  out->graph_repoints = c->graph_repoints;
+  return ok();
+}
+
+tp_status tp_debug_fail_copy(tp_ctx* c, int32_t nth) {
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  if (nth < 0) return fail(TP_E_INVAL, "tp_debug_fail_copy: nth < 0");
+  c->fail_copy = nth;
   return ok();
 }
 

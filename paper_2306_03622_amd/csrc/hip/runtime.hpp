@@ -15,14 +15,25 @@
 
 namespace tp {
 
-// An instantiated graph of one warm forward pass: kernel arguments (weight, workspace,
-// input and output addresses, batch) are baked in, so it is keyed by all of them.
+// An instantiated graph of one warm forward pass of a model at one batch size, over one
+// arena extent and one workspace. Its kernels' arguments name the input and output buffers
+// of the request it was captured from; `launches` holds every kernel's recorded arguments, so
+// a later request with other buffers repoints the kernel nodes that hold those two addresses
+// in place (hipGraphExecKernelNodeSetParams) instead of capturing the pass again.
 struct GraphEntry {
   int batch = 0;
-  const void* in = nullptr;
-  void* out = nullptr;
   const char* base = nullptr;
+  const char* work = nullptr;
+  const void* cap_in = nullptr;   // buffers of the captured request
+  void* cap_out = nullptr;
+  const void* cur_in = nullptr;   // buffers the instantiated nodes hold now
+  void* cur_out = nullptr;
+  hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
+  std::vector<hipGraphNode_t> nodes;        // kernel nodes in launch order
+  std::vector<k::LaunchRecord> launches;    // the same launches as recorded at capture
+  std::vector<uint32_t> io;                 // launches whose arguments hold cap_in or cap_out
+  bool patchable = false;                   // nodes and records matched one to one
   uint64_t stamp = 0;
 };
 
@@ -109,6 +120,12 @@ struct tp_ctx {
   hipEvent_t fork = nullptr;                   // copy[1] starts a swap after copy[0]
   hipStream_t capture = nullptr;               // private stream for graph capture
   uint64_t graph_clock = 0;
+  uint64_t graph_captures = 0, graph_repoints = 0;
+  // cold (swapping) requests run on the library's execution stream, forked from and joined
+  // back to the caller's stream (null under TP_FLAG_CALLER_STREAM)
+  hipStream_t exec = nullptr;
+  hipEvent_t exec_fork = nullptr, exec_join = nullptr;
+  int32_t fail_copy = 0;                       // tp_debug_fail_copy countdown (0: off)
   std::unique_ptr<tp::Arena> policy;
   std::unordered_map<int32_t, std::unique_ptr<tp::Model>> models;
   int32_t next_id = 1;

@@ -145,10 +145,10 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
 hipError_t attention(const uint16_t* qkv, int B, int S, int H, uint16_t* out, hipStream_t s) {
   if (!qkv || !out || B < 1 || H < 1 || S < 32 || (S & 31) || S > 256) return hipErrorInvalidValue;
   dim3 grid((S + 63) / 64, H, B);
-  if (S == 128) hipLaunchKernelGGL((k_attention<128, true>), grid, dim3(256), 0, s, qkv, S, H, out);
-  else if (S < 128) hipLaunchKernelGGL((k_attention<128, false>), grid, dim3(256), 0, s, qkv, S, H, out);
-  else if (S == 256) hipLaunchKernelGGL((k_attention<256, true>), grid, dim3(256), 0, s, qkv, S, H, out);
-  else hipLaunchKernelGGL((k_attention<256, false>), grid, dim3(256), 0, s, qkv, S, H, out);
+  if (S == 128) (void)launch((k_attention<128, true>), grid, dim3(256), 0, s, qkv, S, H, out);
+  else if (S < 128) (void)launch((k_attention<128, false>), grid, dim3(256), 0, s, qkv, S, H, out);
+  else if (S == 256) (void)launch((k_attention<256, true>), grid, dim3(256), 0, s, qkv, S, H, out);
+  else (void)launch((k_attention<256, false>), grid, dim3(256), 0, s, qkv, S, H, out);
   return hipGetLastError();
 }
 

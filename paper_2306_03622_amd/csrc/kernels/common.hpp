@@ -4,6 +4,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <cstddef>
+#include <cstring>
+#include <tuple>
+#include <utility>
+
 #include "kernels.hpp"
 
 namespace tp {
@@ -66,6 +71,48 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// Byte offsets of the device pointers inside a kernel argument of type T (none for values;
+// the argument itself for a pointer; argument blocks specialise this).
+template <typename T>
+struct PtrFields {
+  static void add(std::vector<uint32_t>&, uint32_t) {}
+};
+template <typename T>
+struct PtrFields<T*> {
+  static void add(std::vector<uint32_t>& v, uint32_t at) { v.push_back(at); }
+};
+
+// Launches `kern` with its arguments converted to the kernel's parameter types (the same
+// call the triple-chevron form makes), and records the launch in launch_log when one is set.
+template <typename... P, typename... A>
+hipError_t launch(void (*kern)(P...), dim3 grid, dim3 block, unsigned shmem, hipStream_t s, A&&... a) {
+  static_assert(sizeof...(P) == sizeof...(A), "argument count");
+  std::tuple<P...> args{P(std::forward<A>(a))...};
+  return std::apply(
+      [&](auto&... v) -> hipError_t {
+        void* argv[] = {static_cast<void*>(&v)...};
+        if (launch_log) {
+          LaunchRecord r;
+          r.func = reinterpret_cast<const void*>(kern);
+          r.grid = grid;
+          r.block = block;
+          r.shmem = shmem;
+          auto put = [&](const auto& x) {
+            using T = std::decay_t<decltype(x)>;
+            const uint32_t at = (uint32_t)((r.bytes.size() + 7) & ~size_t(7));
+            r.bytes.resize(at + sizeof(T));
+            std::memcpy(r.bytes.data() + at, &x, sizeof(T));
+            r.arg_at.push_back(at);
+            PtrFields<T>::add(r.ptr_at, at);
+          };
+          (put(v), ...);
+          launch_log->push_back(std::move(r));
+        }
+        return hipLaunchKernel(reinterpret_cast<const void*>(kern), grid, block, argv, shmem, s);
+      },
+      args);
 }
 
 }  // namespace k

@@ -21,6 +21,17 @@ struct GemmArgs {
   float* partials;                        // [splits][M][N] fp32 when splits > 1
 };
 
+template <>
+struct PtrFields<GemmArgs> {
+  static void add(std::vector<uint32_t>& v, uint32_t at) {
+    for (size_t o : {offsetof(GemmArgs, x), offsetof(GemmArgs, w), offsetof(GemmArgs, partials),
+                     offsetof(GemmArgs, ep) + offsetof(Epilogue, bias), offsetof(GemmArgs, ep) + offsetof(Epilogue, res),
+                     offsetof(GemmArgs, ep) + offsetof(Epilogue, out), offsetof(GemmArgs, ep) + offsetof(Epilogue, ln_g),
+                     offsetof(GemmArgs, ep) + offsetof(Epilogue, ln_b), offsetof(GemmArgs, ep) + offsetof(Epilogue, ln_out)})
+      v.push_back(at + (uint32_t)o);
+  }
+};
+
 __device__ __forceinline__ int res_kind_dev(const Epilogue& ep) { return !ep.res ? 0 : ep.res_f32 ? 2 : 1; }
 
 // The epilogue's inputs for four consecutive outputs of a row, as raw bits: fetched

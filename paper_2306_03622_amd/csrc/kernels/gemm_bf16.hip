@@ -557,9 +557,9 @@ __global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
 template <int RES>
 void launch_split_reduce_res(const GemmArgs& a, dim3 grid, dim3 block, hipStream_t s) {
   switch (split_group(a.splits)) {
-    case 2: hipLaunchKernelGGL((k_split_reduce<2, RES>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_split_reduce<4, RES>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((k_split_reduce<8, RES>), grid, block, 0, s, a); break;
+    case 2: (void)launch((k_split_reduce<2, RES>), grid, block, 0, s, a); break;
+    case 4: (void)launch((k_split_reduce<4, RES>), grid, block, 0, s, a); break;
+    default: (void)launch((k_split_reduce<8, RES>), grid, block, 0, s, a); break;
   }
 }
 
@@ -620,11 +620,11 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   dim3 grid(tn, tm, a.splits);
   if constexpr (MODE == X_ROWS) {
     if (a.ep.w_packed) {
-      hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, true, D, WGN, WGM>), grid, dim3(64 * WGN * WGM), 0, s, a);
+      (void)launch((k_gemm<BN, BM, BK, MODE, WVEC, true, D, WGN, WGM>), grid, dim3(64 * WGN * WGM), 0, s, a);
       return finish(a, s);
     }
   }
-  hipLaunchKernelGGL((k_gemm<BN, BM, BK, MODE, WVEC, false, D, WGN, WGM>), grid, dim3(64 * WGN * WGM), 0, s, a);
+  (void)launch((k_gemm<BN, BM, BK, MODE, WVEC, false, D, WGN, WGM>), grid, dim3(64 * WGN * WGM), 0, s, a);
   return finish(a, s);
 }
 
@@ -685,10 +685,10 @@ hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16
     const int rows = max(1, min(8, segs * Ho * B / 448));
     dim3 grid(segs, (Ho + rows - 1) / rows, B);
     switch (C) {
-      case 1: hipLaunchKernelGGL(k_conv_smallc<1>, grid, dim3(256), 0, s, a, rows); break;
-      case 2: hipLaunchKernelGGL(k_conv_smallc<2>, grid, dim3(256), 0, s, a, rows); break;
-      case 3: hipLaunchKernelGGL(k_conv_smallc<3>, grid, dim3(256), 0, s, a, rows); break;
-      default: hipLaunchKernelGGL(k_conv_smallc<4>, grid, dim3(256), 0, s, a, rows); break;
+      case 1: (void)launch(k_conv_smallc<1>, grid, dim3(256), 0, s, a, rows); break;
+      case 2: (void)launch(k_conv_smallc<2>, grid, dim3(256), 0, s, a, rows); break;
+      case 3: (void)launch(k_conv_smallc<3>, grid, dim3(256), 0, s, a, rows); break;
+      default: (void)launch(k_conv_smallc<4>, grid, dim3(256), 0, s, a, rows); break;
     }
     return hipGetLastError();
   }

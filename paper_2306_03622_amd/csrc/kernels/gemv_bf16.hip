@@ -106,11 +106,11 @@ __global__ __launch_bounds__(NW * 64) void k_gemv(GemmArgs a) {
 hipError_t launch_skinny(const GemmArgs& a, hipStream_t s) {
   const dim3 grid((a.N + 15) / 16), block(GEMV_NW * 64);
   if (a.M <= 16) {
-    if (a.ep.w_packed) hipLaunchKernelGGL((k_gemv<1, GEMV_NW, GEMV_U, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_gemv<1, GEMV_NW, GEMV_U, false>), grid, block, 0, s, a);
+    if (a.ep.w_packed) (void)launch((k_gemv<1, GEMV_NW, GEMV_U, true>), grid, block, 0, s, a);
+    else (void)launch((k_gemv<1, GEMV_NW, GEMV_U, false>), grid, block, 0, s, a);
   } else {
-    if (a.ep.w_packed) hipLaunchKernelGGL((k_gemv<2, GEMV_NW, GEMV_U, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_gemv<2, GEMV_NW, GEMV_U, false>), grid, block, 0, s, a);
+    if (a.ep.w_packed) (void)launch((k_gemv<2, GEMV_NW, GEMV_U, true>), grid, block, 0, s, a);
+    else (void)launch((k_gemv<2, GEMV_NW, GEMV_U, false>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }

@@ -5,10 +5,29 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include <vector>
+
 namespace tp {
 namespace k {
 
 enum { ACT_NONE = 0, ACT_RELU = 1, ACT_GELU = 2 };
+
+// One kernel launch as the launchers record it while a forward pass is being captured into
+// a graph: the kernel, its launch shape, a copy of every argument (each at its own 8-byte
+// aligned offset in `bytes`) and the offsets in `bytes` of the device pointers the arguments
+// hold (a pointer argument itself; the pointer fields of a contraction's argument block). The
+// runtime uses it to repoint an instantiated graph at other input and output buffers.
+struct LaunchRecord {
+  const void* func = nullptr;
+  dim3 grid, block;
+  unsigned shmem = 0;
+  std::vector<uint32_t> arg_at;    // offset of each argument in `bytes`
+  std::vector<uint8_t> bytes;
+  std::vector<uint32_t> ptr_at;    // offsets of pointer values in `bytes`
+};
+
+// When set (by the runtime, on the capturing thread), every launcher appends its launches.
+extern thread_local std::vector<LaunchRecord>* launch_log;
 
 // Fused epilogue of the bf16 contractions: v = acc + bias[n] (+ res[m][n]); v = act(v);
 // out[m][n] = v stored as bf16 or fp32. Row stride of res and out is N.

@@ -38,7 +38,7 @@ __global__ __launch_bounds__(256) void k_linear_f32(const float* __restrict__ x,
 hipError_t linear_f32(const float* x, int M, int K, const float* w, int N, const float* bias, int act, float* y,
                       hipStream_t s) {
   if (!x || !w || !y || M < 1 || N < 1 || K < 4 || (K & 3) || act < 0 || act > 2) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_linear_f32, dim3((N + 3) / 4), dim3(256), 0, s, x, M, K, w, N, bias, act, y);
+  (void)launch(k_linear_f32, dim3((N + 3) / 4), dim3(256), 0, s, x, M, K, w, N, bias, act, y);
   return hipGetLastError();
 }
 

@@ -205,9 +205,9 @@ __global__ __launch_bounds__(256) void k_split_reduce_ln(GemmArgs a) {
 template <int PER, int RES>
 void launch_split_reduce_ln_res(const GemmArgs& a, dim3 grid, dim3 block, hipStream_t s) {
   switch (split_group(a.splits)) {
-    case 2: hipLaunchKernelGGL((k_split_reduce_ln<PER, 2, RES>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_split_reduce_ln<PER, 4, RES>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((k_split_reduce_ln<PER, 8, RES>), grid, block, 0, s, a); break;
+    case 2: (void)launch((k_split_reduce_ln<PER, 2, RES>), grid, block, 0, s, a); break;
+    case 4: (void)launch((k_split_reduce_ln<PER, 4, RES>), grid, block, 0, s, a); break;
+    default: (void)launch((k_split_reduce_ln<PER, 8, RES>), grid, block, 0, s, a); break;
   }
 }
 
@@ -223,7 +223,7 @@ void launch_split_reduce_ln(const GemmArgs& a, dim3 grid, dim3 block, hipStream_
 template <int PER>
 hipError_t launch_ln(const float* x, int M, const uint16_t* g, const uint16_t* b, float eps, void* out, int out_f32,
                      hipStream_t s) {
-  hipLaunchKernelGGL((k_layernorm<PER>), dim3((M + 3) / 4), dim3(256), 0, s, x, M, g, b, eps, out, out_f32);
+  (void)launch((k_layernorm<PER>), dim3((M + 3) / 4), dim3(256), 0, s, x, M, g, b, eps, out, out_f32);
   return hipGetLastError();
 }
 
@@ -231,7 +231,7 @@ template <int PER>
 hipError_t launch_embed(const int32_t* ids, int M, int S, int vocab, const uint16_t* tok, const uint16_t* pos,
                         const uint16_t* type, const uint16_t* g, const uint16_t* b, float eps, uint16_t* out,
                         hipStream_t s) {
-  hipLaunchKernelGGL((k_embed_ln<PER>), dim3((M + 3) / 4), dim3(256), 0, s, ids, M, S, vocab, tok, pos, type, g, b,
+  (void)launch((k_embed_ln<PER>), dim3((M + 3) / 4), dim3(256), 0, s, ids, M, S, vocab, tok, pos, type, g, b,
                      eps, out);
   return hipGetLastError();
 }

@@ -95,13 +95,13 @@ hipError_t maxpool3s2(const uint16_t* x, int B, int H, int W, int C, uint16_t* y
   if (!x || !y || B < 1 || H < 1 || W < 1 || C < 8 || (C & 7)) return hipErrorInvalidValue;
   const int Ho = (H + 2 - 3) / 2 + 1, Wo = (W + 2 - 3) / 2 + 1;
   const long total = (long)B * Ho * Wo * (C >> 3);
-  hipLaunchKernelGGL(k_maxpool3s2, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, B, H, W, C, Ho, Wo, y);
+  (void)launch(k_maxpool3s2, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, B, H, W, C, Ho, Wo, y);
   return hipGetLastError();
 }
 
 hipError_t avgpool(const uint16_t* x, int B, int HW, int C, uint16_t* y, hipStream_t s) {
   if (!x || !y || B < 1 || HW < 1 || C < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_avgpool, dim3((B * C + 63) / 64), dim3(64), 0, s, x, B, HW, C, y);
+  (void)launch(k_avgpool, dim3((B * C + 63) / 64), dim3(64), 0, s, x, B, HW, C, y);
   return hipGetLastError();
 }
 
@@ -109,7 +109,7 @@ hipError_t gather_copy(const void* src, void* dst, uint64_t bytes, int wgs, hipS
   if (!src || !dst || (bytes & 15) || wgs < 1 || ((uintptr_t)src & 15) || ((uintptr_t)dst & 15))
     return hipErrorInvalidValue;
   if (bytes == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gather, dim3(wgs), dim3(256), 0, s, static_cast<const uint4*>(src), static_cast<uint4*>(dst),
+  (void)launch(k_gather, dim3(wgs), dim3(256), 0, s, static_cast<const uint4*>(src), static_cast<uint4*>(dst),
                      bytes >> 4);
   return hipGetLastError();
 }
@@ -117,7 +117,7 @@ hipError_t gather_copy(const void* src, void* dst, uint64_t bytes, int wgs, hipS
 hipError_t delay(int us, hipStream_t s) {
   // s_sleep 127 is about 127 * 64 cycles, ~3.4 us at 2.4 GHz
   const int iters = us <= 3 ? 1 : us / 3;
-  hipLaunchKernelGGL(k_delay, dim3(1), dim3(64), 0, s, iters);
+  (void)launch(k_delay, dim3(1), dim3(64), 0, s, iters);
   return hipGetLastError();
 }
 

@@ -26,6 +26,7 @@ TP_ARCH_MLP, TP_ARCH_RESNET50, TP_ARCH_BERT = 0, 1, 2
 TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
 TP_COPY_MEMCPY, TP_COPY_GATHER, TP_COPY_PAGEABLE, TP_COPY_ZERO = 0, 1, 2, 3
 TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR, TP_FLAG_TRACE = 1, 2, 4, 8, 16, 32
+TP_FLAG_CALLER_STREAM = 64
 TP_PLAN_GREEDY, TP_PLAN_COST = 0, 1
 TP_EVICT_LRU, TP_EVICT_HEAVINESS = 0, 1
 TP_CLASS_AUTO, TP_CLASS_LIGHT, TP_CLASS_HEAVY = 0, 1, 2
@@ -73,7 +74,8 @@ class tp_arena_stats_t(C.Structure):
                 ("misses", C.c_uint64), ("evictions", C.c_uint64), ("frag_evictions", C.c_uint64),
                 ("bytes_swapped", C.c_uint64), ("admit_calls", C.c_uint64), ("admit_ns_total", C.c_uint64),
                 ("admit_ns_max", C.c_uint64), ("partitions", C.c_uint32), ("partitions_free", C.c_uint32),
-                ("evacuations", C.c_uint64), ("bytes_moved", C.c_uint64)]
+                ("evacuations", C.c_uint64), ("bytes_moved", C.c_uint64), ("graph_captures", C.c_uint64),
+                ("graph_repoints", C.c_uint64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -126,6 +128,7 @@ _SIGS = {
     "tp_infer": [_P, C.c_int32, _P, C.c_int32, _P, _P],
     "tp_swap_in": [_P, C.c_int32, _P],
     "tp_evict": [_P, C.c_int32],
+    "tp_debug_fail_copy": [_P, C.c_int32],
     "tp_is_resident": [_P, C.c_int32, C.POINTER(C.c_int32)],
     "tp_arena_stats": [_P, C.POINTER(tp_arena_stats_t)],
     "tp_model_info": [_P, C.c_int32, C.POINTER(tp_model_info_t)],
@@ -300,6 +303,10 @@ def tp_swap_in(ctx, model_id, stream=None):
 
 def tp_evict(ctx, model_id):
     _check(lib(), lib().tp_evict(ctx, model_id))
+
+
+def tp_debug_fail_copy(ctx, nth: int):
+    _check(lib(), lib().tp_debug_fail_copy(ctx, nth))
 
 
 def tp_is_resident(ctx, model_id) -> bool:
@@ -634,6 +641,10 @@ class Runtime:
 
     def evict(self, mid):
         tp_evict(self.ctx, mid)
+
+    def fail_copy(self, nth: int):
+        """Test hook: the nth copy enqueued from now on fails (0 disarms)."""
+        tp_debug_fail_copy(self.ctx, nth)
 
     def resident(self, mid) -> bool:
         return tp_is_resident(self.ctx, mid)

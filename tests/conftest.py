@@ -3,10 +3,6 @@ import sys
 
 import pytest
 
-# the benchmark's stream configuration (hardware queues for the copy and request streams,
-# set before the HIP runtime starts)
-os.environ.setdefault("GPU_MAX_HW_QUEUES", "8")
-
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)

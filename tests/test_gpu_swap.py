@@ -114,9 +114,51 @@ def test_warm_graph_replay_equals_kernel_by_kernel():
             rt.infer(ids[k], x, out, stream=s)
             s.synchronize()
             assert np.array_equal(out.cpu().numpy(), want), (m.arch, rep)
-        # a smaller batch through a sliced input makes a new graph
+        # a smaller batch makes a new graph
         got = infer(rt, ids[k], m, x_np[:1])
         assert np.array_equal(got, infer(eager_rt, eager_ids[k], m, x_np[:1]))
+    st = rt.stats()
+    # per family: one capture at batch 3 (the cold request launches eagerly) and one at
+    # batch 1; the batch-3 graph was repointed at the other output buffer on every second
+    # request, then the batch-1 request's new buffers were captured fresh
+    assert st["graph_captures"] == 2 * len(ms), st
+    assert st["graph_repoints"] == 3 * len(ms), st
+    eager_rt.close()
+    rt.close()
+
+
+def test_warm_hits_with_new_buffers_repoint_the_graph():
+    # every warm request brings buffers of its own (as a server does): each must compute the
+    # kernel-by-kernel bits, and only the first warm request per (model, batch) may capture
+    ms = [synth.mlp(18, 256, "bf16", "gelu", seed=64),
+          synth.bert(seed=65, layers=3, d=128, heads=2, ffn=256, seq=64, vocab=500, maxpos=64),
+          synth.resnet50(seed=66, classes=10, image=32)]
+    torch, dev = torch_dev()
+    eager_rt, eager_ids = make_runtime(ms, batch_max=4, flags=tp.TP_FLAG_NO_GRAPH)
+    rt, ids = make_runtime(ms, batch_max=4)
+    s = torch.cuda.Stream(device=dev)
+    keep = []                     # every buffer stays allocated, so no address comes back
+    for k, m in enumerate(ms):
+        for batch in (4, 2):
+            for rep in range(4):
+                x_np = synth.config_input(m, batch, 500 + 31 * k + 7 * rep + batch)
+                want = infer(eager_rt, eager_ids[k], m, x_np)
+                x = to_device(x_np)
+                out = torch.full(out_shape(m, batch), float("nan"), dtype=torch.float32, device=dev)
+                keep += [x, out]
+                torch.cuda.synchronize()
+                rt.infer(ids[k], x, out, stream=s)
+                s.synchronize()
+                got = out.cpu().numpy()
+                assert np.array_equal(got, want), (m.arch, batch, rep)
+                if rep == 0 and batch == 4:
+                    check_parity(got, m, x_np, 2e-2)
+    st = rt.stats()
+    log(f"graph captures {st['graph_captures']}, repoints {st['graph_repoints']}")
+    # per family: the very first request is cold (eager); batch 4 then captures once and
+    # repoints twice, batch 2 captures once and repoints three times
+    assert st["graph_captures"] == 2 * len(ms), st
+    assert st["graph_repoints"] == 5 * len(ms), st
     eager_rt.close()
     rt.close()
 
@@ -128,6 +170,8 @@ def test_eviction_order_and_placement_do_not_change_outputs():
     ref_rt, ref_ids = make_runtime(ms, batch_max=2)
     ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
     ref_rt.close()
+    for r, m, x in zip(ref, ms, xs):
+        check_parity(r, m, x, 2e-2)
     rt, ids = make_runtime(ms, batch_max=2, arena_bytes=small_arena, flags=tp.TP_FLAG_POISON)
     offsets = {i: set() for i in range(3)}
     order = [0, 1, 2, 1, 0, 2, 2, 0, 1, 0]
@@ -148,6 +192,8 @@ def test_throttled_poisoned_swaps_are_bit_identical(plan):
     ref_rt, ref_ids = make_runtime(ms, batch_max=2)
     ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
     ref_rt.close()
+    for r, m, x in zip(ref, ms, xs):
+        check_parity(r, m, x, 2e-2)
     # each chunk waits ~200 us on the copy stream; a layer that did not wait for its chunk
     # would read 0xFF bytes (NaN) left by the poisoned eviction of the previous tenant
     arena = max(m.total_bytes for m in ms) + 4096
@@ -195,6 +241,8 @@ def test_single_chunk_swaps_over_previous_tenant():
     ref_rt, ref_ids = make_runtime(ms, batch_max=2, flags=tp.TP_FLAG_NO_GRAPH)
     ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
     ref_rt.close()
+    for r, m, x in zip(ref, ms, xs):
+        check_parity(r, m, x, 2e-2)
     arena = max(m.total_bytes for m in ms) + 4096
     rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, chunk_min_bytes=1 << 40)
     torch, dev = torch_dev()
@@ -228,6 +276,8 @@ def test_swap_designs_compute_the_same_bits(name):
     ref_rt, ref_ids = make_runtime(ms, batch_max=2, flags=tp.TP_FLAG_NO_GRAPH)
     ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
     ref_rt.close()
+    for r, m, x in zip(ref, ms, xs):                    # the reference itself matches the oracle
+        check_parity(r, m, x, 2e-2)
     arena = max(m.total_bytes for m in ms) + 4096       # one model at a time
     rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, **ABLATION[name])
     zero = ABLATION[name].get("copy_method") == tp.TP_COPY_ZERO
@@ -260,6 +310,8 @@ def test_direct_access_then_background_swap(flags):
     ref_rt, ref_ids = make_runtime(ms, batch_max=2, flags=tp.TP_FLAG_NO_GRAPH)
     ref = [infer(ref_rt, i, m, x) for i, m, x in zip(ref_ids, ms, xs)]
     ref_rt.close()
+    for r, m, x in zip(ref, ms, xs):                    # the reference itself matches the oracle
+        check_parity(r, m, x, 2e-2)
     arena = max(m.total_bytes for m in ms) + 4096
     rt, ids = make_runtime(ms, batch_max=2, arena_bytes=arena, chunk_min_bytes=0, direct_max_bytes=1 << 40,
                            flags=flags | tp.TP_FLAG_POISON | tp.TP_FLAG_THROTTLE, throttle_us=200)
@@ -285,6 +337,7 @@ def test_traced_timeline_is_causal():
     ref_rt, ref_ids = make_runtime([m], batch_max=2)
     want = infer(ref_rt, ref_ids[0], m, x)
     ref_rt.close()
+    check_parity(want, m, x, 2e-2)
     for rep in range(3):
         rt.evict(ids[0])
         assert np.array_equal(infer(rt, ids[0], m, x), want)
