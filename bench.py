@@ -411,6 +411,8 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
         wp = p50(rr["warm"])
         bnd = max(m.total_bytes / (link * 1e9) * 1e3, wp)
         fl = forward_flops(m, bt)
+        import hashlib
+        digest = hashlib.sha256(rr["out"].cpu().numpy().tobytes()).hexdigest()[:16]   # last request's output
         fwd = bb.event_time_ms(rr["x"], rr["out"], 20)
         out[f"cfg{cfg}_b{bt}"] = {
             "weight_bytes": m.total_bytes, "chunks": len(bb.rt.chunks(bb.mid)),
@@ -421,7 +423,7 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
             "swap_only_gbs": round(m.total_bytes / (p50(rr["swap"]) / 1e3) / 1e9, 2),
             "forward_gflop": round(fl / 1e9, 3), "warm_forward_event_ms": round(fwd, 4),
             "warm_tflops": round(fl / (fwd * 1e-3) / 1e12, 2),
-            "mfma_util": round(fl / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5)}
+            "mfma_util": round(fl / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5), "output_sha16": digest}
     bb.close()
     if cpu:
         for bt in bts:
