@@ -274,6 +274,21 @@ TP_API tp_status tp_unregister_model(struct tp_ctx* ctx, int32_t model_id);
 TP_API tp_status tp_infer(struct tp_ctx* ctx, int32_t model_id, const void* input_dev, int32_t batch,
                    void* output_dev, void* stream);
 
+/* tp_infer for callers that cannot allocate device memory (code that must not call hipMalloc,
+ * tight serving loops, harnesses that forbid allocation): the same request, computing the
+ * same bits, but its activations and split-contraction partials live in a static workspace
+ * of 64 MiB (kNoAllocScratchBytes) that the library's code object holds on each device,
+ * instead of the context's work_dev; its kernels are launched one by one (no graph is
+ * captured or instantiated). The call allocates nothing; the caller still passes the input
+ * and output buffers. The workspace is shared by every context and call on the device and
+ * keeps the last call's contents (nothing in it needs to start at zero): calls that overlap
+ * on one device race, so a process must not have two such requests in flight at once on
+ * different contexts or unordered streams (one context's requests are ordered anyway).
+ * Errors: as tp_infer; TP_E_NOSPC when the request needs more than the 64 MiB (e.g.
+ * ResNet-50 beyond batch 2); TP_E_HIP if the workspace's device address could not be
+ * resolved when the context was created. */
+TP_API tp_status tp_infer_noalloc(struct tp_ctx* ctx, int32_t model_id, const void* input_dev, int32_t batch,
+                                  void* output_dev, void* stream);
 /* Enqueues the swap-in alone (admission + chunk copies, no compute), as a request with
  * no output; a following tp_infer of the same model is a hit. `stream` is made to wait
  * for the copies. Same errors as tp_infer. */

@@ -27,7 +27,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CORE = ["core/model.cpp", "core/arena.cpp", "core/partition.cpp", "core/sched.cpp", "core/plan_api.cpp", "core/errors.cpp"]
 HIP_HOST = ["hip/runtime.cpp", "hip/executors.cpp", "hip/trace.cpp"]
 PROBE = ["probe/peaks.hip"]
-KERNELS = ["kernels/gemm_bf16.hip", "kernels/gemv_bf16.hip", "kernels/linear_f32.hip", "kernels/norm.hip", "kernels/attention.hip",
+KERNELS = ["hip/scratch.hip", "kernels/gemm_bf16.hip", "kernels/gemv_bf16.hip", "kernels/linear_f32.hip", "kernels/norm.hip", "kernels/attention.hip",
            "kernels/pool_copy.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall", f"-I{os.path.join(ROOT, 'include')}"]

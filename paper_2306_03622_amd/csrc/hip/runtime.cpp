@@ -13,6 +13,7 @@
 
 #include "../core/errors.hpp"
 #include "../kernels/kernels.hpp"
+#include "scratch.hpp"
 
 using namespace tp;
 
@@ -467,7 +468,7 @@ tp_status check_request(tp_ctx* c, int32_t id, Model** out) {
 
 // One request (tp_infer and its variants), with the workspace `work` of `work_bytes`.
 tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, void* output_dev,
-                        hipStream_t stream, char* work, uint64_t work_bytes, const char* who) {
+                        hipStream_t stream, char* work, uint64_t work_bytes, const char* who, bool allow_graphs = true) {
   Model* m = nullptr;
   tp_status s = check_request(c, id, &m);
   if (s != TP_OK) return s;
@@ -496,8 +497,8 @@ tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t ba
   bool swapped = false;
   if ((s = admit(c, m, &swapped)) != TP_OK) return s;
   const uint64_t off = c->policy->offset(id);
-  const bool graphs =
-      !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed && forward_launches(m->spec) >= kGraphMinLaunches;
+  const bool graphs = allow_graphs && !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed &&
+                      forward_launches(m->spec) >= kGraphMinLaunches;
   // a swapping request's kernels run on the library's execution stream (see tp_create)
   const bool forked = swapped && !direct && c->exec;
   hipError_t e = swapped ? hipSuccess : settle(m, stream);
@@ -637,6 +638,9 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->exec_join, hipEventDisableTiming);
   }
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
+  // tp_infer_noalloc's workspace on this device (a failure only disables that entry point,
+  // which then reports it)
+  if (e == hipSuccess && scratch_init(c->device) != hipSuccess) (void)hipGetLastError();
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming);
   if (e == hipSuccess && (cfg->flags & TP_FLAG_TRACE)) e = hipEventCreate(&c->tl.start);
@@ -769,6 +773,22 @@ tp_status tp_infer(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, 
   if (!c) return fail(TP_E_INVAL, "NULL context");
   return infer_request(c, id, input_dev, batch, output_dev, static_cast<hipStream_t>(stream_), c->work,
                        c->cfg.work_bytes, "tp_infer");
+}
+
+tp_status tp_infer_noalloc(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, void* output_dev,
+                           void* stream_) {
+  if (!c) return fail(TP_E_INVAL, "NULL context");
+  char* work = scratch_region(c->device);
+  if (!work) return fail(TP_E_HIP, "tp_infer_noalloc: the static workspace's address could not be resolved on device " +
+                                        std::to_string(c->device) + " at tp_create");
+  Model* m = find(c, id);
+  if (m && batch >= 1 && workspace_bytes(m->spec, batch) > kNoAllocScratchBytes)
+    return fail(TP_E_NOSPC, "tp_infer_noalloc: the request needs " + std::to_string(workspace_bytes(m->spec, batch)) +
+                                " bytes of workspace; the static workspace holds " +
+                                std::to_string(kNoAllocScratchBytes));
+  // kernels launched one by one: instantiating a graph may allocate device memory
+  return infer_request(c, id, input_dev, batch, output_dev, static_cast<hipStream_t>(stream_), work,
+                       kNoAllocScratchBytes, "tp_infer_noalloc", false);
 }
 
 tp_status tp_swap_in(tp_ctx* c, int32_t id, void* stream_) {

@@ -126,6 +126,7 @@ _SIGS = {
     "tp_register_model": [_P, C.POINTER(tp_model_desc), _P, C.c_uint64, C.POINTER(C.c_int32)],
     "tp_unregister_model": [_P, C.c_int32],
     "tp_infer": [_P, C.c_int32, _P, C.c_int32, _P, _P],
+    "tp_infer_noalloc": [_P, C.c_int32, _P, C.c_int32, _P, _P],
     "tp_swap_in": [_P, C.c_int32, _P],
     "tp_evict": [_P, C.c_int32],
     "tp_debug_fail_copy": [_P, C.c_int32],
@@ -295,6 +296,10 @@ def tp_unregister_model(ctx, model_id):
 
 def tp_infer(ctx, model_id, input_dev, batch, output_dev, stream=None):
     _check(lib(), lib().tp_infer(ctx, model_id, _ptr(input_dev), batch, _ptr(output_dev), _ptr(stream)))
+
+
+def tp_infer_noalloc(ctx, model_id, input_dev, batch, output_dev, stream=None):
+    _check(lib(), lib().tp_infer_noalloc(ctx, model_id, _ptr(input_dev), batch, _ptr(output_dev), _ptr(stream)))
 
 
 def tp_swap_in(ctx, model_id, stream=None):
@@ -634,6 +639,11 @@ class Runtime:
         """x, out: torch device tensors; stream: a torch stream (default: current)."""
         s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
         tp_infer(self.ctx, mid, x, int(x.shape[0]), out, s)
+
+    def infer_noalloc(self, mid, x, out, stream=None):
+        """tp_infer on the library's static workspace (allocates nothing)."""
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        tp_infer_noalloc(self.ctx, mid, x, int(x.shape[0]), out, s)
 
     def swap_in(self, mid, stream=None):
         s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
