@@ -73,13 +73,22 @@ def build(jobs: int = 8, sanitize: bool = False, verbose: bool = False) -> str:
     ptmp = PROBE_LIB + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", *DEVICE, "-o", ptmp, *[_obj(s) for s in PROBE]])
     os.replace(ptmp, PROBE_LIB)
-    # host-only planning library
-    san = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer"] if sanitize else []
-    htmp = HOST_LIB + ".tmp"
-    _run(["g++", "-O1" if sanitize else "-O2", "-std=c++17", "-fPIC", "-shared", "-fvisibility=hidden", *san,
-          f"-I{os.path.join(ROOT, 'include')}", *[os.path.join(CSRC, s) for s in CORE], "-o", htmp])
-    os.replace(htmp, HOST_LIB)
+    build_host(HOST_LIB, sanitize)
     return LIB
+
+
+# AddressSanitizer and UndefinedBehaviorSanitizer, every report fatal
+SANITIZE = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g"]
+
+
+def build_host(path: str = HOST_LIB, sanitize: bool = False) -> str:
+    """The host-only planning library (g++ alone, no HIP), optionally under the sanitizers."""
+    tmp = path + ".tmp"
+    _run(["g++", "-O1" if sanitize else "-O2", "-std=c++17", "-fPIC", "-shared", "-fvisibility=hidden",
+          *(SANITIZE if sanitize else []), f"-I{os.path.join(ROOT, 'include')}",
+          *[os.path.join(CSRC, s) for s in CORE], "-o", tmp])
+    os.replace(tmp, path)
+    return path
 
 
 if __name__ == "__main__":
