@@ -352,7 +352,7 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                       "p99_ms": round(float(np.percentile(lat[sel], 99)), 3),
                       "hit_rate": round(float(hit[sel].mean()), 4)}
     delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
-                                          "evacuations", "bytes_moved")}
+                                          "evacuations", "bytes_moved", "graph_captures", "graph_repoints")}
     delta["partitions"] = st1["partitions"]
     calls = st1["admit_calls"] - st0["admit_calls"]
     adm = np.array([r["admit_ns"] / 1e3 for r in res if not r["hit"]])
@@ -397,7 +397,7 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
     import paper_2306_03622_amd as tp
     import synth
     m = synth.config_model(cfg)
-    out = {}
+    out, outs = {}, {}
     bb = Bench(torch, dev, m, bts, method, chunk, copy_streams, plan=plan, link_gbs=plan_link or link,
                flags=tp.TP_FLAG_TRACE if trace else 0)
     for bt in bts:
@@ -423,13 +423,17 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
             "swap_only_gbs": round(m.total_bytes / (p50(rr["swap"]) / 1e3) / 1e9, 2),
             "forward_gflop": round(fl / 1e9, 3), "warm_forward_event_ms": round(fwd, 4),
             "warm_tflops": round(fl / (fwd * 1e-3) / 1e12, 2),
-            "mfma_util": round(fl / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5), "output_sha16": digest}
+            "mfma_util": round(fl / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5),
+            "hbm_frac_weights": round(m.total_bytes / (fwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "output_sha16": digest}
+        outs[bt] = rr["out"].cpu().numpy()
     bb.close()
     if cpu:
         for bt in bts:
             log(f"  CPU oracle, workload {cfg} batch {bt}")
             out[f"cfg{cfg}_b{bt}"]["cpu_oracle"] = cpu_baseline(m, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt),
-                                                                budget_s=8.0, max_runs=50 if cfg == 1 else 5)
+                                                                budget_s=8.0, max_runs=50 if cfg == 1 else 5,
+                                                                gpu_out=outs[bt])
     m.drop_blob()
     return out
 
@@ -488,8 +492,9 @@ def forward_flops(model, batch):
     return L * per_layer
 
 
-def cpu_baseline(model, batch, seed, budget_s=12.0, max_runs=30):
-    """The oracle (fp32 variant) on this host's cores, a bounded number of runs."""
+def cpu_baseline(model, batch, seed, budget_s=12.0, max_runs=30, gpu_out=None):
+    """The oracle (fp32 variant) on this host's cores, a bounded number of runs; with `gpu_out`
+    (the library's output for the same input) also the normwise error between the two."""
     import synth
     from oracle import forward as oracle
     try:
@@ -498,16 +503,21 @@ def cpu_baseline(model, batch, seed, budget_s=12.0, max_runs=30):
     except Exception:
         threads = 0
     x = synth.config_input(model, batch, seed)
-    oracle.forward(model, x, np.float32)          # first touch
+    ref = oracle.forward(model, x, np.float32)          # first touch
     times = []
     t_start = time.perf_counter()
     while len(times) < max_runs and (time.perf_counter() - t_start) < budget_s:
         t0 = time.perf_counter()
-        oracle.forward(model, x, np.float32)
+        ref = oracle.forward(model, x, np.float32)
         times.append((time.perf_counter() - t0) * 1e3)
-    return {"value": round(p50(times), 3), "unit": "ms", "cores": threads or os.cpu_count(), "kind": "oracle",
-            "sample": f"{len(times)} fp32 oracle forwards of the same workload at batch {batch} "
-                      f"(p50; {os.cpu_count()} host CPUs visible, BLAS threads {threads})"}
+    out = {"value": round(p50(times), 3), "unit": "ms", "cores": threads or os.cpu_count(), "kind": "oracle",
+           "sample": f"{len(times)} fp32 oracle forwards of the same workload at batch {batch} "
+                     f"(p50; {os.cpu_count()} host CPUs visible, BLAS threads {threads})"}
+    if gpu_out is not None:
+        # the GPU's output for the same input beside the oracle's (fp32 variant; it agrees with
+        # the float64 oracle to <= 1e-5 normwise on every workload)
+        out["gpu_normwise_error"] = float(f"{oracle.normwise_error(gpu_out, ref).max():.3e}")
+    return out
 
 
 def main():
@@ -543,7 +553,10 @@ def main():
     ap.add_argument("--pmc-workload", action="store_true",
                     help="run only a fixed workload for hardware-counter passes: 20 warm forwards of the "
                          "bench model, then one 256 MiB device-to-device copy (the byte-count calibration)")
-    ap.add_argument("--full", action="store_true", help="also time the other batches and workloads")
+    ap.add_argument("--full", action="store_true", help="(the default; kept for older command lines)")
+    ap.add_argument("--quick", action="store_true",
+                    help="the headline workload at --batch only: no other batches, workloads or multi-tenant run")
+    ap.add_argument("--no-tenants", action="store_true", help="skip the multi-tenant row of the default run")
     ap.add_argument("--ablation", action="store_true",
                     help="time the cold request under every swap design instead (breakdown table)")
     ap.add_argument("--no-cpu", action="store_true")
@@ -558,7 +571,7 @@ def main():
         sys.exit(2)
 
     children = {}
-    if a.full and not a.workload:
+    if not a.quick and not a.workload and not (a.tenants or a.ablation or a.pmc_workload):
         # Each extra workload runs in a process of its own, started before this process touches
         # the GPU: a serving process holds one context, and after many contexts and streams in
         # one process HIP's stream-to-hardware-queue arrangement can serialise a swap behind
@@ -575,6 +588,16 @@ def main():
             if out.returncode != 0:
                 raise SystemExit(f"workload {cfg} failed with status {out.returncode}")
             children.update(json.loads(out.stdout.strip().splitlines()[-1]))
+        if not a.no_tenants:
+            log("workload 5, multi-tenant (child process)")
+            out = subprocess.run([sys.executable, os.path.abspath(__file__), "--tenants", "3000", "--plan", a.plan],
+                                 stdout=subprocess.PIPE, text=True)
+            if out.returncode != 0:
+                raise SystemExit(f"multi-tenant workload failed with status {out.returncode}")
+            t = json.loads(out.stdout.strip().splitlines()[-1])
+            children["cfg5_multi_tenant"] = {k: t[k] for k in ("p50_ms", "p99_ms", "hit_rate", "requests", "models",
+                                                               "arena_gib", "per_family", "arena", "config",
+                                                               "trace_s")}
 
     import torch
     import synth
@@ -645,7 +668,7 @@ def main():
     model = synth.config_model(2)
     log("generating the 24 x 4096 bf16 MLP weights")
     model.blob()
-    batches = [1, 8, 32] if a.full else [a.batch]
+    batches = [a.batch] if a.quick else sorted({1, 8, 32, a.batch})
     method = a.method
     extra = {}
     if method == "auto":
@@ -693,7 +716,12 @@ def main():
 
     for bt, rr in results.items():
         wp = p50(rr["warm"])
+        fwd = b.event_time_ms(rr["x"], rr["out"], 20) if bt != B else fwd_ms
         extra[f"mlp24x4096_b{bt}"] = {
+            "warm_forward_event_ms": round(fwd, 4),
+            "hbm_frac_weights": round(W / (fwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "mfma_util": round(2 * bt * K * N * 24 / (fwd * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 5),
+            "swap_only_gbs": round(W / (p50(rr["swap"]) / 1e3) / 1e9, 2),
             "cold_p50_ms": round(p50(rr["cold"]), 3), "cold_p10_ms": round(pct(rr["cold"], 10), 3),
             "cold_p90_ms": round(pct(rr["cold"], 90), 3), "warm_p50_ms": round(wp, 4),
             "bound_ms": round(max(W / (link * 1e9) * 1e3, wp), 3),
@@ -710,7 +738,7 @@ def main():
     cpu = None
     if not a.no_cpu:
         log("CPU oracle baseline")
-        cpu = cpu_baseline(model, B, 10200 + B)
+        cpu = cpu_baseline(model, B, 10200 + B, gpu_out=r["out"].cpu().numpy())
     log("matrix-core and HBM peak probes")
     peaks = machine_peaks()
 
