@@ -350,7 +350,9 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
         if sel.any():
             per[a] = {"requests": int(sel.sum()), "p50_ms": round(float(np.percentile(lat[sel], 50)), 3),
                       "p99_ms": round(float(np.percentile(lat[sel], 99)), 3),
-                      "hit_rate": round(float(hit[sel].mean()), 4)}
+                      "hit_rate": round(float(hit[sel].mean()), 4),
+                      "hit_p50_ms": round(float(np.percentile(lat[sel & (hit == 1)], 50)), 3) if (sel & (hit == 1)).any()
+                      else None}
     delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
                                           "evacuations", "bytes_moved", "graph_captures", "graph_repoints")}
     delta["partitions"] = st1["partitions"]
@@ -390,7 +392,7 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
 
 
 def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, link, steps, warmup, trace,
-                     plan_link=None, cpu=False):
+                     plan_link=None, cpu=False, lib_flags=0):
     """Cold, warm and swap-only latencies of workload `cfg` at batches `bts` (one context);
     `link` sets the bound, `plan_link` (default `link`) the cost-model plan; with `cpu` the
     oracle's time at each batch too."""
@@ -399,7 +401,7 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
     m = synth.config_model(cfg)
     out, outs = {}, {}
     bb = Bench(torch, dev, m, bts, method, chunk, copy_streams, plan=plan, link_gbs=plan_link or link,
-               flags=tp.TP_FLAG_TRACE if trace else 0)
+               flags=(tp.TP_FLAG_TRACE if trace else 0) | lib_flags)
     for bt in bts:
         rr = measure(bb, bt, synth.CONFIG_SEEDS[cfg][1] + (0 if cfg == 1 else bt), steps, warmup, max(4 * steps, 100))
         if trace and m.total_bytes > tp.DEFAULT_DIRECT:     # direct-access requests are not traced
@@ -562,6 +564,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--workload", type=int, default=0, help=argparse.SUPPRESS)   # child process of --full
     ap.add_argument("--batches", default="1", help=argparse.SUPPRESS)
+    ap.add_argument("--lib-flags", type=int, default=0, help="extra TP_FLAG_* bits for --workload runs (A/B checks)")
     ap.add_argument("--trace", action="store_true",
                     help="with --full: record the per-chunk timeline of one more cold request per workload")
     a = ap.parse_args()
@@ -645,7 +648,7 @@ def main():
         chunk = tp.DEFAULT_CHUNK if a.chunk in ("default", "elbow") else int(a.chunk)
         res = measure_workload(torch, dev, a.workload, bts, a.method, chunk, a.copy_streams, a.plan, link, a.steps,
                                a.warmup, a.trace, plan_link=link_copy if a.method != "gather" else link_gather,
-                               cpu=not a.no_cpu)
+                               cpu=not a.no_cpu, lib_flags=a.lib_flags)
         for v in res.values():
             if "cold_p50_ms" in v:
                 v["link_peak_gbs"] = round(link, 2)

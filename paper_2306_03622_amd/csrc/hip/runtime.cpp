@@ -250,6 +250,15 @@ hipError_t tp::Waiter::trace_exec(int c) {
   return hipEventRecord(ctx->tl.exec_begin[c], stream);
 }
 
+hipError_t tp::Waiter::hand_back() {
+  hipError_t e = hipEventRecord(ctx->exec_join, stream);
+  if (e == hipSuccess) e = hipStreamWaitEvent(caller, ctx->exec_join, 0);
+  stream = caller;
+  if (slot) *slot = caller;
+  caller = nullptr;
+  return e;
+}
+
 hipError_t tp::Waiter::issue_through(int c) {
   hipError_t e = hipSuccess;
   while (e == hipSuccess && issued <= c && issued < (int)m->chunks.size()) e = enqueue_chunk(ctx, m, base_off, issued++);
@@ -499,8 +508,9 @@ tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t ba
   const uint64_t off = c->policy->offset(id);
   const bool graphs = allow_graphs && !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed &&
                       forward_launches(m->spec) >= kGraphMinLaunches;
-  // a swapping request's kernels run on the library's execution stream (see tp_create)
-  const bool forked = swapped && !direct && c->exec;
+  // a swapping request's kernels run on the library's execution stream (see tp_create),
+  // all but its last chunk's (a single-chunk request stays on the caller's stream)
+  const bool forked = swapped && !direct && c->exec && m->chunks.size() > 1;
   hipError_t e = swapped ? hipSuccess : settle(m, stream);
   if (e != hipSuccess) {
     // fall through to the failure handling below
@@ -555,20 +565,31 @@ tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t ba
       c->tl.n = (uint32_t)m->chunks.size();
       e = hipEventRecord(c->tl.start, stream);
     }
+    // the first chunk's copy goes out before anything else is enqueued
+    if (e == hipSuccess && swapped) e = w.issue_through(0);
     if (e == hipSuccess && forked) {
-      e = hipEventRecord(c->exec_fork, stream);
-      if (e == hipSuccess) e = hipStreamWaitEvent(c->exec, c->exec_fork, 0);
+      // the execution stream waits for the caller's earlier work, unless all of it has
+      // already completed (then the hand-over would only add a cross-queue wait)
+      const hipError_t q = hipStreamQuery(stream);
+      if (q == hipErrorNotReady) {
+        e = hipEventRecord(c->exec_fork, stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(c->exec, c->exec_fork, 0);
+      } else if (q != hipSuccess) {
+        e = q;
+      }
+      w.caller = stream;
+      w.slot = &x.stream;
     }
     // swap, then execute: every chunk is waited for before the first kernel
     if (e == hipSuccess && swapped && (c->cfg.flags & TP_FLAG_SERIAL)) e = w.need(m->spec.n_layers - 1);
     if (e == hipSuccess) e = run_forward(x);
     // every layer asks for its chunk; issue any the forward pass did not reach
     if (e == hipSuccess && swapped) e = w.issue_through((int)m->chunks.size() - 1);
-    if (forked) {
-      // join whatever was enqueued on the execution stream, also after a failure, so that
-      // the request's completion (and the model's last use) covers it
-      hipError_t ej = hipEventRecord(c->exec_join, c->exec);
-      if (ej == hipSuccess) ej = hipStreamWaitEvent(stream, c->exec_join, 0);
+    if (w.caller) {
+      // not handed back (a failure before the last chunk): join whatever was enqueued on
+      // the execution stream, so that the request's completion (and the model's last use)
+      // covers it
+      const hipError_t ej = w.hand_back();
       if (e == hipSuccess) e = ej;
     }
   }

@@ -63,6 +63,13 @@ struct Model {
 // the kernels of chunk c. When the runtime maps the copy stream onto the same hardware
 // queue as the compute stream, this order keeps each chunk's event packet behind the
 // kernels that precede it instead of ahead of all of them.
+//
+// A forked request runs the layers of every chunk but the last on the library's execution
+// stream and hands back to the caller's stream (`caller`) for the last chunk's layers: the
+// caller's stream then waits for the execution stream's work so far (which is done long
+// before the last chunk lands in a transfer-bound request) and for the last chunk itself,
+// so the hand-back adds no latency at the end. `slot` is the stream the layer kernels are
+// launched on (the request's ExecCtx::stream), switched at the hand-back.
 struct Waiter {
   const Model* m = nullptr;
   hipStream_t stream = nullptr;
@@ -71,11 +78,15 @@ struct Waiter {
   tp_ctx* ctx = nullptr;
   uint64_t base_off = 0;
   int issued = 0;                // chunks whose copies are enqueued
+  hipStream_t caller = nullptr;  // forked requests: the caller's stream, else null
+  hipStream_t* slot = nullptr;
   hipError_t issue_through(int c);
+  hipError_t hand_back();
   hipError_t need(uint32_t layer) {
     if (!swapping) return hipSuccess;
     const int c = (int)m->chunk_of_layer[layer];
     hipError_t e = issue_through(c);
+    if (e == hipSuccess && caller && c == (int)m->chunks.size() - 1) e = hand_back();
     while (e == hipSuccess && waited < c) {
       ++waited;
       e = hipStreamWaitEvent(stream, m->chunk_ev[waited], 0);

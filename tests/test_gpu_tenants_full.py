@@ -147,7 +147,9 @@ def test_full_size_trace_matches_oracle():
         "per_family": {a: {"requests": int((arch == a).sum()),
                            "p50_ms": round(float(np.percentile(lat[arch == a], 50)), 3),
                            "p99_ms": round(float(np.percentile(lat[arch == a], 99)), 3),
-                           "hit_rate": round(float(hits[arch == a].mean()), 4)} for a in ("mlp", "resnet50", "bert")},
+                           "hit_rate": round(float(hits[arch == a].mean()), 4),
+                           "hit_p50_ms": round(float(np.percentile(lat[(arch == a) & hits], 50)), 3)}
+                       for a in ("mlp", "resnet50", "bert")},
         "hit_rate_arena": round(float(hits.mean()), 4), "hit_rate_simulator": round(float(np.mean(want_hits)), 4),
         "hit_rate_byte_capacity_lru": round(float(np.mean(lru)), 4),
         "arena": {k: st[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
