@@ -591,29 +591,9 @@ hipError_t finish(const GemmArgs& a, hipStream_t s) {
 }
 
 template <int BN, int BM, int BK, int MODE, bool WVEC, int D, int WGN = 2, int WGM = 2>
-hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
-  const int tn = (a.N + BN - 1) / BN, tm = (a.M + BM - 1) / BM, tiles = tn * tm;
+hipError_t launch_tiled(GemmArgs a, int splits, const Split& sp, hipStream_t s) {
+  const int tn = (a.N + BN - 1) / BN, tm = (a.M + BM - 1) / BM;
   const int nst = (a.K + BK - 1) / BK;
-  int splits = 1;
-  if (sp.partials && tiles < 512) {
-    // aim for about 512 workgroups (two per CU), at least 8 k-stages per split, within
-    // the scratch; 4 k-stages once the contraction is split anyway, its fp32 partials are
-    // at most 512 KiB per split and no LayerNorm rides on the reduction (ResNet-50 at batch
-    // 1: forward -5.5%; ResNet-50 at batch 8 with its larger partials, BERT-base's FFN2 at
-    // batch 1, or also splitting contractions that 8 stages leave whole: 3-10% slower)
-    const size_t per_split = (size_t)a.M * a.N * 4;
-    int want = (512 + tiles - 1) / tiles;
-    const int min_stages = (nst / 8 >= 2 && per_split <= (512u << 10) && !a.ep.ln_g) ? 4 : 8;
-    want = min(want, max(nst / min_stages, 1));
-    want = min(want, 16);
-    while (want > 1 && per_split * want > sp.partial_bytes) --want;
-    splits = max(want, 1);
-  }
-  // a row LayerNorm epilogue costs a launch of its own unless a split reduction carries it
-  // (BERT-base's attention output projection: warm forward -1.9% at batch 1)
-  if (splits == 1 && sp.partials && a.ep.ln_g && split_reduce_ln_fits(a.N) && nst >= 2 &&
-      (size_t)a.M * a.N * 4 * 2 <= sp.partial_bytes)
-    splits = 2;
   a.kst = (nst + splits - 1) / splits;
   a.splits = (nst + a.kst - 1) / a.kst;        // no empty split
   a.partials = sp.partials;
@@ -628,15 +608,52 @@ hipError_t launch_tiled(GemmArgs a, const Split& sp, hipStream_t s) {
   return finish(a, s);
 }
 
+// Tile shape and k split of a tiled contraction. Measured on MI355X over every contraction of
+// ResNet-50 and BERT-base at batch 1 and 8 (each shape timed under graph replay with 20 tile
+// shapes and 6 split counts): the fastest launches fill the 256 CUs with about one to three
+// workgroups each rather than many small ones or a few large ones; a k split pays only for
+// contractions deeper than about 12 stages whose tiles alone leave CUs idle, since its
+// reduction is a launch of its own (about 2-3 us); tiles larger than 64 x 64 and 128-deep
+// stages were never faster at these sizes (in whole forward passes, 128-deep stages for the
+// smaller tiles: -1% at batch 1, +3% at batch 8; a ring of four stages: +3-6%). So: the largest of 64 x 64, 64 x 32, 32 x 64 and
+// 32 x 32 (output features x rows) whose grid has at least 256 tiles (else 32 x 32); then
+// splits while a split keeps more than 12 stages, the grid stays within 768 workgroups, each
+// split keeps at least 4 stages and the fp32 partials fit the scratch. A row LayerNorm then
+// rides on the split reduction, or takes a launch of its own. 128 x 128 tiles for grids of
+// well over a few such tiles per CU.
+struct TilePlan {
+  int bn, bm, splits;
+};
+
+TilePlan plan_tiles(const GemmArgs& a, const Split& sp) {
+  auto tiles = [&](int bn, int bm) { return (long)((a.N + bn - 1) / bn) * ((a.M + bm - 1) / bm); };
+  if (tiles(128, 128) >= 1024) return {128, 128, 1};
+  static constexpr int kShapes[4][2] = {{64, 64}, {64, 32}, {32, 64}, {32, 32}};
+  TilePlan p{32, 32, 1};
+  for (const auto& t : kShapes)
+    if (tiles(t[0], t[1]) >= 256) {
+      p.bn = t[0];
+      p.bm = t[1];
+      break;
+    }
+  const long nt = tiles(p.bn, p.bm);
+  const int nst = (a.K + 63) / 64;
+  const size_t per_split = (size_t)a.M * a.N * 4;
+  if (sp.partials)
+    while (nst > 12 * p.splits && nt * (p.splits + 1) <= 768 && nst >= 4 * (p.splits + 1) &&
+           per_split * (p.splits + 1) <= sp.partial_bytes)
+      ++p.splits;
+  return p;
+}
+
 template <int MODE, bool WVEC>
 hipError_t pick_tiled(const GemmArgs& a, const Split& sp, hipStream_t s) {
-  // 64 x 64 tiles keep four workgroups per CU resident (latency hiding by occupancy; a
-  // ring of two stages keeps them within 128 VGPRs: measured 5-15% faster on ResNet-50 and
-  // BERT-base than four stages at two workgroups per CU); 128 x 128 only once the grid has
-  // well over a few tiles per CU
-  const long tiles128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
-  if (tiles128 >= 1024) return launch_tiled<128, 128, 64, MODE, WVEC, 2>(a, sp, s);
-  return launch_tiled<64, 64, 64, MODE, WVEC, 2>(a, sp, s);
+  const TilePlan p = plan_tiles(a, sp);
+  if (p.bn == 128) return launch_tiled<128, 128, 64, MODE, WVEC, 2>(a, p.splits, sp, s);
+  if (p.bn == 64 && p.bm == 64) return launch_tiled<64, 64, 64, MODE, WVEC, 2>(a, p.splits, sp, s);
+  if (p.bn == 64) return launch_tiled<64, 32, 64, MODE, WVEC, 2>(a, p.splits, sp, s);
+  if (p.bm == 64) return launch_tiled<32, 64, 64, MODE, WVEC, 2>(a, p.splits, sp, s);
+  return launch_tiled<32, 32, 64, MODE, WVEC, 2>(a, p.splits, sp, s);
 }
 
 bool ep_ok(const Epilogue& ep) {
