@@ -343,6 +343,9 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
     rt.close()
     lat = np.array([(r["done_ns"] - q[4]) / 1e6 for r, q in zip(res, reqs)])
     hit = np.array([r["hit"] for r in res])
+    # requests issued with nothing of theirs queued ahead on the GPU (the previous request had
+    # completed): their latency is the request's own service time
+    idle = np.array([i == 0 or res[i]["issue_ns"] >= res[i - 1]["done_ns"] for i in range(len(res))])
     arch = np.array([kinds[q[0]] for q in reqs])
     per = {}
     for a in ("mlp", "resnet50", "bert"):
@@ -352,7 +355,9 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                       "p99_ms": round(float(np.percentile(lat[sel], 99)), 3),
                       "hit_rate": round(float(hit[sel].mean()), 4),
                       "hit_p50_ms": round(float(np.percentile(lat[sel & (hit == 1)], 50)), 3) if (sel & (hit == 1)).any()
-                      else None}
+                      else None,
+                      "idle_hit_p50_ms": round(float(np.percentile(lat[sel & (hit == 1) & idle], 50)), 3)
+                      if (sel & (hit == 1) & idle).any() else None}
     delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
                                           "evacuations", "bytes_moved", "graph_captures", "graph_repoints")}
     delta["partitions"] = st1["partitions"]

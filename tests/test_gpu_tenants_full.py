@@ -137,6 +137,7 @@ def test_full_size_trace_matches_oracle():
     lat = np.array([(q["done_ns"] - rq[4]) / 1e6 for q, rq in zip(res, reqs)])
     arch = np.array([kinds[rq[0]] for rq in reqs])
     hits = np.array(got_hits)
+    idle = np.array([i == 0 or res[i]["issue_ns"] >= res[i - 1]["done_ns"] for i in range(len(res))])
     lru = byte_lru_hits(sizes, [rq[0] for rq in reqs], ARENA)
     summary = {
         "workload": f"{N_MODELS} models (24x4096 MLP / ResNet-50 / BERT-base by index mod 3), 8 GiB arena, "
@@ -148,7 +149,8 @@ def test_full_size_trace_matches_oracle():
                            "p50_ms": round(float(np.percentile(lat[arch == a], 50)), 3),
                            "p99_ms": round(float(np.percentile(lat[arch == a], 99)), 3),
                            "hit_rate": round(float(hits[arch == a].mean()), 4),
-                           "hit_p50_ms": round(float(np.percentile(lat[(arch == a) & hits], 50)), 3)}
+                           "hit_p50_ms": round(float(np.percentile(lat[(arch == a) & hits], 50)), 3),
+                           "idle_hit_p50_ms": round(float(np.percentile(lat[(arch == a) & hits & idle], 50)), 3)}
                        for a in ("mlp", "resnet50", "bert")},
         "hit_rate_arena": round(float(hits.mean()), 4), "hit_rate_simulator": round(float(np.mean(want_hits)), 4),
         "hit_rate_byte_capacity_lru": round(float(np.mean(lru)), 4),
