@@ -643,6 +643,17 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   TP_HIP(hipGetDevice(&c->device));
   c->ncopy = cfg->copy_streams == 2 ? 2 : 1;
   hipError_t e = hipSuccess;
+  // One small device copy on the legacy null stream before the library creates its CU-masked
+  // streams (which synchronise with the null stream). Measured on MI355X: when a process had
+  // made no such copy before they were created, synchronising the caller's stream after a
+  // direct-access request also waited for the swap enqueued behind it on the copy stream
+  // (1 MB fp32 MLP cold: 145 us instead of 54 us, for as long as the process ran); a copy
+  // made after the streams exist did not help, one made before did. It copies the arena's
+  // first 256 bytes over the next 256, which nothing has been placed in yet.
+  if (cfg->arena_bytes >= 512) {
+    e = hipMemcpyAsync(c->arena + 256, c->arena, 256, hipMemcpyDeviceToDevice, nullptr);
+    if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  }
   if (cfg->copy_stream) {
     c->copy[0] = static_cast<hipStream_t>(cfg->copy_stream);
   } else {
@@ -662,6 +673,7 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   // tp_infer_noalloc's workspace on this device (a failure only disables that entry point,
   // which then reports it)
   if (e == hipSuccess && scratch_init(c->device) != hipSuccess) (void)hipGetLastError();
+
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming);
   if (e == hipSuccess && (cfg->flags & TP_FLAG_TRACE)) e = hipEventCreate(&c->tl.start);
