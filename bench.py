@@ -121,6 +121,7 @@ class Bench:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         self.rt.infer(self.mid, x, out, stream=self.stream)
+        self.last_enqueue_ms = (time.perf_counter() - t0) * 1e3      # host time of the call alone
         self.stream.synchronize()
         return (time.perf_counter() - t0) * 1e3
 
@@ -163,12 +164,19 @@ def measure(b: Bench, batch, seed, steps, warmup, warm_reps):
     torch = b.torch
     torch.cuda.synchronize()
     t_all = time.perf_counter()
-    cold = [b.request(x, out, cold=True) for _ in range(steps)]
+    cold, cold_enq = [], []
+    for _ in range(steps):
+        cold.append(b.request(x, out, cold=True))
+        cold_enq.append(b.last_enqueue_ms)
     torch.cuda.synchronize()
     t_all = time.perf_counter() - t_all
-    warm = [b.request(x, out, cold=False) for _ in range(warm_reps)]
+    warm, warm_enq = [], []
+    for _ in range(warm_reps):
+        warm.append(b.request(x, out, cold=False))
+        warm_enq.append(b.last_enqueue_ms)
     swap = [b.swap_only() for _ in range(max(5, steps // 2))]
-    return {"cold": cold, "warm": warm, "swap": swap, "t_all": t_all, "x": x, "out": out}
+    return {"cold": cold, "warm": warm, "swap": swap, "t_all": t_all, "x": x, "out": out,
+            "cold_enqueue": cold_enq, "warm_enqueue": warm_enq}
 
 
 def elbow_sweep(torch, dev, method, copy_streams=0, sizes=(256 << 10, 512 << 10, 1 << 20, 2 << 20, 4 << 20, 8 << 20, 16 << 20,
@@ -426,6 +434,8 @@ def measure_workload(torch, dev, cfg, bts, method, chunk, copy_streams, plan, li
             "cold_p50_ms": round(p50(rr["cold"]), 4), "cold_p10_ms": round(pct(rr["cold"], 10), 4),
             "cold_p90_ms": round(pct(rr["cold"], 90), 4),
             "warm_p50_ms": round(wp, 4), "bound_ms": round(bnd, 4),
+            "cold_enqueue_p50_ms": round(p50(rr["cold_enqueue"]), 4),
+            "warm_enqueue_p50_ms": round(p50(rr["warm_enqueue"]), 4),
             "cold_over_bound": round(p50(rr["cold"]) / bnd, 4),
             "swap_only_gbs": round(m.total_bytes / (p50(rr["swap"]) / 1e3) / 1e9, 2),
             "forward_gflop": round(fl / 1e9, 3), "warm_forward_event_ms": round(fwd, 4),
