@@ -60,11 +60,12 @@ def out_shape(m, b):
 
 def link_rates(torch, dev):
     """(bound rate, copy-engine rate, gather-kernel rate) of the host link in GB/s: the
-    best single 1 GiB pinned copy and the best 1 GiB kernel gather from pinned memory; the
-    bound uses the higher."""
+    best single 1 GiB pinned copy and the best 1 GiB kernel gather from pinned memory (64
+    workgroups, the library's default grid and the fastest in the copy comparison); the bound
+    uses the higher."""
     import paper_2306_03622_amd as tp
     memcpy = link_peak(torch, dev)
-    gather = tp.probe_gather_h2d(1 << 30, 1024, 5)
+    gather = tp.probe_gather_h2d(1 << 30, 64, 5)
     return max(memcpy, gather), memcpy, gather
 
 
@@ -99,7 +100,7 @@ def link_peak(torch, dev, reps=10, nbytes=1 << 30):
 
 class Bench:
     def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0, flags=0, direct=None, plan="greedy",
-                 link_gbs=0.0):
+                 link_gbs=0.0, gather_wgs=0):
         import paper_2306_03622_amd as tp
         self.tp, self.torch, self.dev, self.m = tp, torch, dev, model
         self.desc = tp.ModelDesc.of(model)
@@ -107,7 +108,7 @@ class Bench:
         cm = {"memcpy": tp.TP_COPY_MEMCPY, "gather": tp.TP_COPY_GATHER, "pageable": tp.TP_COPY_PAGEABLE,
               "zero": tp.TP_COPY_ZERO}[method]
         self.rt = tp.Runtime(model.total_bytes + (1 << 20), ws, chunk_min_bytes=chunk, copy_method=cm,
-                             copy_streams=copy_streams, flags=flags,
+                             gather_wgs=gather_wgs, copy_streams=copy_streams, flags=flags,
                              direct_max_bytes=tp.DEFAULT_DIRECT if direct is None else direct,
                              plan=tp.TP_PLAN_COST if plan == "cost" else tp.TP_PLAN_GREEDY,
                              plan_batch=max(batches), link_gbs=link_gbs)
@@ -260,6 +261,39 @@ def ablation(torch, dev, chunk, link_gbs, budget_s=2.5, max_reps=20):
                          "chunks": len(b.rt.chunks(b.mid)), "bitwise_equal_to_first": same})
             b.close()
         out[f"cfg{cfg}_b{bt}"] = {"weight_bytes": m.total_bytes, "designs": rows}
+        m.drop_blob()
+    return out
+
+
+def copy_compare(torch, dev, link_copy, link_gather, wgs=(64, 256, 1024, 2048), reps=10):
+    """The copy engine against the gather kernel at several grid sizes, on the chunk plans the
+    library uses (cost plan, batch 8): swap-only and cold p50 per design, and whether the cold
+    outputs are bitwise equal to the copy engine's. Run under rocprofv3 with the kernel and
+    memory-copy traces to get the per-chunk durations of both on the device."""
+    import synth
+    import paper_2306_03622_amd as tp
+    out = {}
+    for cfg in (2, 3, 4):
+        m = synth.config_model(cfg)
+        m.blob()
+        rows, ref = [], None
+        for method, w in [("memcpy", 0)] + [("gather", v) for v in wgs]:
+            log(f"copy compare cfg{cfg}: {method} {w or ''}")
+            b = Bench(torch, dev, m, [8], method, tp.DEFAULT_CHUNK, plan="cost",
+                      link_gbs=link_gather if method == "gather" else link_copy, gather_wgs=w)
+            x, y = b.io(8, synth.CONFIG_SEEDS[cfg][1] + 8)
+            b.swap_only()
+            sw = p50([b.swap_only() for _ in range(reps)])
+            b.request(x, y, cold=True)
+            cold = p50([b.request(x, y, cold=True) for _ in range(reps)])
+            got = y.cpu()
+            same = bool(torch.equal(got, ref)) if ref is not None else True
+            ref = got if ref is None else ref
+            rows.append({"method": method, "gather_wgs": w or None, "chunks": len(b.rt.chunks(b.mid)),
+                         "swap_ms": round(sw, 3), "swap_gbs": round(m.total_bytes / (sw / 1e3) / 1e9, 2),
+                         "cold_p50_ms": round(cold, 3), "bitwise_equal_to_copy_engine": same})
+            b.close()
+        out[f"cfg{cfg}_b8"] = {"weight_bytes": m.total_bytes, "rows": rows}
         m.drop_blob()
     return out
 
@@ -576,6 +610,8 @@ def main():
     ap.add_argument("--no-tenants", action="store_true", help="skip the multi-tenant row of the default run")
     ap.add_argument("--ablation", action="store_true",
                     help="time the cold request under every swap design instead (breakdown table)")
+    ap.add_argument("--copy-compare", action="store_true",
+                    help="copy engine against the gather kernel (grid sizes 64-2048) on workloads 2-4, batch 8")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--workload", type=int, default=0, help=argparse.SUPPRESS)   # child process of --full
     ap.add_argument("--batches", default="1", help=argparse.SUPPRESS)
@@ -589,7 +625,7 @@ def main():
         sys.exit(2)
 
     children = {}
-    if not a.quick and not a.workload and not (a.tenants or a.ablation or a.pmc_workload):
+    if not a.quick and not a.workload and not (a.tenants or a.ablation or a.pmc_workload or a.copy_compare):
         # Each extra workload runs in a process of its own, started before this process touches
         # the GPU: a serving process holds one context, and after many contexts and streams in
         # one process HIP's stream-to-hardware-queue arrangement can serialise a swap behind
@@ -637,6 +673,13 @@ def main():
         link = link_peak(torch, dev)
         print(json.dumps({"ablation": ablation(torch, dev, tp.DEFAULT_CHUNK, link), "link_peak_gbs": round(link, 2),
                           "group_bytes": tp.DEFAULT_CHUNK}), flush=True)
+        return
+
+    if a.copy_compare:
+        _, link_copy, link_gather = link_rates(torch, dev)
+        print(json.dumps({"copy_compare": copy_compare(torch, dev, link_copy, link_gather),
+                          "link_copy_engine_gbs": round(link_copy, 2), "link_gather_kernel_gbs": round(link_gather, 2)}),
+              flush=True)
         return
 
     if a.pmc_workload:
