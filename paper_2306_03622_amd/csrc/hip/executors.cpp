@@ -46,6 +46,31 @@ hipError_t run_mlp(ExecCtx& x) {
   return hipSuccess;
 }
 
+bool mlp_swapin_fits(const ModelSpec& s, int batch) {
+  return s.arch == TP_ARCH_MLP && s.dtype == TP_F32 && batch <= 8 && s.dims[1] <= 1024 &&
+         s.t(0, TP_ROLE_W).offset % 16 == 0;
+}
+
+hipError_t run_mlp_swapin(ExecCtx& x, const void* host_image) {
+  const ModelSpec& s = x.m->spec;
+  const int L = s.dims[0], W = s.dims[1], act = s.dims[2], B = x.batch;
+  const uint64_t bytes = round_up((uint64_t)B * W * 4, 256);
+  char* buf[2] = {x.work, x.work + bytes};
+  void* dst = L == 1 ? x.out : buf[0];
+  TP_TRY(k::linear_f32_swap(static_cast<const float*>(x.in), B, W, W, L == 1 ? k::ACT_NONE : act,
+                            static_cast<float*>(dst), host_image, x.base, s.host_bytes, s.t(0, TP_ROLE_W).offset,
+                            s.t(0, TP_ROLE_B).offset, x.stream));
+  const void* cur = dst;
+  for (int l = 1; l < L; ++l) {
+    const bool last = l == L - 1;
+    dst = last ? x.out : buf[l & 1];
+    TP_TRY(k::linear_f32(static_cast<const float*>(cur), B, W, x.t<float>(l, TP_ROLE_W), W, x.t<float>(l, TP_ROLE_B),
+                         last ? k::ACT_NONE : act, static_cast<float*>(dst), x.stream));
+    cur = dst;
+  }
+  return hipSuccess;
+}
+
 hipError_t run_resnet(ExecCtx& x) {
   const ModelSpec& s = x.m->spec;
   const int classes = s.dims[0], image = s.dims[1], B = x.batch;

@@ -75,6 +75,7 @@ void destroy_streams(tp_ctx* c) {
   if (c->tl.start) (void)hipEventDestroy(c->tl.start);
   if (c->tl.done) (void)hipEventDestroy(c->tl.done);
   if (c->fork) (void)hipEventDestroy(c->fork);
+  if (c->claim_ev) (void)hipEventDestroy(c->claim_ev);
   for (hipEvent_t e : c->trace_ev)
     if (e) (void)hipEventDestroy(e);
 }
@@ -133,8 +134,10 @@ tp_status claim(tp_ctx* c, uint64_t off, uint64_t len) {
       keep.push_back(r);
       continue;
     }
+    // (an owner whose last use has already completed needs no wait packet on the copy stream)
     Model* m = find(c, r.model);
-    if (m && m->used) TP_HIP(hipStreamWaitEvent(c->copy[0], m->last_use, 0));
+    if (m && m->used && hipEventQuery(m->last_use) != hipSuccess)
+      TP_HIP(hipStreamWaitEvent(c->copy[0], m->last_use, 0));
     if (r.off < off) keep.push_back({r.off, off - r.off, r.model});
     if (rend > end) keep.push_back({end, rend - end, r.model});
   }
@@ -511,9 +514,46 @@ tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t ba
   // a swapping request's kernels run on the library's execution stream (see tp_create),
   // all but its last chunk's (a single-chunk request stays on the caller's stream)
   const bool forked = swapped && !direct && c->exec && m->chunks.size() > 1;
+  // a small fp32 MLP's cold request swaps it in with its own first kernel (run_mlp_swapin)
+  const bool swapin = direct && swapped && !graphs && !(c->cfg.flags & TP_FLAG_POISON) &&
+                      mlp_swapin_fits(m->spec, batch);
   hipError_t e = swapped ? hipSuccess : settle(m, stream);
   if (e != hipSuccess) {
     // fall through to the failure handling below
+  } else if (swapin) {
+    // The extent is written from the caller's stream, so that stream first waits for what the
+    // copy stream must finish before the extent may be written (the waits for its retired
+    // readers that admission enqueued there, earlier copies), unless all of it is done.
+    const hipError_t q = hipStreamQuery(c->copy[0]);
+    if (q == hipErrorNotReady) {
+      e = hipEventRecord(c->claim_ev, c->copy[0]);
+      if (e == hipSuccess) e = hipStreamWaitEvent(stream, c->claim_ev, 0);
+    } else if (q != hipSuccess) {
+      e = q;
+    }
+    if (e == hipSuccess && injected_failure(c)) e = hipErrorInvalidValue;   // counts as the copy
+    if (e == hipSuccess) {
+      Waiter w;
+      w.m = m;
+      ExecCtx x{m, c->arena + off, work, input_dev, output_dev, batch, stream, &w, make_split(work, m, batch)};
+      e = run_mlp_swapin(x, m->host_dev);
+    }
+    if (e == hipSuccess && (s = end_request(c, m, stream)) == TP_OK) {
+      // the chunk events (which later copies and moves order themselves on) complete with
+      // the request, on the copy stream: recorded on the caller's stream, the completion of
+      // that stream measured ~15 us later on MI355X
+      e = hipStreamWaitEvent(c->copy[0], c->req_done, 0);
+      for (size_t i = 0; e == hipSuccess && i < m->chunk_ev.size(); ++i) e = hipEventRecord(m->chunk_ev[i], c->copy[0]);
+      if (e == hipSuccess) return ok();
+      c->policy->evict(id);
+      (void)retire(c, id, off, m->spec.host_bytes);
+      return hip_fail(e, std::string(who) + ": swap-in events");
+    }
+    if (s != TP_OK) {
+      c->policy->evict(id);
+      (void)retire(c, id, off, m->spec.host_bytes);
+      return s;
+    }
   } else if (direct) {
     // The request's kernels read the host copy and own the host link while they run; the
     // swap is enqueued after the request's completion event, on the copy stream that
@@ -676,6 +716,7 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
 
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->req_done, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->claim_ev, hipEventDisableTiming);
   if (e == hipSuccess && (cfg->flags & TP_FLAG_TRACE)) e = hipEventCreate(&c->tl.start);
   if (e == hipSuccess && (cfg->flags & TP_FLAG_TRACE)) e = hipEventCreate(&c->tl.done);
   if (e != hipSuccess) {

@@ -115,6 +115,11 @@ struct ExecCtx {
 };
 
 hipError_t run_mlp(ExecCtx& x);
+// An fp32 MLP's cold forward that is also its swap-in: the first layer reads its weights from
+// the pinned host image and, in the same launch, the whole image is copied into the extent at
+// x.base; the other layers then run from the extent. Same results as run_mlp.
+bool mlp_swapin_fits(const ModelSpec& s, int batch);
+hipError_t run_mlp_swapin(ExecCtx& x, const void* host_image);
 hipError_t run_resnet(ExecCtx& x);
 hipError_t run_bert(ExecCtx& x);
 
@@ -129,6 +134,7 @@ struct tp_ctx {
   int ncopy = 1;
   bool own_copy = false;
   hipEvent_t fork = nullptr;                   // copy[1] starts a swap after copy[0]
+  hipEvent_t claim_ev = nullptr;               // a swap-in kernel's stream waits for copy[0]
   hipStream_t capture = nullptr;               // private stream for graph capture
   uint64_t graph_clock = 0;
   uint64_t graph_captures = 0, graph_repoints = 0;

@@ -94,6 +94,25 @@ def test_failed_background_swap_behind_direct_access():
     rt.close()
 
 
+def test_failed_swap_in_kernel_of_a_small_fp32_model():
+    # a small fp32 MLP's cold request swaps it in with its first layer kernel; that launch
+    # counts as the copy, fails, and leaves the model non-resident for the retry
+    m = synth.config_model(1)
+    x = synth.config_input(m, 2, 97)
+    rt, (mid,) = make_runtime([m], batch_max=2, direct_max_bytes=1 << 40)
+    rt.fail_copy(1)
+    _expect_hip_error(lambda: infer(rt, mid, m, x))
+    st = rt.stats()
+    assert not rt.resident(mid)
+    assert (st["misses"], st["hits"], st["resident"]) == (1, 0, 0), st
+    got = infer(rt, mid, m, x)
+    check_parity(got, m, x, 1e-4)
+    assert rt.resident(mid) and rt.stats()["misses"] == 2
+    assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob())
+    assert np.array_equal(infer(rt, mid, m, x), got)
+    rt.close()
+
+
 def test_armed_failure_counts_only_copies():
     # the countdown passes over warm requests (no copies) and fires on the next swap
     m, x = _bert(), synth.config_input(_bert(), 1, 96)

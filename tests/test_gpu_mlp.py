@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import synth
-from tests.common import check_parity, infer, log, make_runtime
+from tests.common import check_parity, infer, log, make_runtime, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -26,6 +26,36 @@ def test_cfg1_fp32_cold_then_warm():
     assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob())
     st = rt.stats()
     assert (st["hits"], st["misses"], st["bytes_swapped"]) == (1, 1, m.total_bytes)
+    rt.close()
+
+
+@pytest.mark.parametrize("width,batch", [(256, 1), (256, 8), (264, 3), (1024, 2), (256, 9), (1032, 2)])
+def test_fp32_cold_request_swaps_in_with_its_first_kernel(width, batch):
+    # Small fp32 MLPs under direct access: up to width 1024 and batch 8 the cold request's
+    # first layer kernel also copies the whole image into the arena (run_mlp_swapin); batch 9
+    # and width 1032 take direct access with the swap behind it. Two models share an arena that
+    # holds one, so each cold request reuses the extent the other just used, from a new
+    # stream (first pass) or the same one (second pass).
+    a = synth.mlp(4, width, "f32", "relu", seed=40 + width)
+    b = synth.mlp(4, width, "f32", "gelu", seed=41 + width, bias_std=0.1)
+    xa = synth.mlp_input(batch, width, "f32", 50 + batch)
+    xb = synth.mlp_input(batch, width, "f32", 60 + batch)
+    arena = max(a.total_bytes, b.total_bytes) + 4096
+    rt, (ia, ib) = make_runtime([a, b], batch_max=batch, arena_bytes=arena, direct_max_bytes=1 << 40)
+    torch, dev = torch_dev()
+    same = torch.cuda.Stream(device=dev)
+    for rep in range(2):
+        for mid, m, x in ((ia, a, xa), (ib, b, xb)):
+            log(f"fp32 swap-in: width {width} batch {batch} rep {rep} model {mid}")
+            s = same if rep else None
+            cold = infer(rt, mid, m, x, stream=s)
+            assert rt.resident(mid)
+            warm = infer(rt, mid, m, x, stream=s)
+            check_parity(cold, m, x, 1e-4)
+            assert np.array_equal(cold, warm)
+            assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob())
+    st = rt.stats()
+    assert (st["misses"], st["hits"], st["bytes_swapped"]) == (4, 4, 2 * (a.total_bytes + b.total_bytes))
     rt.close()
 
 
