@@ -6,6 +6,7 @@
 #include <algorithm>
 
 #include "../kernels/kernels.hpp"
+#include "../kernels/swapin.hpp"
 #include "runtime.hpp"
 
 namespace tp {

@@ -6,6 +6,7 @@
 
 #include "common.hpp"
 #include "kernels.hpp"
+#include "swapin.hpp"
 
 namespace tp {
 namespace k {
