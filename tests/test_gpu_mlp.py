@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import synth
-from tests.common import check_parity, infer, log, make_runtime, torch_dev
+from tests.common import check_parity, expected_host_image, infer, log, make_runtime, to_device, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -56,6 +56,49 @@ def test_fp32_cold_request_swaps_in_with_its_first_kernel(width, batch):
             assert np.array_equal(rt.extent(mid).cpu().numpy(), m.blob())
     st = rt.stats()
     assert (st["misses"], st["hits"], st["bytes_swapped"]) == (4, 4, 2 * (a.total_bytes + b.total_bytes))
+    rt.close()
+
+
+@pytest.mark.parametrize("layers,dtype", [(1, "f32"), (2, "f32"), (1, "bf16"), (2, "bf16")])
+def test_shallow_mlps(layers, dtype):
+    # one- and two-layer models (the first layer is also the last) through the swap path and
+    # under direct access (for fp32 the swap-in kernel): oracle parity, cold == warm bitwise,
+    # the extent equals the library's host image
+    m = synth.mlp(layers, 256, dtype, "relu", seed=80 + layers)
+    x = synth.mlp_input(3, 256, dtype, 81)
+    tol = 1e-4 if dtype == "f32" else 2e-2
+    for direct in (0, 1 << 40):
+        log(f"mlp {layers} x 256 {dtype}, direct limit {direct}")
+        rt, (mid,) = make_runtime([m], batch_max=3, direct_max_bytes=direct)
+        cold = infer(rt, mid, m, x)
+        warm = infer(rt, mid, m, x)
+        check_parity(cold, m, x, tol)
+        assert np.array_equal(cold, warm)
+        assert np.array_equal(rt.extent(mid).cpu().numpy(), expected_host_image(m))
+        rt.close()
+
+
+def test_infer_rejects_malformed_requests():
+    # argument errors come back as TP_E_INVAL / TP_E_NOSPC before anything is enqueued, and
+    # leave the context serving
+    import paper_2306_03622_amd as tp
+    m = synth.mlp(2, 256, "f32", "relu", seed=91)
+    x_np = synth.mlp_input(2, 256, "f32", 92)
+    rt, (mid,) = make_runtime([m], batch_max=2)
+    torch, dev = torch_dev()
+    x = to_device(x_np)
+    out = torch.empty((2, 256), dtype=torch.float32, device=dev)
+    for batch, xi, oi, want in ((0, x, out, tp.TP_E_INVAL), (2, None, out, tp.TP_E_INVAL),
+                                (2, x, None, tp.TP_E_INVAL), (64, x, out, tp.TP_E_NOSPC)):
+        with pytest.raises(tp.TorporError) as ei:
+            tp.tp_infer(rt.ctx, mid, xi, batch, oi, torch.cuda.current_stream(dev))
+        assert ei.value.status == want, (batch, ei.value)
+    with pytest.raises(tp.TorporError) as ei:
+        tp.tp_infer(rt.ctx, mid + 100, x, 2, out, torch.cuda.current_stream(dev))
+    assert ei.value.status == tp.TP_E_NOENT
+    assert rt.stats()["misses"] == 0 and not rt.resident(mid)
+    got = infer(rt, mid, m, x_np)
+    check_parity(got, m, x_np, 1e-4)
     rt.close()
 
 
