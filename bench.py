@@ -318,6 +318,24 @@ def native_alloc_us(sizes, reps=10):
     return out
 
 
+def byte_lru_hit_rate(seq, sizes, capacity):
+    """Hit rate of an LRU cache of `capacity` bytes over the request sequence with no placement
+    constraint (a model fits whenever the resident bytes allow it): the figure the arena's
+    contiguous placement loses hits against."""
+    from collections import OrderedDict
+    res, used, hits = OrderedDict(), 0, 0
+    for mid in seq:
+        if mid in res:
+            hits += 1
+            res.move_to_end(mid)
+            continue
+        while used + sizes[mid] > capacity:
+            used -= res.popitem(last=False)[1]
+        res[mid] = sizes[mid]
+        used += sizes[mid]
+    return hits / len(seq)
+
+
 def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost", queue=None, rate=50.0,
             deadline_ms=None, slo_pct=0.98, alloc="first-fit", partition_mib=0):
     """Open-loop multi-tenant run: n_models registered models of the three families, an
@@ -428,7 +446,10 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                "scheduler": sched}
     return {"metric": "multi-tenant request latency (open loop, LRU)", "unit": "ms",
             "p50_ms": round(float(np.percentile(lat, 50)), 3), "p99_ms": round(float(np.percentile(lat, 99)), 3),
-            "hit_rate": round(float(hit.mean()), 4), "requests": n_requests, "models": n_models,
+            "hit_rate": round(float(hit.mean()), 4),
+            "byte_lru_hit_rate": round(byte_lru_hit_rate([q[0] for q in reqs], {m: -(-b // 256) * 256 for m, b in
+                                                                               host_bytes.items()}, arena_gib << 30), 4),
+            "requests": n_requests, "models": n_models,
             "arena_gib": arena_gib, "registered_host_bytes": int(sum(host_bytes.values())),
             "register_s": round(reg_s, 1), "trace_s": round(float(trace.arrival_s[-1]), 2),
             "per_family": per, "arena": delta, "admission": admit, "heavy_by_family": heavy, "slo": slo,
@@ -649,7 +670,8 @@ def main():
             if out.returncode != 0:
                 raise SystemExit(f"multi-tenant workload failed with status {out.returncode}")
             t = json.loads(out.stdout.strip().splitlines()[-1])
-            children["cfg5_multi_tenant"] = {k: t[k] for k in ("p50_ms", "p99_ms", "hit_rate", "requests", "models",
+            children["cfg5_multi_tenant"] = {k: t[k] for k in ("p50_ms", "p99_ms", "hit_rate", "byte_lru_hit_rate",
+                                                               "requests", "models",
                                                                "arena_gib", "per_family", "arena", "config",
                                                                "trace_s")}
 
