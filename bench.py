@@ -339,8 +339,8 @@ def byte_lru_hit_rate(seq, sizes, capacity):
 def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost", queue=None, rate=50.0,
             deadline_ms=None, slo_pct=0.98, alloc="first-fit", partition_mib=0):
     """Open-loop multi-tenant run: n_models registered models of the three families, an
-    arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU or
-    heaviness-aware eviction, first-fit or two-tier partitioned placement (with or without
+    arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU,
+    heaviness-aware or contiguous-window eviction, first-fit or two-tier partitioned placement (with or without
     consolidation)."""
     import paper_2306_03622_amd as tp
     import synth
@@ -353,7 +353,8 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
     alloc_mode = {"first-fit": tp.TP_ALLOC_FIRST_FIT, "partition": tp.TP_ALLOC_PARTITION,
                   "consolidate": tp.TP_ALLOC_PARTITION_CONSOLIDATE}[alloc]
     rt = tp.Runtime(arena_gib << 30, ws, plan=tp.TP_PLAN_COST if plan == "cost" else tp.TP_PLAN_GREEDY,
-                    evict_policy=tp.TP_EVICT_HEAVINESS if evict == "heaviness" else tp.TP_EVICT_LRU,
+                    evict_policy={"lru": tp.TP_EVICT_LRU, "heaviness": tp.TP_EVICT_HEAVINESS,
+                                  "window": tp.TP_EVICT_LRU_WINDOW}[evict],
                     alloc=alloc_mode, partition_bytes=partition_mib << 20)
     t0 = time.perf_counter()
     ids = []
@@ -444,7 +445,7 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                "requests_within_deadline": round(float(np.mean([(r["done_ns"] - q[4]) <= deadline_ms[kinds[q[0]]] * 1e6
                                                                  for r, q in zip(res, reqs)])), 4),
                "scheduler": sched}
-    return {"metric": "multi-tenant request latency (open loop, LRU)", "unit": "ms",
+    return {"metric": f"multi-tenant request latency (open loop, {evict} eviction)", "unit": "ms",
             "p50_ms": round(float(np.percentile(lat, 50)), 3), "p99_ms": round(float(np.percentile(lat, 99)), 3),
             "hit_rate": round(float(hit.mean()), 4),
             "byte_lru_hit_rate": round(byte_lru_hit_rate([q[0] for q in reqs], {m: -(-b // 256) * 256 for m, b in
@@ -610,8 +611,8 @@ def main():
                     help="run the multi-tenant open-loop workload with this many requests instead")
     ap.add_argument("--tenant-models", type=int, default=100)
     ap.add_argument("--tenant-arena-gib", type=int, default=8)
-    ap.add_argument("--evict", choices=["lru", "heaviness"], default="lru",
-                    help="eviction policy of the multi-tenant run")
+    ap.add_argument("--evict", choices=["lru", "heaviness", "window"], default="lru",
+                    help="eviction policy of the multi-tenant run (window: TP_EVICT_LRU_WINDOW)")
     ap.add_argument("--alloc", choices=["first-fit", "partition", "consolidate"], default="first-fit",
                     help="multi-tenant arena placement: first fit, two-tier partitions, or partitions with "
                          "consolidation")

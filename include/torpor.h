@@ -164,7 +164,14 @@ enum { TP_PLAN_GREEDY = 0, TP_PLAN_COST = 1 };
  *     time; tp_set_model_class overrides this. The default separates the paper's light
  *     models, whose swapped latency is within about 1.2x of native, from its heavy one
  *     (about 3.4x; Sec. 7, table of remoting and swapping latencies). */
-enum { TP_EVICT_LRU = 0, TP_EVICT_HEAVINESS = 1 };
+/*   TP_EVICT_LRU_WINDOW (beyond the paper; first-fit placement only, partitioned placement
+ *     treats it as TP_EVICT_LRU): when no free gap fits, the victims are chosen together as
+ *     the extents that one contiguous range of the needed size overlaps, taking among the
+ *     ranges that start at the arena's base or where a resident extent ends the one whose most
+ *     recently used victim is the oldest, then the one with fewer victim bytes, then the lower
+ *     address. Least-recently-used eviction one model at a time frees space scattered over the
+ *     arena and can invalidate several models for a gap one of them would have made. */
+enum { TP_EVICT_LRU = 0, TP_EVICT_HEAVINESS = 1, TP_EVICT_LRU_WINDOW = 2 };
 enum { TP_CLASS_AUTO = 0, TP_CLASS_LIGHT = 1, TP_CLASS_HEAVY = 2 };
 /* alloc chooses where in the arena a model's extent goes:
  *   TP_ALLOC_FIRST_FIT: the lowest-addressed free gap that fits.

@@ -20,6 +20,12 @@ least recently used heavy model (policy "heaviness"; a model's class is given, a
 changed between requests). An eviction is counted as a fragmentation eviction when the
 total free space already sufficed before it. A model larger than the whole arena is refused
 with no state change.
+
+* Contiguous-window variant (policy "lru_window", beyond the paper): when no gap fits, the
+  victims are chosen together as the set of extents one contiguous range of the needed size
+  overlaps, taking the range whose most recently used victim is the oldest (then fewer victim
+  bytes, then the lower address), instead of invalidating the globally least recently used
+  model one at a time, which frees space scattered over the arena.
 """
 from __future__ import annotations
 
@@ -34,7 +40,7 @@ class NoSpace(Exception):
 
 class ArenaSim:
     def __init__(self, capacity: int, align: int = 256, policy: str = "lru"):
-        assert policy in ("lru", "heaviness")
+        assert policy in ("lru", "heaviness", "lru_window")
         self.capacity = capacity
         self.align = align
         self.policy = policy
@@ -68,6 +74,23 @@ class ArenaSim:
     def used(self) -> int:
         return sum(self.size[m] for m in self.where)
 
+    def window_victims(self, need: int) -> list:
+        """Policy "lru_window": the resident models to invalidate so that one contiguous range of
+        `need` bytes becomes free. Every range starting at address 0 or where a resident extent
+        ends is a candidate; its victims are the extents it overlaps. The candidate whose most
+        recently used victim is the oldest wins, then the one with fewer victim bytes, then the
+        lower address. Victims are returned least recently used first."""
+        ext = sorted((o, m) for m, o in self.where.items())
+        best = None
+        for start in [0] + [o + self.size[m] for o, m in ext]:
+            if start + need > self.capacity:
+                continue
+            hit = [m for o, m in ext if o < start + need and o + self.size[m] > start]
+            key = (max(self.last[m] for m in hit), sum(self.size[m] for m in hit), start)
+            if best is None or key < best[0]:
+                best = (key, hit)
+        return sorted(best[1], key=lambda m: self.last[m])
+
     def gaps(self):
         """Free gaps (offset, length) in address order."""
         out, cur = [], 0
@@ -97,6 +120,14 @@ class ArenaSim:
         self.misses += 1
         evicted = []
         off = self.first_fit(need)
+        if off is None and self.policy == "lru_window":
+            for victim in self.window_victims(need):
+                if self.capacity - self.used() >= need:
+                    self.frag_evictions += 1
+                del self.where[victim]
+                self.evictions += 1
+                evicted.append(victim)
+            off = self.first_fit(need)
         while off is None:
             victim = self.victim()
             if self.capacity - self.used() >= need:

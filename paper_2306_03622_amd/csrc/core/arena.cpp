@@ -55,6 +55,41 @@ bool Arena::first_fit(uint64_t need, uint64_t* off) const {
   return false;
 }
 
+std::vector<int32_t> Arena::window_victims(uint64_t need) const {
+  // candidate ranges start at 0 or where a resident extent ends; the victims of a range are
+  // the extents it overlaps (by_addr_ is sorted by offset, so they follow the range's start)
+  struct Key {
+    uint64_t newest, bytes, start;
+    bool operator<(const Key& o) const {
+      return newest != o.newest ? newest < o.newest : bytes != o.bytes ? bytes < o.bytes : start < o.start;
+    }
+  };
+  bool found = false;
+  Key best{};
+  size_t best_from = 0, best_to = 0;
+  for (size_t i = 0; i <= by_addr_.size(); ++i) {
+    const uint64_t start = i == 0 ? 0 : models_.at(by_addr_[i - 1]).offset + models_.at(by_addr_[i - 1]).bytes;
+    if (start + need > capacity_) continue;
+    Key k{0, 0, start};
+    size_t j = i;
+    for (; j < by_addr_.size(); ++j) {
+      const Rec& r = models_.at(by_addr_[j]);
+      if (r.offset >= start + need) break;
+      k.newest = std::max(k.newest, r.last);
+      k.bytes += r.bytes;
+    }
+    if (!found || k < best) {
+      found = true;
+      best = k;
+      best_from = i;
+      best_to = j;
+    }
+  }
+  std::vector<int32_t> v(by_addr_.begin() + (long)best_from, by_addr_.begin() + (long)best_to);
+  std::sort(v.begin(), v.end(), [&](int32_t a, int32_t b) { return models_.at(a).last < models_.at(b).last; });
+  return v;
+}
+
 int32_t Arena::victim() const {
   // least recently used resident model; under the heaviness-aware policy only light models
   // are candidates while any is resident (never the requester: it is not resident)
@@ -85,6 +120,15 @@ Arena::Decision Arena::request(int32_t id) {
   }
   ++misses_;
   uint64_t off = 0;
+  if (policy_ == TP_EVICT_LRU_WINDOW && !parts_ && !place(id, me.bytes, &off)) {
+    for (int32_t victim : window_victims(me.bytes)) {
+      if (capacity_ - used() >= me.bytes) ++frag_evictions_;
+      d.steps.push_back({false, victim, models_.at(victim).offset, 0});
+      evict(victim);
+      ++evictions_;
+      d.victims.push_back(victim);
+    }
+  }
   while (!place(id, me.bytes, &off)) {
     if (consolidate_) {
       std::vector<Partitions::Move> mv;

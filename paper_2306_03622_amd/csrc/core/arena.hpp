@@ -2,7 +2,8 @@
 // per resident model, placement in the lowest-addressed free gap that fits, and eviction
 // (invalidate only) one victim at a time until a gap fits: least recently used, or, under
 // the heaviness-aware policy, the least recently used light model while one is resident and
-// only then the least recently used heavy one. Host-only C++; the runtime attaches
+// only then the least recently used heavy one, or, under the contiguous-window policy, all
+// victims at once: those of the cheapest contiguous range. Host-only C++; the runtime attaches
 // device-side ordering (events) to the decisions made here. With partitioned placement
 // (set_partitioned) the offset comes from the two-tier partition scheme instead of first
 // fit; a size class is common while at least two registered models have it.
@@ -72,6 +73,10 @@ class Arena {
   bool first_fit(uint64_t need, uint64_t* off) const;
   bool place(int32_t id, uint64_t need, uint64_t* off);
   int32_t victim() const;
+  // TP_EVICT_LRU_WINDOW: the extents one contiguous range of `need` bytes overlaps, for the
+  // range whose most recently used victim is the oldest (then fewest victim bytes, then lowest
+  // address); least recently used first
+  std::vector<int32_t> window_victims(uint64_t need) const;
   uint64_t used() const;
 
   uint64_t capacity_, align_;

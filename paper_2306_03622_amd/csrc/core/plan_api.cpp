@@ -183,7 +183,8 @@ tp_status tph_arena_evict(tph_arena* a, int32_t id) {
 
 tp_status tph_arena_set_policy(tph_arena* a, int32_t policy) {
   if (!a) return fail(TP_E_INVAL, "NULL arena");
-  if (policy != TP_EVICT_LRU && policy != TP_EVICT_HEAVINESS) return fail(TP_E_INVAL, "unknown eviction policy");
+  if (policy != TP_EVICT_LRU && policy != TP_EVICT_HEAVINESS && policy != TP_EVICT_LRU_WINDOW)
+    return fail(TP_E_INVAL, "unknown eviction policy");
   a->a.set_policy(policy);
   return ok();
 }

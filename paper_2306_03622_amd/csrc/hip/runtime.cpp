@@ -661,7 +661,8 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
   if (cfg->plan < TP_PLAN_GREEDY || cfg->plan > TP_PLAN_COST || cfg->plan_batch < 0 || cfg->plan_batch > 65536 ||
       !(cfg->link_gbs >= 0) || cfg->link_gbs > 1e4 || !(cfg->chunk_us >= 0) || cfg->chunk_us > 1e5)
     return fail(TP_E_INVAL, "tp_create: plan, plan_batch, link_gbs or chunk_us out of range");
-  if ((cfg->evict_policy != TP_EVICT_LRU && cfg->evict_policy != TP_EVICT_HEAVINESS) || !(cfg->heavy_ratio >= 0) ||
+  if ((cfg->evict_policy != TP_EVICT_LRU && cfg->evict_policy != TP_EVICT_HEAVINESS &&
+       cfg->evict_policy != TP_EVICT_LRU_WINDOW) || !(cfg->heavy_ratio >= 0) ||
       cfg->heavy_ratio > 1e6)
     return fail(TP_E_INVAL, "tp_create: evict_policy or heavy_ratio out of range");
   if (cfg->alloc < TP_ALLOC_FIRST_FIT || cfg->alloc > TP_ALLOC_PARTITION_CONSOLIDATE ||

@@ -28,7 +28,7 @@ TP_COPY_MEMCPY, TP_COPY_GATHER, TP_COPY_PAGEABLE, TP_COPY_ZERO = 0, 1, 2, 3
 TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR, TP_FLAG_TRACE = 1, 2, 4, 8, 16, 32
 TP_FLAG_CALLER_STREAM = 64
 TP_PLAN_GREEDY, TP_PLAN_COST = 0, 1
-TP_EVICT_LRU, TP_EVICT_HEAVINESS = 0, 1
+TP_EVICT_LRU, TP_EVICT_HEAVINESS, TP_EVICT_LRU_WINDOW = 0, 1, 2
 TP_CLASS_AUTO, TP_CLASS_LIGHT, TP_CLASS_HEAVY = 0, 1, 2
 TP_ALLOC_FIRST_FIT, TP_ALLOC_PARTITION, TP_ALLOC_PARTITION_CONSOLIDATE = 0, 1, 2
 TP_QUEUE_FIFO, TP_QUEUE_SLO = 0, 1

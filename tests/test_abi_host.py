@@ -121,7 +121,8 @@ def test_workspace_grows_with_batch():
 
 def _replay(trace, sizes, cap, L, policy="lru", heavy=None):
     sim = ArenaSim(cap, align=256, policy=policy)
-    ha = tp.HostArena(cap, 256, L=L, policy=tp.TP_EVICT_HEAVINESS if policy == "heaviness" else tp.TP_EVICT_LRU)
+    ha = tp.HostArena(cap, 256, L=L, policy={"lru": tp.TP_EVICT_LRU, "heaviness": tp.TP_EVICT_HEAVINESS,
+                                             "lru_window": tp.TP_EVICT_LRU_WINDOW}[policy])
     heavy = heavy or [False] * len(sizes)
     for i, nb in enumerate(sizes):
         sim.register(i, nb, heavy=heavy[i])
@@ -295,6 +296,18 @@ def test_arena_heaviness_policy_matches_simulator(sizes, ops, frac, heavy_bits):
     trace = [(op, k % len(sizes)) for op, k in ops]
     _replay(trace, sizes, cap, tp.lib(), "heaviness", heavy)
     _replay(trace, sizes, cap, tp.host_lib(), "heaviness", heavy)
+
+
+@settings(max_examples=60, deadline=None)
+@given(sizes=st.lists(st.integers(1, 40).map(lambda x: x * 1000), min_size=2, max_size=12),
+       ops=st.lists(st.tuples(st.sampled_from(["req", "req", "req", "req", "evict"]), st.integers(0, 11)),
+                    max_size=100),
+       frac=st.floats(0.2, 1.2))
+def test_arena_window_policy_matches_simulator(sizes, ops, frac):
+    cap = max(int(sum(sizes) * frac), 256) // 256 * 256
+    trace = [(op, k % len(sizes)) for op, k in ops]
+    _replay(trace, sizes, cap, tp.lib(), "lru_window")
+    _replay(trace, sizes, cap, tp.host_lib(), "lru_window")
 
 
 def test_arena_policy_errors():

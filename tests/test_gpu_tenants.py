@@ -1,6 +1,6 @@
 """Multi-tenant open-loop replay (tp_run_trace) on the GPU, scaled down: 9 models of the
 three families, an arena that holds about a third of them, Poisson/Zipf arrivals, under
-LRU and under heaviness-aware eviction.
+LRU, heaviness-aware and contiguous-window eviction.
 
 Checks: every request's hit flag and the arena's counters equal the reference simulator
 replayed on the same request sequence; every model's first output matches the oracle."""
@@ -17,7 +17,7 @@ from tests.common import log, out_shape, to_device, torch_dev
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("policy", ["lru", "heaviness"])
+@pytest.mark.parametrize("policy", ["lru", "heaviness", "lru_window"])
 def test_tenant_trace_lru_and_first_outputs(policy):
     torch, dev = torch_dev()
     specs = synth.tenant_models(9)
@@ -25,7 +25,8 @@ def test_tenant_trace_lru_and_first_outputs(policy):
     trace = synth.tenant_trace(120, n_models=9)
     cap = (models[0].total_bytes + models[1].total_bytes + models[2].total_bytes) // 256 * 256 + (64 << 20)
     ws = max(tp.tp_workspace_bytes(tp.ModelDesc.of(m), 1) for m in models)
-    rt = tp.Runtime(cap, ws, evict_policy=tp.TP_EVICT_HEAVINESS if policy == "heaviness" else tp.TP_EVICT_LRU)
+    rt = tp.Runtime(cap, ws, evict_policy={"lru": tp.TP_EVICT_LRU, "heaviness": tp.TP_EVICT_HEAVINESS,
+                                           "lru_window": tp.TP_EVICT_LRU_WINDOW}[policy])
     ids = [rt.register(tp.ModelDesc.of(m), m.blob()) for m in models]
     heavy = [bool(rt.info(i)["heavy"]) for i in ids]
     # the cost model classes the transfer-bound families heavy and ResNet-50 (whose compute

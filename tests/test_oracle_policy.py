@@ -149,6 +149,30 @@ def test_best_grouping_hand_worked():
 
 # ------------------------------------------------------------------ heaviness-aware eviction
 
+def test_window_policy_hand_worked():
+    # capacity 100: a, b, c of 30 at 0, 30, 60, recency b < c < a, then d (40) with 10 free at 90.
+    # LRU one at a time: b, then c (free [30, 100)), d at 30. The window policy's candidate
+    # ranges start at 0 (overlaps a: newest victim a), 30 (b and c: newest c, 60 bytes), 60
+    # (c: newest c, 30 bytes), 90 (does not fit): c alone, d at 60.
+    for policy, want_off, want_ev in (("lru", 30, ["b", "c"]), ("lru_window", 60, ["c"])):
+        a = ArenaSim(100, align=1, policy=policy)
+        for m, nb in (("a", 30), ("b", 30), ("c", 30), ("d", 40)):
+            a.register(m, nb)
+        for m in ("a", "b", "c", "a"):
+            a.request(m)
+        assert a.request("d") == {"hit": False, "offset": want_off, "evicted": want_ev}
+        assert a.stats()["evictions"] == len(want_ev)
+    # ties on the newest victim go to fewer victim bytes, then to the lower address
+    a = ArenaSim(90, align=1, policy="lru_window")
+    for m, nb in (("p", 20), ("q", 20), ("r", 20), ("s", 30), ("t", 40)):
+        a.register(m, nb)
+    for m in ("p", "q", "r", "s"):
+        a.request(m)                      # p 0, q 20, r 40, s 60; full
+    # t (40): ranges 0 (p, q: newest q), 20 (q, r: newest r), 40 (r, s: newest s), 60 (s,
+    # then past the end: does not fit) -> newest q is the oldest -> p and q
+    assert a.request("t") == {"hit": False, "offset": 0, "evicted": ["p", "q"]}
+
+
 def test_heaviness_policy_evicts_light_first_then_lru_among_heavy():
     a = ArenaSim(1000, align=100, policy="heaviness")
     a.register(0, 300, heavy=True)
