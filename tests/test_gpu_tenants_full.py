@@ -3,8 +3,8 @@
 100 registered models (model i: the 24 x 4096 MLP, ResNet-50 or BERT-base by i mod 3, weight
 seed 1000 + i; 36.26 GB of pinned host copies), an 8 GiB arena, 3000 requests at batch 1 with
 Poisson arrivals at 50 per second and Zipf(1.1) popularity, replayed open loop by
-tp_run_trace under LRU eviction and first-fit placement; every request brings input and
-output buffers of its own. Checks:
+tp_run_trace under LRU or contiguous-window eviction and first-fit placement; every request
+brings input and output buffers of its own. Checks:
   * every request's hit flag, and the arena's counters, equal the oracle's arena simulator
     replayed on the same request sequence (paper Sec. 4.3 "Model eviction", Sec. 5.4 LRU);
   * the first request of every requested model matches the oracle's float64 forward pass
@@ -12,8 +12,8 @@ output buffers of its own. Checks:
   * warm requests capture a graph only at the first hit after a swap to a new extent; every
     other hit repoints a cached graph at its own buffers.
 It writes a summary (latency, hit rates beside a byte-capacity LRU without contiguity, the
-achieved errors) to gpurun_out/tenants_full.json. It takes about four minutes, so it runs
-only when TP_FULL_TENANTS=1 is set."""
+achieved errors) to gpurun_out/tenants_full_<policy>.json. It takes about four minutes per
+policy, so it runs only when TP_FULL_TENANTS=1 is set."""
 import json
 import os
 import time
@@ -52,7 +52,8 @@ def byte_lru_hits(sizes, sequence, capacity):
     return hits
 
 
-def test_full_size_trace_matches_oracle():
+@pytest.mark.parametrize("policy", ["lru", "lru_window"])
+def test_full_size_trace_matches_oracle(policy):
     torch, dev = torch_dev()
     specs = synth.tenant_models(N_MODELS)
     trace = synth.tenant_trace(N_REQUESTS, n_models=N_MODELS)
@@ -61,7 +62,8 @@ def test_full_size_trace_matches_oracle():
         first.setdefault(int(k), r)
     log(f"{len(first)} of {N_MODELS} models are requested")
     ws = max(tp.tp_workspace_bytes(tp.ModelDesc.of(synth.config_model(c, 0)), 1) for c in (2, 3, 4))
-    rt = tp.Runtime(ARENA, ws, plan=tp.TP_PLAN_COST)
+    rt = tp.Runtime(ARENA, ws, plan=tp.TP_PLAN_COST,
+                    evict_policy=tp.TP_EVICT_LRU_WINDOW if policy == "lru_window" else tp.TP_EVICT_LRU)
     ids, sizes, kinds, expected, inputs = [], {}, {}, {}, {}
     t0 = time.perf_counter()
     for i, m in synth.build_models(specs, workers=16):
@@ -94,7 +96,7 @@ def test_full_size_trace_matches_oracle():
     assert all(q["status"] == 0 for q in res)
     st = rt.stats()
 
-    sim = ArenaSim(ARENA, align=256)
+    sim = ArenaSim(ARENA, align=256, policy=policy)
     for mid in ids:
         sim.register(mid, sizes[mid])
     decisions = [sim.request(q[0]) for q in reqs]
@@ -141,7 +143,8 @@ def test_full_size_trace_matches_oracle():
     lru = byte_lru_hits(sizes, [rq[0] for rq in reqs], ARENA)
     summary = {
         "workload": f"{N_MODELS} models (24x4096 MLP / ResNet-50 / BERT-base by index mod 3), 8 GiB arena, "
-                    f"{N_REQUESTS} requests, Poisson 50/s, Zipf(1.1), batch 1, LRU, first fit",
+                    f"{N_REQUESTS} requests, Poisson 50/s, Zipf(1.1), batch 1, first fit",
+        "eviction": policy,
         "models_requested": len(first), "models_checked_against_oracle": len(errors),
         "worst_normwise_error_by_family": worst, "tolerance": 2e-2,
         "p50_ms": round(float(np.percentile(lat, 50)), 3), "p99_ms": round(float(np.percentile(lat, 99)), 3),
@@ -161,6 +164,6 @@ def test_full_size_trace_matches_oracle():
     log(json.dumps(summary))
     out_dir = os.path.dirname(PARITY_LOG)
     os.makedirs(out_dir, exist_ok=True)
-    with open(os.path.join(out_dir, "tenants_full.json"), "w") as f:
+    with open(os.path.join(out_dir, f"tenants_full_{policy}.json"), "w") as f:
         json.dump(summary, f, indent=1)
     rt.close()
