@@ -472,10 +472,11 @@ __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
       if (i < nv) reinterpret_cast<uint4*>(xl)[i] = wv[u];
     }
     __syncthreads();
-    for (int i = tid; i < 64 * KP; i += 256) {
-      const int n = i / KP, k = i - n * KP;
-      wl[n * SC_KS + k] = (n < a.N && k < K) ? xl[n * K + k] : (uint16_t)0;
-    }
+    // four threads per weight row, each taking every fourth k: no division by the run-time
+    // row length in the index arithmetic
+    const int wn = tid >> 2;
+    for (int k = tid & 3; k < KP; k += 4)
+      wl[wn * SC_KS + k] = (wn < a.N && k < K) ? xl[wn * K + k] : (uint16_t)0;
   }
   const int p = wave * 16 + (lane & 15), q = lane >> 4;
   const int pofs = p * a.stride * C;
