@@ -389,104 +389,95 @@ void k_gemm(GemmArgs a) {
 
 // Convolutions whose input has at most 4 channels (the ResNet stem: 7 x 7, stride 2,
 // 3 channels), where an im2col row is not made of 16-byte runs. A workgroup owns all
-// (<= 64) output channels and SC_W consecutive output pixels of `rows` output rows of one
-// sample. The weights are brought in once per workgroup as 16-byte loads of the flat
-// [N][K] array and re-laid out in LDS with rows zero-padded to a multiple of 32. Per
-// output row, the KH input rows that its windows touch are staged in LDS (zero where a
-// window leaves the image), every global load of a stage issued before the first LDS
-// store, and the next row's loads are issued before this row's multiplications. Wave w
-// multiplies the 16 pixels 16w .. 16w+15 against every output channel: the activation
-// operand is gathered element by element from the staged rows (k = (kh * KW + kw) * C +
-// c, so a k-run inside one filter row is a run of a staged input row), the weight
-// operand read as 16-byte vectors.
-constexpr int SC_W = 64, SC_MAXC = 4, SC_MAXK = 7, SC_MAXS = 2;
+// (<= 64) output channels and SC_W consecutive output pixels of `rows` consecutive output
+// rows of one sample. Its loads are issued together before any LDS store, so it waits for
+// memory once: the weights as 16-byte loads of the flat [N][K] array (re-laid out in LDS
+// with rows zero-padded to a multiple of 32), and every input row the windows of its output
+// rows touch (zero outside the image). Wave w multiplies the 16 pixels 16w .. 16w+15 of each
+// output row against every output channel: the activation operand is gathered element by
+// element from the staged rows (k = (kh * KW + kw) * C + c, so a k-run inside one filter row
+// is a run of a staged input row), the weight operand read as 16-byte vectors.
+constexpr int SC_W = 64, SC_MAXC = 4, SC_MAXK = 7, SC_MAXS = 2, SC_MAXR = 8;
 constexpr int SC_KP = ((SC_MAXK * SC_MAXK * SC_MAXC + 31) / 32) * 32;   // 224
 constexpr int SC_KS = SC_KP + 8;                                        // weight row stride in LDS
 constexpr int SC_RL = ((SC_W - 1) * SC_MAXS + SC_MAXK) * SC_MAXC;       // longest staged input row
+constexpr int SC_MAXIN = (SC_MAXR - 1) * SC_MAXS + SC_MAXK;             // input rows of SC_MAXR output rows
 constexpr int SC_PER = (SC_RL + 255) / 256;                             // staged elements per thread and row
 constexpr int SC_WV = (64 * SC_MAXK * SC_MAXK * SC_MAXC * 2 / 16 + 255) / 256;  // 16-byte weight loads per thread
+// the staged input rows, or the flat weights (with the tail of their last 16-byte vector) on their way to wl
+constexpr int SC_XL = SC_MAXIN * SC_RL > 64 * SC_MAXK * SC_MAXK * SC_MAXC + 8 ? SC_MAXIN * SC_RL
+                                                                            : 64 * SC_MAXK * SC_MAXK * SC_MAXC + 8;
 
-template <int C>
-struct SmallConvRow {
-  uint16_t v[SC_MAXK][SC_PER];
-  // loads of output row oh's input window rows (zero outside the image or beyond KH)
-  __device__ void load(const GemmArgs& a, int b, int oh, int iw0, int KH, int rl, int tid) {
-    const int ih0 = oh * a.stride - a.pad;
-#pragma unroll
-    for (int kh = 0; kh < SC_MAXK; ++kh) {
-      const int ih = ih0 + kh;
-      const bool hin = kh < KH && ih >= 0 && ih < a.H;
-      const uint16_t* xrow = a.x + ((size_t)b * a.H + (hin ? ih : 0)) * a.W * C;
-#pragma unroll
-      for (int u = 0; u < SC_PER; ++u) {
-        const int j = u * 256 + tid;
-        const int col = j / C, iw = iw0 + col;
-        v[kh][u] = (hin && j < rl && iw >= 0 && iw < a.W) ? xrow[(size_t)iw * C + (j - col * C)] : (uint16_t)0;
-      }
-    }
-  }
-  __device__ void store(uint16_t* xl, int KH, int rl, int tid) const {
-#pragma unroll
-    for (int kh = 0; kh < SC_MAXK; ++kh)
-#pragma unroll
-      for (int u = 0; u < SC_PER; ++u) {
-        const int j = u * 256 + tid;
-        if (kh < KH && j < rl) xl[kh * rl + j] = v[kh][u];
-      }
-  }
-};
-
-template <int C>
+// IN: input rows staged at most (SC_MAXK for one output row per workgroup, SC_MAXIN for up to
+// SC_MAXR), so that a workgroup of one output row computes no addresses for rows it never loads
+template <int C, int IN>
 __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
   __shared__ __align__(16) uint16_t wl[64 * SC_KS];
-  __shared__ __align__(16) uint16_t xl[SC_MAXK * SC_RL > 64 * SC_KP ? SC_MAXK * SC_RL : 64 * SC_KP];
+  __shared__ __align__(16) uint16_t xl[SC_XL];
   __shared__ __align__(16) int koff[SC_KP];   // staged-row offset of window element k, -1 beyond K
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int KW = a.KW, K = a.K, KWC = KW * C, KH = K / KWC;
   const int KP = (K + 31) & ~31;
   const int ow0 = blockIdx.x * SC_W, b = blockIdx.z;
   const int rl = ((SC_W - 1) * a.stride + KW) * C;
+  const int oh_first = blockIdx.y * rows;
+  const int nrows = min(rows, a.Ho - oh_first);          // >= 1: the grid covers Ho exactly
+  const int nin = (nrows - 1) * a.stride + KH;            // input rows staged
+  const int ih_first = oh_first * a.stride - a.pad, iw0 = ow0 * a.stride - a.pad;
   for (int k = tid; k < KP; k += 256) {
     const int kh = k / KWC;
     koff[k] = k < K ? kh * rl + (k - kh * KWC) : -1;
   }
-  const int iw0 = ow0 * a.stride - a.pad;
-  const int oh_first = blockIdx.y * rows;
-  SmallConvRow<C> nxt;
-  {
-    // the flat weights through xl (all loads first), then padded rows into wl
-    const int nw = a.N * K;                       // elements; the array starts 16-byte aligned
-    const int nv = (nw * 2 + 15) / 16;
-    uint4 wv[SC_WV];
+  // every global load first: the flat weights, then the staged input rows
+  const int nw = a.N * K;                         // weight elements; the array starts 16-byte aligned
+  const int nv = (nw * 2 + 15) / 16;
+  uint4 wv[SC_WV];
 #pragma unroll
-    for (int u = 0; u < SC_WV; ++u) {
-      const int i = u * 256 + tid;
-      // the last vector may extend past the array end; it stays inside the 256-byte
-      // aligned allocation unit of the weight tensor
-      wv[u] = i < nv ? reinterpret_cast<const uint4*>(a.w)[i] : make_uint4(0, 0, 0, 0);
-    }
-    nxt.load(a, b, oh_first, iw0, KH, rl, tid);
-#pragma unroll
-    for (int u = 0; u < SC_WV; ++u) {
-      const int i = u * 256 + tid;
-      if (i < nv) reinterpret_cast<uint4*>(xl)[i] = wv[u];
-    }
-    __syncthreads();
-    // four threads per weight row, each taking every fourth k: no division by the run-time
-    // row length in the index arithmetic
-    const int wn = tid >> 2;
-    for (int k = tid & 3; k < KP; k += 4)
-      wl[wn * SC_KS + k] = (wn < a.N && k < K) ? xl[wn * K + k] : (uint16_t)0;
+  for (int u = 0; u < SC_WV; ++u) {
+    const int i = u * 256 + tid;
+    // the last vector may extend past the array end; it stays inside the 256-byte
+    // aligned allocation unit of the weight tensor
+    wv[u] = i < nv ? reinterpret_cast<const uint4*>(a.w)[i] : make_uint4(0, 0, 0, 0);
   }
+  static_assert(IN <= SC_MAXIN, "staged rows");
+  uint16_t xv[IN][SC_PER];
+#pragma unroll
+  for (int r = 0; r < IN; ++r) {
+    const int ih = ih_first + r;
+    const bool hin = r < nin && ih >= 0 && ih < a.H;
+    const uint16_t* xrow = a.x + ((size_t)b * a.H + (hin ? ih : 0)) * a.W * C;
+#pragma unroll
+    for (int u = 0; u < SC_PER; ++u) {
+      const int j = u * 256 + tid;
+      const int col = j / C, iw = iw0 + col;
+      xv[r][u] = (hin && j < rl && iw >= 0 && iw < a.W) ? xrow[(size_t)iw * C + (j - col * C)] : (uint16_t)0;
+    }
+  }
+  // the flat weights through xl, then padded rows into wl (four threads per row, every fourth
+  // k: no division by the run-time row length), then the input rows into xl
+#pragma unroll
+  for (int u = 0; u < SC_WV; ++u) {
+    const int i = u * 256 + tid;
+    if (i < nv) reinterpret_cast<uint4*>(xl)[i] = wv[u];
+  }
+  __syncthreads();
+  const int wn = tid >> 2;
+  for (int k = tid & 3; k < KP; k += 4)
+    wl[wn * SC_KS + k] = (wn < a.N && k < K) ? xl[wn * K + k] : (uint16_t)0;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < IN; ++r)
+#pragma unroll
+    for (int u = 0; u < SC_PER; ++u) {
+      const int j = u * 256 + tid;
+      if (r < nin && j < rl) xl[r * rl + j] = xv[r][u];
+    }
+  __syncthreads();
+
   const int p = wave * 16 + (lane & 15), q = lane >> 4;
   const int pofs = p * a.stride * C;
-  for (int r = 0; r < rows; ++r) {
-    const int oh = oh_first + r;
-    if (oh >= a.Ho) break;
-    __syncthreads();                  // wl written; every read of xl (weights or last row) done
-    nxt.store(xl, KH, rl, tid);
-    __syncthreads();
-    if (r + 1 < rows && oh + 1 < a.Ho) nxt.load(a, b, oh + 1, iw0, KH, rl, tid);
+  for (int r = 0; r < nrows; ++r) {
+    const int oh = oh_first + r, rbase = r * a.stride * rl + pofs;
     f32x4 acc[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -500,7 +491,7 @@ __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
       uint32_t bw[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const uint32_t v = xl[(o[e] < 0 ? 0 : o[e]) + pofs];
+        const uint32_t v = xl[(o[e] < 0 ? 0 : o[e]) + rbase];
         bw[e >> 1] |= (o[e] < 0 ? 0u : v) << (16 * (e & 1));
       }
       const uint4 bv = make_uint4(bw[0], bw[1], bw[2], bw[3]);
@@ -700,13 +691,15 @@ hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16
       a.K <= SC_KP) {
     // enough workgroups to fill the chip, each reusing its staged weights over `rows` rows
     const int segs = (Wo + SC_W - 1) / SC_W;
-    const int rows = max(1, min(8, segs * Ho * B / 448));
+    const int rows = max(1, min(SC_MAXR, segs * Ho * B / 448));
     dim3 grid(segs, (Ho + rows - 1) / rows, B);
+    auto go = [&](auto kern) { (void)launch(kern, grid, dim3(256), 0, s, a, rows); };
+    const bool one = rows == 1;
     switch (C) {
-      case 1: (void)launch(k_conv_smallc<1>, grid, dim3(256), 0, s, a, rows); break;
-      case 2: (void)launch(k_conv_smallc<2>, grid, dim3(256), 0, s, a, rows); break;
-      case 3: (void)launch(k_conv_smallc<3>, grid, dim3(256), 0, s, a, rows); break;
-      default: (void)launch(k_conv_smallc<4>, grid, dim3(256), 0, s, a, rows); break;
+      case 1: one ? go(k_conv_smallc<1, SC_MAXK>) : go(k_conv_smallc<1, SC_MAXIN>); break;
+      case 2: one ? go(k_conv_smallc<2, SC_MAXK>) : go(k_conv_smallc<2, SC_MAXIN>); break;
+      case 3: one ? go(k_conv_smallc<3, SC_MAXK>) : go(k_conv_smallc<3, SC_MAXIN>); break;
+      default: one ? go(k_conv_smallc<4, SC_MAXK>) : go(k_conv_smallc<4, SC_MAXIN>); break;
     }
     return hipGetLastError();
   }
