@@ -405,12 +405,18 @@ constexpr int SC_MAXIN = (SC_MAXR - 1) * SC_MAXS + SC_MAXK;             // input
 constexpr int SC_PER = (SC_RL + 255) / 256;                             // staged elements per thread and row
 constexpr int SC_WV = (64 * SC_MAXK * SC_MAXK * SC_MAXC * 2 / 16 + 255) / 256;  // 16-byte weight loads per thread
 // the staged input rows, or the flat weights (with the tail of their last 16-byte vector) on their way to wl
-constexpr int SC_XL = SC_MAXIN * SC_RL > 64 * SC_MAXK * SC_MAXK * SC_MAXC + 8 ? SC_MAXIN * SC_RL
-                                                                            : 64 * SC_MAXK * SC_MAXK * SC_MAXC + 8;
+constexpr int SC_RLV = (SC_MAXC * 2 + SC_RL + 7) / 8 * 8;   // staged row stride of the vector path (below)
+constexpr int SC_XL = SC_MAXIN * SC_RLV > 64 * SC_MAXK * SC_MAXK * SC_MAXC + 8 ? SC_MAXIN * SC_RLV
+                                                                             : 64 * SC_MAXK * SC_MAXK * SC_MAXC + 8;
 
 // IN: input rows staged at most (SC_MAXK for one output row per workgroup, SC_MAXIN for up to
-// SC_MAXR), so that a workgroup of one output row computes no addresses for rows it never loads
-template <int C, int IN>
+// SC_MAXR), so that a workgroup of one output row computes no addresses for rows it never loads.
+// VX: image rows of a multiple of 8 elements from a 16-byte aligned image are staged as whole
+// 16-byte vectors (the window's first element then sits `sh` elements into the staged row;
+// vectors outside the image read as zero, and the image's edges fall on vector boundaries), so
+// that staging costs a few vector loads per thread instead of element loads with their
+// addressing; otherwise element by element.
+template <int C, int IN, bool VX>
 __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
   __shared__ __align__(16) uint16_t wl[64 * SC_KS];
   __shared__ __align__(16) uint16_t xl[SC_XL];
@@ -424,9 +430,15 @@ __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
   const int nrows = min(rows, a.Ho - oh_first);          // >= 1: the grid covers Ho exactly
   const int nin = (nrows - 1) * a.stride + KH;            // input rows staged
   const int ih_first = oh_first * a.stride - a.pad, iw0 = ow0 * a.stride - a.pad;
+  // vector path: staged row r holds image-row elements from vector vfirst on, so the window's
+  // element j sits at sh + j; element path: at j
+  const int vfirst = (iw0 * C) >> 3;                      // floor division (iw0 may be negative)
+  const int sh = VX ? iw0 * C - vfirst * 8 : 0;
+  const int rs = VX ? (sh + rl + 7) & ~7 : rl;            // staged row stride
+  const int nvec = rs >> 3;
   for (int k = tid; k < KP; k += 256) {
     const int kh = k / KWC;
-    koff[k] = k < K ? kh * rl + (k - kh * KWC) : -1;
+    koff[k] = k < K ? kh * rs + (k - kh * KWC) : -1;
   }
   // every global load first: the flat weights, then the staged input rows
   const int nw = a.N * K;                         // weight elements; the array starts 16-byte aligned
@@ -440,17 +452,36 @@ __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
     wv[u] = i < nv ? reinterpret_cast<const uint4*>(a.w)[i] : make_uint4(0, 0, 0, 0);
   }
   static_assert(IN <= SC_MAXIN, "staged rows");
-  uint16_t xv[IN][SC_PER];
+  static_assert(SC_RLV / 8 <= 128, "two vectors per lane cover a staged row");
+  constexpr int XE = VX ? 1 : IN, XU = VX ? 1 : SC_PER;       // element path: rows x elements per thread
+  constexpr int XR = VX ? (IN + 3) / 4 : 1;                   // vector path: rows per wave (row r = wave + 4 i)
+  uint16_t xv[XE][XU];
+  uint4 xq[XR][2];
+  if constexpr (VX) {
+    const int rowv = (a.W * C) >> 3;                        // vectors per image row
 #pragma unroll
-  for (int r = 0; r < IN; ++r) {
-    const int ih = ih_first + r;
-    const bool hin = r < nin && ih >= 0 && ih < a.H;
-    const uint16_t* xrow = a.x + ((size_t)b * a.H + (hin ? ih : 0)) * a.W * C;
+    for (int i = 0; i < XR; ++i) {
+      const int r = wave + 4 * i, ih = ih_first + r;
+      const bool hin = r < nin && ih >= 0 && ih < a.H;
+      const uint4* xrow = reinterpret_cast<const uint4*>(a.x + ((size_t)b * a.H + (hin ? ih : 0)) * a.W * C);
 #pragma unroll
-    for (int u = 0; u < SC_PER; ++u) {
-      const int j = u * 256 + tid;
-      const int col = j / C, iw = iw0 + col;
-      xv[r][u] = (hin && j < rl && iw >= 0 && iw < a.W) ? xrow[(size_t)iw * C + (j - col * C)] : (uint16_t)0;
+      for (int h = 0; h < 2; ++h) {
+        const int vi = lane + 64 * h, gv = vfirst + vi;
+        xq[i][h] = (hin && vi < nvec && gv >= 0 && gv < rowv) ? xrow[gv] : make_uint4(0, 0, 0, 0);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < IN; ++r) {
+      const int ih = ih_first + r;
+      const bool hin = r < nin && ih >= 0 && ih < a.H;
+      const uint16_t* xrow = a.x + ((size_t)b * a.H + (hin ? ih : 0)) * a.W * C;
+#pragma unroll
+      for (int u = 0; u < SC_PER; ++u) {
+        const int j = u * 256 + tid;
+        const int col = j / C, iw = iw0 + col;
+        xv[r][u] = (hin && j < rl && iw >= 0 && iw < a.W) ? xrow[(size_t)iw * C + (j - col * C)] : (uint16_t)0;
+      }
     }
   }
   // the flat weights through xl, then padded rows into wl (four threads per row, every fourth
@@ -465,19 +496,31 @@ __global__ __launch_bounds__(256) void k_conv_smallc(GemmArgs a, int rows) {
   for (int k = tid & 3; k < KP; k += 4)
     wl[wn * SC_KS + k] = (wn < a.N && k < K) ? xl[wn * K + k] : (uint16_t)0;
   __syncthreads();
+  if constexpr (VX) {
 #pragma unroll
-  for (int r = 0; r < IN; ++r)
+    for (int i = 0; i < XR; ++i) {
+      const int r = wave + 4 * i;
 #pragma unroll
-    for (int u = 0; u < SC_PER; ++u) {
-      const int j = u * 256 + tid;
-      if (r < nin && j < rl) xl[r * rl + j] = xv[r][u];
+      for (int h = 0; h < 2; ++h) {
+        const int vi = lane + 64 * h;
+        if (r < nin && vi < nvec) *reinterpret_cast<uint4*>(&xl[r * rs + vi * 8]) = xq[i][h];
+      }
     }
+  } else {
+#pragma unroll
+    for (int r = 0; r < IN; ++r)
+#pragma unroll
+      for (int u = 0; u < SC_PER; ++u) {
+        const int j = u * 256 + tid;
+        if (r < nin && j < rl) xl[r * rs + j] = xv[r][u];
+      }
+  }
   __syncthreads();
 
   const int p = wave * 16 + (lane & 15), q = lane >> 4;
   const int pofs = p * a.stride * C;
   for (int r = 0; r < nrows; ++r) {
-    const int oh = oh_first + r, rbase = r * a.stride * rl + pofs;
+    const int oh = oh_first + r, rbase = r * a.stride * rs + pofs + sh;
     f32x4 acc[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -694,12 +737,16 @@ hipError_t conv_bf16(const uint16_t* x, int B, int H, int W, int C, const uint16
     const int rows = max(1, min(SC_MAXR, segs * Ho * B / 448));
     dim3 grid(segs, (Ho + rows - 1) / rows, B);
     auto go = [&](auto kern) { (void)launch(kern, grid, dim3(256), 0, s, a, rows); };
-    const bool one = rows == 1;
-    switch (C) {
-      case 1: one ? go(k_conv_smallc<1, SC_MAXK>) : go(k_conv_smallc<1, SC_MAXIN>); break;
-      case 2: one ? go(k_conv_smallc<2, SC_MAXK>) : go(k_conv_smallc<2, SC_MAXIN>); break;
-      case 3: one ? go(k_conv_smallc<3, SC_MAXK>) : go(k_conv_smallc<3, SC_MAXIN>); break;
-      default: one ? go(k_conv_smallc<4, SC_MAXK>) : go(k_conv_smallc<4, SC_MAXIN>); break;
+    const bool one = rows == 1, vx = (W * C) % 8 == 0 && ((uintptr_t)x & 15) == 0;
+    // the vector path for the channel counts of network stems (RGB, RGBA), the element path
+    // otherwise
+    if (vx && C == 3) one ? go(k_conv_smallc<3, SC_MAXK, true>) : go(k_conv_smallc<3, SC_MAXIN, true>);
+    else if (vx && C == 4) one ? go(k_conv_smallc<4, SC_MAXK, true>) : go(k_conv_smallc<4, SC_MAXIN, true>);
+    else switch (C) {
+      case 1: one ? go(k_conv_smallc<1, SC_MAXK, false>) : go(k_conv_smallc<1, SC_MAXIN, false>); break;
+      case 2: one ? go(k_conv_smallc<2, SC_MAXK, false>) : go(k_conv_smallc<2, SC_MAXIN, false>); break;
+      case 3: one ? go(k_conv_smallc<3, SC_MAXK, false>) : go(k_conv_smallc<3, SC_MAXIN, false>); break;
+      default: one ? go(k_conv_smallc<4, SC_MAXK, false>) : go(k_conv_smallc<4, SC_MAXIN, false>); break;
     }
     return hipGetLastError();
   }

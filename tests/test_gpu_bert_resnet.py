@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 import synth
-from tests.common import check_parity, infer, log, make_runtime
+from tests.common import check_parity, infer, log, make_runtime, out_shape, to_device, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -64,6 +64,31 @@ def test_resnet_small_images(image, batch):
     rt, (mid,) = make_runtime([m], batch_max=batch)
     log(f"resnet image {image} batch {batch}")
     check_parity(infer(rt, mid, m, x), m, x, 2e-2)
+    rt.close()
+
+
+@pytest.mark.parametrize("image,batch", [(64, 2), (224, 1), (224, 8)])
+def test_resnet_input_alignment_paths(image, batch):
+    # the stem stages its input rows as 16-byte vectors when the image is 16-byte aligned and
+    # element by element otherwise: an input one element into a buffer takes the second path;
+    # both give the oracle's result and the same bits
+    torch, dev = torch_dev()
+    m = synth.resnet50(seed=53, classes=10, image=image)
+    x = synth.resnet_input(batch, 54, image=image)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    aligned = infer(rt, mid, m, x)
+    check_parity(aligned, m, x, 2e-2)
+    flat = to_device(x).reshape(-1)
+    buf = torch.zeros(flat.numel() + 8, dtype=flat.dtype, device=dev)
+    buf[1:1 + flat.numel()] = flat
+    xs = buf[1:1 + flat.numel()].view(x.shape)
+    assert xs.data_ptr() % 16 == 2
+    out = torch.full(out_shape(m, batch), float("nan"), dtype=torch.float32, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    rt.infer(mid, xs, out, stream=s)
+    s.synchronize()
+    assert np.array_equal(out.cpu().numpy(), aligned)
     rt.close()
 
 
