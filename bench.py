@@ -100,20 +100,38 @@ def link_peak(torch, dev, reps=10, nbytes=1 << 30):
 
 class Bench:
     def __init__(self, torch, dev, model, batches, method, chunk, copy_streams=0, flags=0, direct=None, plan="greedy",
-                 link_gbs=0.0, gather_wgs=0):
+                 link_gbs=0.0, gather_wgs=0, spacers=0):
         import paper_2306_03622_amd as tp
+        import synth
         self.tp, self.torch, self.dev, self.m = tp, torch, dev, model
         self.desc = tp.ModelDesc.of(model)
         ws = tp.tp_workspace_bytes(self.desc, max(batches))
+        # spacers: small models registered beside the measured one, swapped in below it to
+        # place it at another arena offset
+        spacer = synth.mlp(2, 256, "bf16", "gelu", seed=5) if spacers else None
+        extra = spacers * (spacer.total_bytes + 4096) if spacers else 0
         cm = {"memcpy": tp.TP_COPY_MEMCPY, "gather": tp.TP_COPY_GATHER, "pageable": tp.TP_COPY_PAGEABLE,
               "zero": tp.TP_COPY_ZERO}[method]
-        self.rt = tp.Runtime(model.total_bytes + (1 << 20), ws, chunk_min_bytes=chunk, copy_method=cm,
+        self.rt = tp.Runtime(model.total_bytes + extra + (1 << 20), ws, chunk_min_bytes=chunk, copy_method=cm,
                              gather_wgs=gather_wgs, copy_streams=copy_streams, flags=flags,
                              direct_max_bytes=tp.DEFAULT_DIRECT if direct is None else direct,
                              plan=tp.TP_PLAN_COST if plan == "cost" else tp.TP_PLAN_GREEDY,
                              plan_batch=max(batches), link_gbs=link_gbs)
         self.mid = self.rt.register(self.desc, model.blob())
+        self.spacers = [self.rt.register(tp.ModelDesc.of(spacer), spacer.blob()) for _ in range(spacers)]
         self.stream = torch.cuda.Stream(device=dev)
+
+    def place(self, k):
+        """Makes the model resident above the first k spacers (another arena offset for each
+        k), with nothing of it in flight."""
+        self.rt.evict(self.mid)
+        for j, sp in enumerate(self.spacers):
+            self.rt.evict(sp)
+        for sp in self.spacers[:k]:
+            self.rt.swap_in(sp, stream=self.stream)
+        self.rt.swap_in(self.mid, stream=self.stream)
+        self.stream.synchronize()
+        return self.rt.info(self.mid)["extent_offset"]
 
     def request(self, x, out, cold):
         torch = self.torch
@@ -298,6 +316,68 @@ def copy_compare(torch, dev, link_copy, link_gather, wgs=(64, 256, 1024, 2048), 
     return out
 
 
+def hit_conditions(torch, dev, reps=40, idle_s=0.02, flush_bytes=512 << 20):
+    """A warm request (weights resident) of workloads 2-4 at batch 1 under the conditions a hit
+    meets in the multi-tenant workload, one at a time: back to back with the same buffers (the
+    isolated warm figure), with a new input/output pair each time (the cached graph is
+    repointed), after an idle gap of the trace's mean inter-arrival time, after a device copy of
+    flush_bytes that displaces the weights from the caches (other models ran in between), both,
+    and after the model came back into another arena offset (five offsets in turn). Host latency (the call plus the stream synchronisation) and the device span of the
+    request (events on its stream), p50 of `reps` each."""
+    import synth
+    import paper_2306_03622_amd as tp
+    src = torch.empty(flush_bytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    out = {}
+    for cfg in (2, 3, 4):
+        m = synth.config_model(cfg)
+        m.blob()
+        b = Bench(torch, dev, m, [1], "memcpy", tp.DEFAULT_CHUNK, plan="cost", spacers=4)
+        pairs = [b.io(1, synth.CONFIG_SEEDS[cfg][1] + 1), b.io(1, synth.CONFIG_SEEDS[cfg][1] + 1)]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+        def one(k, idle, flush, move=False):
+            x, y = pairs[k % 2]
+            if move:
+                offsets.add(b.place(k % 5))
+            if flush:
+                dst.copy_(src)
+            torch.cuda.synchronize()
+            if idle:
+                time.sleep(idle_s)
+            t0 = time.perf_counter()
+            e0.record(b.stream)
+            b.rt.infer(b.mid, x, y, stream=b.stream)
+            e1.record(b.stream)
+            b.stream.synchronize()
+            return (time.perf_counter() - t0) * 1e3, e0.elapsed_time(e1)
+
+        offsets = set()
+        b.place(0)
+        b.request(*pairs[0], cold=False)
+        for k in range(6):
+            one(k, False, False)
+        rows = {}
+        for name, alt, idle, flush, move in (("back_to_back", False, False, False, False),
+                                             ("new_buffers", True, False, False, False),
+                                             ("idle", False, True, False, False), ("flushed", False, False, True, False),
+                                             ("idle_flushed", False, True, True, False),
+                                             ("idle_flushed_new_buffers", True, True, True, False),
+                                             ("moved_new_buffers", True, False, False, True)):
+            log(f"hit conditions cfg{cfg}: {name}")
+            r = [one(k if alt else 0, idle, flush, move) for k in range(1, reps + 1)]
+            rows[name] = {"p50_ms": round(p50([v[0] for v in r]), 4),
+                          "device_p50_ms": round(p50([v[1] for v in r]), 4)}
+        same = bool(torch.equal(pairs[0][1], pairs[1][1]))
+        out[f"cfg{cfg}_b1"] = {"weight_bytes": m.total_bytes, "conditions": rows,
+                               "outputs_of_both_buffer_pairs_equal": same, "moved_offsets": len(offsets)}
+        st = b.rt.stats()
+        out[f"cfg{cfg}_b1"]["graphs"] = {k: st.get(k) for k in ("graph_captures", "graph_repoints", "graph_rebases")}
+        b.close()
+        m.drop_blob()
+    return out
+
+
 def native_alloc_us(sizes, reps=10):
     """p50 of hipMalloc + hipFree of each size (the per-swap allocation that a reserved arena
     avoids), through the HIP runtime torch has loaded."""
@@ -404,6 +484,8 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
     rt.close()
     lat = np.array([(r["done_ns"] - q[4]) / 1e6 for r, q in zip(res, reqs)])
     hit = np.array([r["hit"] for r in res])
+    issue_delay = np.array([(r["issue_ns"] - q[4]) / 1e6 for r, q in zip(res, reqs)])
+    service = np.array([(r["done_ns"] - r["issue_ns"]) / 1e6 for r in res])
     # requests issued with nothing of theirs queued ahead on the GPU (the previous request had
     # completed): their latency is the request's own service time
     idle = np.array([i == 0 or res[i]["issue_ns"] >= res[i - 1]["done_ns"] for i in range(len(res))])
@@ -419,8 +501,15 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                       else None,
                       "idle_hit_p50_ms": round(float(np.percentile(lat[sel & (hit == 1) & idle], 50)), 3)
                       if (sel & (hit == 1) & idle).any() else None}
+            ih = sel & (hit == 1) & idle
+            if ih.any():
+                # an idle hit's latency split: arrival -> tp_infer call (the driver's wake-up),
+                # call -> completion seen by the host
+                per[a]["idle_hit_issue_delay_p50_ms"] = round(float(np.percentile(issue_delay[ih], 50)), 4)
+                per[a]["idle_hit_service_p50_ms"] = round(float(np.percentile(service[ih], 50)), 4)
     delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
-                                          "evacuations", "bytes_moved", "graph_captures", "graph_repoints")}
+                                          "evacuations", "bytes_moved", "graph_captures", "graph_repoints",
+                                          "graph_rebases")}
     delta["partitions"] = st1["partitions"]
     calls = st1["admit_calls"] - st0["admit_calls"]
     adm = np.array([r["admit_ns"] / 1e3 for r in res if not r["hit"]])
@@ -634,6 +723,8 @@ def main():
                     help="time the cold request under every swap design instead (breakdown table)")
     ap.add_argument("--copy-compare", action="store_true",
                     help="copy engine against the gather kernel (grid sizes 64-2048) on workloads 2-4, batch 8")
+    ap.add_argument("--hit-conditions", action="store_true",
+                    help="warm requests of workloads 2-4 at batch 1: back to back, new buffers, idle gap, flushed caches")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--workload", type=int, default=0, help=argparse.SUPPRESS)   # child process of --full
     ap.add_argument("--batches", default="1", help=argparse.SUPPRESS)
@@ -647,7 +738,7 @@ def main():
         sys.exit(2)
 
     children = {}
-    if not a.quick and not a.workload and not (a.tenants or a.ablation or a.pmc_workload or a.copy_compare):
+    if not a.quick and not a.workload and not (a.tenants or a.ablation or a.pmc_workload or a.copy_compare or a.hit_conditions):
         # Each extra workload runs in a process of its own, started before this process touches
         # the GPU: a serving process holds one context, and after many contexts and streams in
         # one process HIP's stream-to-hardware-queue arrangement can serialise a swap behind
@@ -703,6 +794,10 @@ def main():
         print(json.dumps({"copy_compare": copy_compare(torch, dev, link_copy, link_gather),
                           "link_copy_engine_gbs": round(link_copy, 2), "link_gather_kernel_gbs": round(link_gather, 2)}),
               flush=True)
+        return
+
+    if a.hit_conditions:
+        print(json.dumps({"hit_conditions": hit_conditions(torch, dev)}), flush=True)
         return
 
     if a.pmc_workload:

@@ -225,9 +225,11 @@ typedef struct {
   uint64_t admit_calls, admit_ns_total, admit_ns_max;
   uint32_t partitions, partitions_free;   /* TP_ALLOC_PARTITION*: partitions in all, unoccupied */
   uint64_t evacuations, bytes_moved;      /* TP_ALLOC_PARTITION_CONSOLIDATE: partitions freed by moves, bytes moved */
-  /* warm-request graphs: forward passes captured and instantiated, and graph launches whose
-   * kernel nodes were repointed at a request's input and output buffers instead */
-  uint64_t graph_captures, graph_repoints;
+  /* warm-request graphs: forward passes captured and instantiated; graph launches whose
+   * kernel nodes were repointed instead (at the request's input and output buffers, or at the
+   * model's weights in another extent than the nodes held); and those of the repointed
+   * launches that moved the weights */
+  uint64_t graph_captures, graph_repoints, graph_rebases;
 } tp_arena_stats_t;
 
 typedef struct {

@@ -281,10 +281,13 @@ hipError_t run_forward(ExecCtx& x) {
 
 // Warm request: replay the model's forward pass as one graph launch. A graph is captured
 // from the same kernel sequence (on a private stream, nothing executes) the first time a
-// (batch, extent, workspace) combination is seen; up to kGraphs combinations stay
-// instantiated per model. A request with other input or output buffers than the graph's
-// nodes hold repoints those nodes in place. If capture fails the model falls back to
-// launching its kernels one by one, which computes the same bits.
+// (batch, workspace) combination is seen; up to kGraphs combinations stay instantiated per
+// model. A request whose weights lie elsewhere than the graph's nodes hold (the model came
+// back into another extent) or with other input or output buffers repoints those nodes in
+// place; an input or output whose address has another residue modulo 16 than the captured
+// one is captured afresh instead, since a launcher may choose its kernel by that alignment.
+// If capture fails the model falls back to launching its kernels one by one, which computes
+// the same bits.
 constexpr size_t kGraphs = 4;
 
 // A graph launch costs more host and device time than a few direct kernel launches
@@ -324,21 +327,30 @@ bool chain_nodes(hipGraph_t g, const std::vector<k::LaunchRecord>& rec, std::vec
   return out->size() == rec.size();
 }
 
-// Points the graph's nodes that held the captured request's input and output at `in` and
-// `out`: each such kernel's recorded arguments with those two addresses replaced.
-hipError_t repoint(GraphEntry& g, const void* in, void* out) {
-  for (uint32_t i : g.io) {
+// Points the graph's nodes at the weights at `base` and at `in` and `out`: each node that
+// holds a pointer into the captured extent, input or output gets its recorded arguments
+// with those pointers moved by the same displacement (weights) or replaced (buffers). Only
+// the nodes whose pointers change are set.
+hipError_t repoint(GraphEntry& g, const char* base, const void* in, void* out) {
+  const bool moved = base != g.cur_base, io = in != g.cur_in || out != g.cur_out;
+  const uintptr_t b0 = (uintptr_t)g.cap_base, b1 = b0 + g.extent_bytes;
+  std::vector<uint8_t> b;
+  std::vector<void*> argv;
+  for (uint32_t i = 0; i < g.launches.size(); ++i) {
+    const uint8_t use = g.use[i];
+    if (!((moved && (use & kUsesWeights)) || (io && (use & kUsesBuffers)))) continue;
     const k::LaunchRecord& r = g.launches[i];
-    std::vector<uint8_t> b = r.bytes;
+    b = r.bytes;
     for (uint32_t at : r.ptr_at) {
       uintptr_t v;
       std::memcpy(&v, b.data() + at, sizeof v);
       if (v == (uintptr_t)g.cap_in) v = (uintptr_t)in;
       else if (v == (uintptr_t)g.cap_out) v = (uintptr_t)out;
+      else if (v >= b0 && v < b1) v = (uintptr_t)base + (v - b0);
       else continue;
       std::memcpy(b.data() + at, &v, sizeof v);
     }
-    std::vector<void*> argv(r.arg_at.size());
+    argv.resize(r.arg_at.size());
     for (size_t j = 0; j < argv.size(); ++j) argv[j] = b.data() + r.arg_at[j];
     hipKernelNodeParams p{};
     p.func = const_cast<void*>(r.func);
@@ -350,6 +362,7 @@ hipError_t repoint(GraphEntry& g, const void* in, void* out) {
     const hipError_t e = hipGraphExecKernelNodeSetParams(g.exec, g.nodes[i], &p);
     if (e != hipSuccess) return e;
   }
+  g.cur_base = base;
   g.cur_in = in;
   g.cur_out = out;
   return hipSuccess;
@@ -359,7 +372,7 @@ hipError_t repoint(GraphEntry& g, const void* in, void* out) {
 hipError_t capture_graph(tp_ctx* c, Model* m, GraphEntry& g) {
   Waiter w;
   w.m = m;
-  char* base = const_cast<char*>(g.base);
+  char* base = const_cast<char*>(g.cap_base);
   char* work = const_cast<char*>(g.work);
   ExecCtx x{m, base, work, g.cap_in, g.cap_out, g.batch, c->capture, &w, make_split(work, m, g.batch)};
   g.launches.clear();
@@ -377,19 +390,19 @@ hipError_t capture_graph(tp_ctx* c, Model* m, GraphEntry& g) {
     return e;
   }
   ++c->graph_captures;
+  g.cur_base = g.cap_base;
   g.cur_in = g.cap_in;
   g.cur_out = g.cap_out;
   g.patchable = chain_nodes(g.graph, g.launches, &g.nodes);
-  g.io.clear();
+  g.use.assign(g.launches.size(), 0);
+  const uintptr_t b0 = (uintptr_t)g.cap_base, b1 = b0 + g.extent_bytes;
   for (uint32_t i = 0; g.patchable && i < g.launches.size(); ++i) {
     const k::LaunchRecord& r = g.launches[i];
     for (uint32_t at : r.ptr_at) {
       uintptr_t v;
       std::memcpy(&v, r.bytes.data() + at, sizeof v);
-      if (v == (uintptr_t)g.cap_in || v == (uintptr_t)g.cap_out) {
-        g.io.push_back(i);
-        break;
-      }
+      if (v == (uintptr_t)g.cap_in || v == (uintptr_t)g.cap_out) g.use[i] |= kUsesBuffers;
+      else if (v >= b0 && v < b1) g.use[i] |= kUsesWeights;
     }
   }
   return hipSuccess;
@@ -399,11 +412,15 @@ hipError_t launch_graph(tp_ctx* c, Model* m, char* base, char* work, const void*
                         hipStream_t stream) {
   GraphEntry* hit = nullptr;
   for (auto& g : m->graphs)
-    if (g.batch == batch && g.base == base && g.work == work) hit = &g;
-  if (hit && (hit->cur_in != in || hit->cur_out != out)) {
-    hipError_t e = hit->patchable ? repoint(*hit, in, out) : hipErrorNotSupported;
+    if (g.batch == batch && g.work == work) hit = &g;
+  if (hit && (hit->cur_base != base || hit->cur_in != in || hit->cur_out != out)) {
+    const bool same_align = ((uintptr_t)in & 15) == ((uintptr_t)hit->cap_in & 15) &&
+                            ((uintptr_t)out & 15) == ((uintptr_t)hit->cap_out & 15);
+    const bool moved = hit->cur_base != base;
+    hipError_t e = hit->patchable && same_align ? repoint(*hit, base, in, out) : hipErrorNotSupported;
     if (e == hipSuccess) {
       ++c->graph_repoints;
+      if (moved) ++c->graph_rebases;
     } else {
       (void)hipGetLastError();
       destroy_graph(*hit);                 // captured again below, for these buffers
@@ -420,7 +437,8 @@ hipError_t launch_graph(tp_ctx* c, Model* m, char* base, char* work, const void*
     }
     GraphEntry g;
     g.batch = batch;
-    g.base = base;
+    g.cap_base = base;
+    g.extent_bytes = m->spec.host_bytes;
     g.work = work;
     g.cap_in = in;
     g.cap_out = out;
@@ -933,6 +951,7 @@ tp_status tp_arena_stats(tp_ctx* c, tp_arena_stats_t* out) {
   out->admit_ns_max = c->admit_ns_max;
   out->graph_captures = c->graph_captures;
   out->graph_repoints = c->graph_repoints;
+  out->graph_rebases = c->graph_rebases;
   return ok();
 }
 

@@ -20,9 +20,14 @@ namespace tp {
 // of the request it was captured from; `launches` holds every kernel's recorded arguments, so
 // a later request with other buffers repoints the kernel nodes that hold those two addresses
 // in place (hipGraphExecKernelNodeSetParams) instead of capturing the pass again.
+// Which pointers a recorded launch of a graph holds (GraphEntry::use).
+enum : uint8_t { kUsesWeights = 1, kUsesBuffers = 2 };
+
 struct GraphEntry {
   int batch = 0;
-  const char* base = nullptr;
+  const char* cap_base = nullptr;   // the weights' extent at capture, and its size
+  uint64_t extent_bytes = 0;
+  const char* cur_base = nullptr;   // the extent the instantiated nodes point into now
   const char* work = nullptr;
   const void* cap_in = nullptr;   // buffers of the captured request
   void* cap_out = nullptr;
@@ -32,7 +37,7 @@ struct GraphEntry {
   hipGraphExec_t exec = nullptr;
   std::vector<hipGraphNode_t> nodes;        // kernel nodes in launch order
   std::vector<k::LaunchRecord> launches;    // the same launches as recorded at capture
-  std::vector<uint32_t> io;                 // launches whose arguments hold cap_in or cap_out
+  std::vector<uint8_t> use;                 // per launch: kUsesWeights | kUsesBuffers
   bool patchable = false;                   // nodes and records matched one to one
   uint64_t stamp = 0;
 };
@@ -137,7 +142,7 @@ struct tp_ctx {
   hipEvent_t claim_ev = nullptr;               // a swap-in kernel's stream waits for copy[0]
   hipStream_t capture = nullptr;               // private stream for graph capture
   uint64_t graph_clock = 0;
-  uint64_t graph_captures = 0, graph_repoints = 0;
+  uint64_t graph_captures = 0, graph_repoints = 0, graph_rebases = 0;
   // cold (swapping) requests run on the library's execution stream, forked from and joined
   // back to the caller's stream (null under TP_FLAG_CALLER_STREAM)
   hipStream_t exec = nullptr;

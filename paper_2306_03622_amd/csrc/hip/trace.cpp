@@ -25,6 +25,16 @@ uint64_t since(std::chrono::steady_clock::time_point t0) {
       .count();
 }
 
+// Waits until `when`: sleeps until shortly before it, then spins, so that a request is issued
+// within a few microseconds of its arrival instead of after the sleep's wake-up delay (timer
+// slack and scheduling, tens of microseconds), which would count as latency.
+constexpr auto kSpin = std::chrono::microseconds(200);
+void wait_until(std::chrono::steady_clock::time_point when) {
+  if (std::chrono::steady_clock::now() + kSpin < when) std::this_thread::sleep_until(when - kSpin);
+  while (std::chrono::steady_clock::now() < when) {
+  }
+}
+
 tp_status make_ring(tp_ctx* c) {
   if (!c->trace_ev.empty()) return TP_OK;
   c->trace_ev.assign(kRing, nullptr);
@@ -80,7 +90,7 @@ extern "C" tp_status tp_run_trace(tp_ctx* c, const tp_request* reqs, uint32_t n,
   tp_status first_err = TP_OK;
   std::string first_msg;
   for (uint32_t i = 0; i < n; ++i) {
-    std::this_thread::sleep_until(t0 + std::chrono::nanoseconds(reqs[i].arrival_ns));
+    wait_until(t0 + std::chrono::nanoseconds(reqs[i].arrival_ns));
     {
       std::unique_lock<std::mutex> lk(mu);
       cv.wait(lk, [&] { return in_flight < kRing; });
@@ -223,7 +233,7 @@ extern "C" tp_status tp_run_trace_sched(tp_ctx* c, const tp_request* reqs, uint3
     const uint64_t now = since(t0);
     while (next < n && reqs[next].arrival_ns <= now) queue.push_back(next++);
     if (queue.empty()) {
-      std::this_thread::sleep_until(t0 + std::chrono::nanoseconds(reqs[next].arrival_ns));
+      wait_until(t0 + std::chrono::nanoseconds(reqs[next].arrival_ns));
       continue;
     }
     size_t k = 0;                               // FIFO: the earliest arrival

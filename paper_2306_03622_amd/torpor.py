@@ -75,7 +75,7 @@ class tp_arena_stats_t(C.Structure):
                 ("bytes_swapped", C.c_uint64), ("admit_calls", C.c_uint64), ("admit_ns_total", C.c_uint64),
                 ("admit_ns_max", C.c_uint64), ("partitions", C.c_uint32), ("partitions_free", C.c_uint32),
                 ("evacuations", C.c_uint64), ("bytes_moved", C.c_uint64), ("graph_captures", C.c_uint64),
-                ("graph_repoints", C.c_uint64)]
+                ("graph_repoints", C.c_uint64), ("graph_rebases", C.c_uint64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

@@ -83,12 +83,20 @@ def test_resnet_input_alignment_paths(image, batch):
     buf[1:1 + flat.numel()] = flat
     xs = buf[1:1 + flat.numel()].view(x.shape)
     assert xs.data_ptr() % 16 == 2
-    out = torch.full(out_shape(m, batch), float("nan"), dtype=torch.float32, device=dev)
     s = torch.cuda.Stream(device=dev)
-    torch.cuda.synchronize()
-    rt.infer(mid, xs, out, stream=s)
-    s.synchronize()
-    assert np.array_equal(out.cpu().numpy(), aligned)
+    # warm requests alternate between the unaligned and an aligned input: the cached graph
+    # is captured afresh whenever the input's alignment changes (its stem kernel was chosen by
+    # the captured one's), and repointed when it does not
+    xa = to_device(x)
+    assert xa.data_ptr() % 16 == 0
+    for k, xin in enumerate((xs, xa, xs, xs)):
+        out = torch.full(out_shape(m, batch), float("nan"), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        rt.infer(mid, xin, out, stream=s)
+        s.synchronize()
+        assert np.array_equal(out.cpu().numpy(), aligned), k
+    st = rt.stats()
+    assert (st["graph_captures"], st["graph_repoints"]) == (3, 1), st
     rt.close()
 
 

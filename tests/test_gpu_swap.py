@@ -163,6 +163,61 @@ def test_warm_hits_with_new_buffers_repoint_the_graph():
     rt.close()
 
 
+def test_warm_hits_after_a_move_rebase_the_graph():
+    # a model that comes back into another extent keeps its graph: the nodes holding weight
+    # pointers are moved to the new extent (retired extents are poisoned, so a node left
+    # pointing at the old one reads poison); the bits stay the kernel-by-kernel ones
+    ms = [synth.mlp(18, 256, "bf16", "gelu", seed=71),
+          synth.bert(seed=72, layers=3, d=128, heads=2, ffn=256, seq=64, vocab=500, maxpos=64),
+          synth.resnet50(seed=73, classes=10, image=32)]
+    spacer = synth.mlp(2, 256, "bf16", "gelu", seed=74)
+    eager_rt, eager_ids = make_runtime(ms, batch_max=2, flags=tp.TP_FLAG_NO_GRAPH)
+    arena = max(m.total_bytes for m in ms) + spacer.total_bytes + (1 << 20)
+    rt, ids = make_runtime(ms + [spacer], batch_max=2, arena_bytes=arena, flags=tp.TP_FLAG_POISON)
+    sp = ids[-1]
+    torch, dev = torch_dev()
+    s = torch.cuda.Stream(device=dev)
+    rebases, keep = 0, []
+    for k, m in enumerate(ms):
+        x_np = synth.config_input(m, 2, 700 + k)
+        want = infer(eager_rt, eager_ids[k], m, x_np)
+        for mid in ids:
+            rt.evict(mid)
+        seen = []
+        # resident at the arena's base, then after the spacer, then at the base again
+        for step, with_spacer in enumerate((False, False, True, True, False)):
+            if step:
+                rt.evict(ids[k])
+                rt.evict(sp)
+                if with_spacer:
+                    rt.swap_in(sp, stream=s)
+            rt.swap_in(ids[k], stream=s)
+            s.synchronize()
+            off = rt.info(ids[k])["extent_offset"]
+            if seen and off != seen[-1]:
+                rebases += 1
+            seen.append(off)
+            # a warm hit with buffers of its own (kept allocated, so no address comes back)
+            x = to_device(x_np)
+            out = torch.full(out_shape(m, 2), float("nan"), dtype=torch.float32, device=dev)
+            keep += [x, out]
+            torch.cuda.synchronize()
+            rt.infer(ids[k], x, out, stream=s)
+            s.synchronize()
+            assert np.array_equal(out.cpu().numpy(), want), (m.arch, step, off)
+        log(f"{m.arch}: offsets {seen}")
+        assert len(set(seen)) == 2, seen
+    st = rt.stats()
+    log(f"graph captures {st['graph_captures']}, repoints {st['graph_repoints']}, rebases {st['graph_rebases']}")
+    # one capture per model (its first hit); every later hit repoints, those after a move also
+    # move the weight pointers
+    assert st["graph_captures"] == len(ms), st
+    assert st["graph_repoints"] == 4 * len(ms), st
+    assert st["graph_rebases"] == rebases == 2 * len(ms), st
+    eager_rt.close()
+    rt.close()
+
+
 def test_eviction_order_and_placement_do_not_change_outputs():
     ms = _models()
     xs = _inputs(ms)

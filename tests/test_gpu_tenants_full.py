@@ -118,24 +118,24 @@ def test_full_size_trace_matches_oracle(policy):
     log(f"first-request errors, worst per family: {worst}")
     assert all(e <= 2e-2 for _, e in errors.values()), [(r, a, e) for r, (a, e) in errors.items() if e > 2e-2]
 
-    # Warm requests replay a graph per (model, batch, extent): the first hit at a new extent
-    # captures one (up to 4 kept per model, least recently used dropped), every other hit
-    # repoints it at its own buffers; no hit captures because its buffers are new.
-    cached, want_captures = {}, 0
+    # Warm requests replay a graph per (model, batch): the first hit of a model captures it,
+    # every later hit repoints it at its own buffers, and a hit in another extent than the
+    # model's previous hit also moves the graph's weight pointers; no hit captures again.
+    last_hit_off, want_captures, want_rebases = {}, 0, 0
     for rq, d in zip(reqs, decisions):
         if not d["hit"]:
             continue
-        keys = cached.setdefault(rq[0], [])
-        if d["offset"] in keys:
-            keys.remove(d["offset"])
-        else:
+        prev = last_hit_off.get(rq[0])
+        if prev is None:
             want_captures += 1
-            if len(keys) == 4:
-                keys.pop(0)
-        keys.append(d["offset"])
-    log(f"graph captures {st['graph_captures']} (expected {want_captures}), repoints {st['graph_repoints']}")
+        elif prev != d["offset"]:
+            want_rebases += 1
+        last_hit_off[rq[0]] = d["offset"]
+    log(f"graph captures {st['graph_captures']} (expected {want_captures}), repoints {st['graph_repoints']}, "
+        f"rebases {st['graph_rebases']} (expected {want_rebases})")
     assert st["graph_captures"] == want_captures, st
     assert st["graph_repoints"] == st["hits"] - want_captures, st
+    assert st["graph_rebases"] == want_rebases, st
     lat = np.array([(q["done_ns"] - rq[4]) / 1e6 for q, rq in zip(res, reqs)])
     arch = np.array([kinds[rq[0]] for rq in reqs])
     hits = np.array(got_hits)
@@ -158,7 +158,7 @@ def test_full_size_trace_matches_oracle(policy):
         "hit_rate_arena": round(float(hits.mean()), 4), "hit_rate_simulator": round(float(np.mean(want_hits)), 4),
         "hit_rate_byte_capacity_lru": round(float(np.mean(lru)), 4),
         "arena": {k: st[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
-                                     "graph_captures", "graph_repoints")},
+                                     "graph_captures", "graph_repoints", "graph_rebases")},
         "decisions_equal_simulator": True,
     }
     log(json.dumps(summary))
