@@ -124,6 +124,19 @@ def test_mlp_bf16_blocked_weights(batch):
     rt.close()
 
 
+@pytest.mark.parametrize("width,batch", [(320, 100), (1088, 1030)])
+def test_mlp_bf16_row_major_epilogue_prefetch(width, batch):
+    # row-major weights (width % 128 != 0) whose width is a multiple of the tile: the tiled
+    # kernel fetches bias values with its first operands (32 x 32 tiles at width 320, 64 x 64
+    # at 1088), on batches that leave a partial tile of rows
+    m = synth.mlp(3, width, "bf16", "gelu", seed=27)
+    x = synth.mlp_input(batch, width, "bf16", 700 + batch)
+    rt, (mid,) = make_runtime([m], batch_max=batch)
+    log(f"mlp bf16 width {width} batch {batch}")
+    check_parity(infer(rt, mid, m, x), m, x, 2e-2)
+    rt.close()
+
+
 @pytest.mark.parametrize("act", ["relu", "none", "gelu"])
 def test_mlp_f32_acts(act):
     # gelu: the kernels' fp32 erf (Abramowitz-Stegun 7.1.26, |error| <= 1.5e-7) against the
