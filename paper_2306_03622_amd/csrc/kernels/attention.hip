@@ -146,7 +146,8 @@ hipError_t attention(const uint16_t* qkv, int B, int S, int H, uint16_t* out, hi
   if (!qkv || !out || B < 1 || H < 1 || S < 32 || (S & 31) || S > 256) return hipErrorInvalidValue;
   // four waves (64 queries) per workgroup: with one or two, staging K and V once per
   // workgroup costs more than the extra workgroups gain (BERT-base at batch 8: 0.790 ms warm
-  // with four, 0.839 with two, 0.915 with one)
+  // with four, 0.839 with two, 0.915 with one; with the present staging, two waves at batch
+  // 1, where four leave 24 workgroups on 256 CUs: 0.462 -> 0.475 ms)
   constexpr int NW = 4;
   dim3 grid((S + 16 * NW - 1) / (16 * NW), H, B), block(64 * NW);
   if (S == 128) (void)launch((k_attention<128, true, NW>), grid, block, 0, s, qkv, S, H, out);
