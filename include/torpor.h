@@ -126,10 +126,11 @@ enum {
  * host-mapped pinned memory with gather_wgs workgroups (0 = default). throttle_us:
  * delay per chunk under TP_FLAG_THROTTLE. Warm requests of models whose forward pass
  * launches at least 16 kernels replay an instantiated HIP graph of it, cached per (model,
- * batch, extent, workspace; up to 4 per model), unless TP_FLAG_NO_GRAPH is set; a request
- * whose input or output buffer differs from the graph's repoints the graph's kernels that
- * read the input or write the output (no new capture); shorter forward passes are
- * launched kernel by kernel, which is faster for them. A cold request's kernels run on an
+ * batch, workspace; up to 4 per model), unless TP_FLAG_NO_GRAPH is set; a request whose
+ * input or output buffer differs from the graph's, or whose model now lies in another
+ * extent, repoints the graph's kernels that hold those addresses (no new capture; an input
+ * or output address with another residue modulo 16 is captured afresh); shorter forward
+ * passes are launched kernel by kernel, which is faster for them. A cold request's kernels run on an
  * execution stream the library creates (with a hardware queue of its own, like the copy
  * streams), forked from the caller's stream by an event and joined back to it by another;
  * so whatever hardware queue the caller's stream maps to, the chunk copies overlap the
