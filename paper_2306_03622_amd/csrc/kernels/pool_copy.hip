@@ -6,7 +6,11 @@ namespace tp {
 namespace k {
 namespace {
 
-// one thread per (sample, output pixel, 8 channels); padded taps are skipped (never win)
+// One thread per (sample, output pixel, 8 channels). The nine taps are loaded together (a tap
+// in the padding reads the nearest pixel inside the image and is then ignored, so every load
+// is in bounds and none waits for another) and reduced in the fixed order dh, dw; padded taps
+// never win, as if skipped. (With each tap's load behind its bounds test the loads were issued
+// one after another: 7.0 us per launch at ResNet-50 batch 1.)
 __global__ __launch_bounds__(256) void k_maxpool3s2(const uint16_t* __restrict__ x, int B, int H, int W, int C,
                                                     int Ho, int Wo, uint16_t* __restrict__ y) {
   const int c8n = C >> 3;
@@ -19,22 +23,32 @@ __global__ __launch_bounds__(256) void k_maxpool3s2(const uint16_t* __restrict__
   p /= Wo;
   const int oh = (int)(p % Ho);
   const int b = (int)(p / Ho);
+  uint4 v[9];
+  bool ok[9];
+#pragma unroll
+  for (int dh = 0; dh < 3; ++dh) {
+    const int ih = oh * 2 - 1 + dh;
+    const bool hin = ih >= 0 && ih < H;
+    const int ihc = ih < 0 ? 0 : (ih >= H ? H - 1 : ih);
+#pragma unroll
+    for (int dw = 0; dw < 3; ++dw) {
+      const int iw = ow * 2 - 1 + dw;
+      const int iwc = iw < 0 ? 0 : (iw >= W ? W - 1 : iw);
+      ok[dh * 3 + dw] = hin && iw >= 0 && iw < W;
+      v[dh * 3 + dw] = *reinterpret_cast<const uint4*>(x + (((size_t)b * H + ihc) * W + iwc) * C + c8 * 8);
+    }
+  }
   float m[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) m[e] = -INFINITY;
-  for (int dh = 0; dh < 3; ++dh) {
-    const int ih = oh * 2 - 1 + dh;
-    if (ih < 0 || ih >= H) continue;
-    for (int dw = 0; dw < 3; ++dw) {
-      const int iw = ow * 2 - 1 + dw;
-      if (iw < 0 || iw >= W) continue;
-      const uint4 v = *reinterpret_cast<const uint4*>(x + (((size_t)b * H + ih) * W + iw) * C + c8 * 8);
-      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        m[2 * e] = fmaxf(m[2 * e], bf2f(w[e] & 0xffff));
-        m[2 * e + 1] = fmaxf(m[2 * e + 1], bf2f(w[e] >> 16));
-      }
+  for (int t = 0; t < 9; ++t) {
+    if (!ok[t]) continue;
+    const uint32_t w[4] = {v[t].x, v[t].y, v[t].z, v[t].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      m[2 * e] = fmaxf(m[2 * e], bf2f(w[e] & 0xffff));
+      m[2 * e + 1] = fmaxf(m[2 * e + 1], bf2f(w[e] >> 16));
     }
   }
   uint4 o;
