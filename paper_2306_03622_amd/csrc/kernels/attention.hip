@@ -1,14 +1,14 @@
 // Multi-head self-attention for head dim 64 and short sequences (S <= 256, S % 32 == 0),
 // one workgroup per (sample, head, 16 NW queries); each wave owns 16 queries.
 //
-// K of the head is staged row-major in LDS and V transposed ([d][key]). Scores are
+// K and V of the head are staged row-major in LDS ([key][d]). Scores are
 // computed as S^T = K Q^T on MFMA (A = 16 keys, B = 16 queries), so lane l holds the
 // scores of query l % 16 against keys 16 t + 4 (l / 16) + e. The softmax reductions
 // over keys therefore stay inside a lane plus two cross-lane exchanges (lanes l ^ 16,
 // l ^ 32), in fp32. The normalised probabilities, rounded to bf16, are used directly as
 // the A operand of O = P V: a 32-key MFMA k-block takes the lane's own values from two
-// consecutive score tiles, and the matching V entries are read from the transposed copy
-// with the same key order, so no data moves between lanes.
+// consecutive score tiles, and the matching V entries are read with gfx950's transposing LDS
+// load (ds_read_b64_tr_b16) in the same key order, so no data moves between lanes.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -21,10 +21,10 @@ namespace {
 template <int SMAX, bool FULL, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attention(const uint16_t* __restrict__ qkv, int S_arg, int H,
                                                        uint16_t* __restrict__ out) {
-  constexpr int LDK = 72, LDV = SMAX + 12, NT = SMAX / 16, NTHR = 64 * NW;
+  constexpr int LDK = 72, LDV = 80, NT = SMAX / 16, NTHR = 64 * NW;
   const int S = FULL ? SMAX : S_arg;
   __shared__ __attribute__((aligned(16))) uint16_t Ks[SMAX * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[64 * LDV];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[SMAX * LDV];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int h = blockIdx.y, b = blockIdx.z;
@@ -41,12 +41,11 @@ __global__ __launch_bounds__(64 * NW) void k_attention(const uint16_t* __restric
 
   // K and V of the head: every load of this thread issued before the first LDS store, so
   // the round trips overlap. Both are read as key = 32 i + tid / 8, 8 dims at (tid % 8) * 8,
-  // a key's 128 bytes per 8 lanes, so one wave's load covers 8 whole rows; V is then stored
-  // transposed 2 bytes at a time. Measured per launch at BERT-base batch 1 / 8 against the
-  // alternatives, all computing the same bits: V read with each wave holding 64 consecutive
-  // keys of the same 8 dims (64 rows per load, conflict-free 2-byte stores) 6.8 / 6.7 us;
-  // these loads with LDV = SMAX + 8 5.8 / 5.7 us, + 4 6.4 / 5.5, + 12 (below) 5.6 / 5.5; an
-  // 8 x 8 transpose among lanes by three exchange steps, then 16-byte stores, 7.4 / 6.7 us.
+  // a key's 128 bytes per 8 lanes, so one wave's load covers 8 whole rows; both are stored
+  // as whole 16-byte pieces. (V stored transposed 2 bytes at a time, read as 8-byte pieces,
+  // took 5.6 / 5.5 us per launch at BERT-base batch 1 / 8 with the best padding of several;
+  // other transposes, by lanes holding 64 consecutive keys or by an 8 x 8 exchange among
+  // lanes, 6.7-7.4 us; all the same bits.)
   constexpr int NV = SMAX * 8 / NTHR;
   static_assert(SMAX * 8 % NTHR == 0 && SMAX % 64 == 0, "staging map");
   uint4 kv[NV], vv[NV];
@@ -62,12 +61,7 @@ __global__ __launch_bounds__(64 * NW) void k_attention(const uint16_t* __restric
     const int key = (i * NTHR + tid) >> 3, d8 = (tid & 7) << 3;
     if (key < S) {
       *reinterpret_cast<uint4*>(&Ks[key * LDK + d8]) = kv[i];
-      const uint32_t w[4] = {vv[i].x, vv[i].y, vv[i].z, vv[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        Vt[(d8 + 2 * e) * LDV + key] = (uint16_t)(w[e] & 0xffff);
-        Vt[(d8 + 2 * e + 1) * LDV + key] = (uint16_t)(w[e] >> 16);
-      }
+      *reinterpret_cast<uint4*>(&Vs[key * LDV + d8]) = vv[i];
     }
   }
   __syncthreads();
@@ -124,10 +118,16 @@ __global__ __launch_bounds__(64 * NW) void k_attention(const uint16_t* __restric
       pa.w = (uint32_t)f2bf(p1[2] * inv) | ((uint32_t)f2bf(p1[3] * inv) << 16);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        const uint16_t* vr = &Vt[(16 * dt + r) * LDV + 32 * u + 4 * g];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pa), as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)),
+        // V^T fragment of keys 32 u + 4 g + 0..3 (lo) and 16 further (hi), dim 16 dt + r, read
+        // transposed from row-major V: within a 16-lane group, lane l receives element l % 4 of
+        // the 8-byte pieces the group's lanes l / 4 + 4 j (j = 0..3) address, so lane s of the
+        // group addresses key row (s % 16) / 4 at dims 16 dt + 4 (s % 4)
+        const uint16_t* vr = &Vs[(32 * u + 4 * g + (r >> 2)) * LDV + 16 * dt + 4 * (r & 3)];
+        typedef short v4s __attribute__((ext_vector_type(4)));
+        const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)vr);
+        const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(vr + 16 * LDV));
+        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pa), as_bf16x8(make_uint4(l2.x, l2.y, h2.x, h2.y)),
                                                         o[dt], 0, 0, 0);
       }
     }
