@@ -58,10 +58,12 @@ def infer(rt, mid, model, x_np, stream=None):
     return out.cpu().numpy()
 
 
+# where GPU tests leave their records: $TP_RESULTS_DIR, else results/ at the repository root
+RESULTS_DIR = os.environ.get("TP_RESULTS_DIR") or os.path.join(
+    os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "results")
 # every parity check appends its achieved error here (one JSON object per line), so a GPU
 # run leaves a record of the errors behind its pass/fail verdicts
-PARITY_LOG = os.environ.get("TP_PARITY_LOG", os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(
-    __file__))), "gpurun_out", "parity_errors.jsonl"))
+PARITY_LOG = os.environ.get("TP_PARITY_LOG", os.path.join(RESULTS_DIR, "parity_errors.jsonl"))
 
 
 def record_parity(model, batch, err, tol):

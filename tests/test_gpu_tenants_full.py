@@ -12,7 +12,8 @@ brings input and output buffers of its own. Checks:
   * warm requests capture a graph only at the first hit after a swap to a new extent; every
     other hit repoints a cached graph at its own buffers.
 It writes a summary (latency, hit rates beside a byte-capacity LRU without contiguity, the
-achieved errors) to gpurun_out/tenants_full_<policy>.json. It takes about four minutes per
+achieved errors) to tenants_full_<policy>.json in the results folder ($TP_RESULTS_DIR, else
+results/ at the repository root). It takes about four minutes per
 policy, so it runs only when TP_FULL_TENANTS=1 is set."""
 import json
 import os
@@ -26,7 +27,7 @@ import paper_2306_03622_amd as tp
 import synth
 from oracle import forward as oracle
 from oracle.arena_sim import ArenaSim
-from tests.common import PARITY_LOG, log, out_shape, record_parity, to_device, torch_dev
+from tests.common import RESULTS_DIR, log, out_shape, record_parity, to_device, torch_dev
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(os.environ.get("TP_FULL_TENANTS") != "1",
@@ -162,7 +163,7 @@ def test_full_size_trace_matches_oracle(policy):
         "decisions_equal_simulator": True,
     }
     log(json.dumps(summary))
-    out_dir = os.path.dirname(PARITY_LOG)
+    out_dir = RESULTS_DIR
     os.makedirs(out_dir, exist_ok=True)
     with open(os.path.join(out_dir, f"tenants_full_{policy}.json"), "w") as f:
         json.dump(summary, f, indent=1)
