@@ -713,7 +713,7 @@ hipError_t launch_tiled(GemmArgs a, int splits, const Split& sp, hipStream_t s) 
     }
   }
   // an unsplit row-major contraction fetches its epilogue inputs with its first operands
-  // (EPF). Against fetching them after the main loop, whole warm forwards (same-box A/B):
+  // (EPF). Against fetching them after the main loop, whole warm forwards (A/B on one machine):
   // ResNet-50 -3 to -4% at batch 1 and 8, BERT-base -3% at batch 1, -1% at batch 8; for
   // the convolution taps as well, no further change (-0.5% to +0.3%), so those do not.
   constexpr bool kEpfTile = MODE == X_ROWS && BM <= 64 * WGN * WGM / (BN / 16);
