@@ -322,58 +322,70 @@ def hit_conditions(torch, dev, reps=40, idle_s=0.02, flush_bytes=512 << 20):
     isolated warm figure), with a new input/output pair each time (the cached graph is
     repointed), after an idle gap of the trace's mean inter-arrival time, after a device copy of
     flush_bytes that displaces the weights from the caches (other models ran in between), both,
-    and after the model came back into another arena offset (five offsets in turn). Host latency (the call plus the stream synchronisation) and the device span of the
-    request (events on its stream), p50 of `reps` each."""
+    and after the model came back into another arena offset (five offsets in turn). Then the
+    cache conditions again in a context where every warm request pre-reads its weights into the
+    caches (TP_FLAG_TOUCH_ALWAYS; by default only a request that follows another model's does).
+    Host latency (the call plus the stream synchronisation) and the device span of the request
+    (events on its stream), p50 of `reps` each."""
     import synth
     import paper_2306_03622_amd as tp
     src = torch.empty(flush_bytes, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
     out = {}
+    conditions = (("back_to_back", False, False, False, False), ("new_buffers", True, False, False, False),
+                  ("idle", False, True, False, False), ("flushed", False, False, True, False),
+                  ("idle_flushed", False, True, True, False), ("idle_flushed_new_buffers", True, True, True, False),
+                  ("moved_new_buffers", True, False, False, True))
+    touched = ("back_to_back", "flushed", "idle_flushed_new_buffers")
     for cfg in (2, 3, 4):
         m = synth.config_model(cfg)
         m.blob()
-        b = Bench(torch, dev, m, [1], "memcpy", tp.DEFAULT_CHUNK, plan="cost", spacers=4)
-        pairs = [b.io(1, synth.CONFIG_SEEDS[cfg][1] + 1), b.io(1, synth.CONFIG_SEEDS[cfg][1] + 1)]
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        row = {"weight_bytes": m.total_bytes}
+        for flags, key, names in ((0, "conditions", [c[0] for c in conditions]),
+                                  (tp.TP_FLAG_TOUCH_ALWAYS, "conditions_touch_always", touched)):
+            b = Bench(torch, dev, m, [1], "memcpy", tp.DEFAULT_CHUNK, plan="cost", spacers=4, flags=flags)
+            pairs = [b.io(1, synth.CONFIG_SEEDS[cfg][1] + 1), b.io(1, synth.CONFIG_SEEDS[cfg][1] + 1)]
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            offsets = set()
 
-        def one(k, idle, flush, move=False):
-            x, y = pairs[k % 2]
-            if move:
-                offsets.add(b.place(k % 5))
-            if flush:
-                dst.copy_(src)
-            torch.cuda.synchronize()
-            if idle:
-                time.sleep(idle_s)
-            t0 = time.perf_counter()
-            e0.record(b.stream)
-            b.rt.infer(b.mid, x, y, stream=b.stream)
-            e1.record(b.stream)
-            b.stream.synchronize()
-            return (time.perf_counter() - t0) * 1e3, e0.elapsed_time(e1)
+            def one(k, idle, flush, move=False):
+                x, y = pairs[k % 2]
+                if move:
+                    offsets.add(b.place(k % 5))
+                if flush:
+                    dst.copy_(src)
+                torch.cuda.synchronize()
+                if idle:
+                    time.sleep(idle_s)
+                t0 = time.perf_counter()
+                e0.record(b.stream)
+                b.rt.infer(b.mid, x, y, stream=b.stream)
+                e1.record(b.stream)
+                b.stream.synchronize()
+                return (time.perf_counter() - t0) * 1e3, e0.elapsed_time(e1)
 
-        offsets = set()
-        b.place(0)
-        b.request(*pairs[0], cold=False)
-        for k in range(6):
-            one(k, False, False)
-        rows = {}
-        for name, alt, idle, flush, move in (("back_to_back", False, False, False, False),
-                                             ("new_buffers", True, False, False, False),
-                                             ("idle", False, True, False, False), ("flushed", False, False, True, False),
-                                             ("idle_flushed", False, True, True, False),
-                                             ("idle_flushed_new_buffers", True, True, True, False),
-                                             ("moved_new_buffers", True, False, False, True)):
-            log(f"hit conditions cfg{cfg}: {name}")
-            r = [one(k if alt else 0, idle, flush, move) for k in range(1, reps + 1)]
-            rows[name] = {"p50_ms": round(p50([v[0] for v in r]), 4),
-                          "device_p50_ms": round(p50([v[1] for v in r]), 4)}
-        same = bool(torch.equal(pairs[0][1], pairs[1][1]))
-        out[f"cfg{cfg}_b1"] = {"weight_bytes": m.total_bytes, "conditions": rows,
-                               "outputs_of_both_buffer_pairs_equal": same, "moved_offsets": len(offsets)}
-        st = b.rt.stats()
-        out[f"cfg{cfg}_b1"]["graphs"] = {k: st.get(k) for k in ("graph_captures", "graph_repoints", "graph_rebases")}
-        b.close()
+            b.place(0)
+            b.request(*pairs[0], cold=False)
+            for k in range(6):
+                one(k, False, False)
+            rows = {}
+            for name, alt, idle, flush, move in conditions:
+                if name not in names:
+                    continue
+                log(f"hit conditions cfg{cfg}: {name}" + (" (touch always)" if flags else ""))
+                r = [one(k if alt else 0, idle, flush, move) for k in range(1, reps + 1)]
+                rows[name] = {"p50_ms": round(p50([v[0] for v in r]), 4),
+                              "device_p50_ms": round(p50([v[1] for v in r]), 4)}
+            row[key] = rows
+            st = b.rt.stats()
+            if flags:
+                row["cache_touches"] = st.get("cache_touches")
+            else:
+                row["outputs_of_both_buffer_pairs_equal"] = bool(torch.equal(pairs[0][1], pairs[1][1]))
+                row["moved_offsets"] = len(offsets)
+                row["graphs"] = {k: st.get(k) for k in ("graph_captures", "graph_repoints", "graph_rebases")}
+            b.close()
+        out[f"cfg{cfg}_b1"] = row
         m.drop_blob()
     return out
 
@@ -417,7 +429,7 @@ def byte_lru_hit_rate(seq, sizes, capacity):
 
 
 def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", plan="cost", queue=None, rate=50.0,
-            deadline_ms=None, slo_pct=0.98, alloc="first-fit", partition_mib=0):
+            deadline_ms=None, slo_pct=0.98, alloc="first-fit", partition_mib=0, lib_flags=0):
     """Open-loop multi-tenant run: n_models registered models of the three families, an
     arena of arena_gib GiB, Poisson arrivals at 50/s with Zipf(1.1) popularity, LRU,
     heaviness-aware or contiguous-window eviction, first-fit or two-tier partitioned placement (with or without
@@ -435,7 +447,7 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
     rt = tp.Runtime(arena_gib << 30, ws, plan=tp.TP_PLAN_COST if plan == "cost" else tp.TP_PLAN_GREEDY,
                     evict_policy={"lru": tp.TP_EVICT_LRU, "heaviness": tp.TP_EVICT_HEAVINESS,
                                   "window": tp.TP_EVICT_LRU_WINDOW}[evict],
-                    alloc=alloc_mode, partition_bytes=partition_mib << 20)
+                    alloc=alloc_mode, partition_bytes=partition_mib << 20, flags=lib_flags)
     t0 = time.perf_counter()
     ids = []
     for i, m in synth.build_models(specs, workers):
@@ -509,7 +521,7 @@ def tenants(torch, dev, n_requests, n_models, arena_gib, workers, evict="lru", p
                 per[a]["idle_hit_service_p50_ms"] = round(float(np.percentile(service[ih], 50)), 4)
     delta = {k: st1[k] - st0[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
                                           "evacuations", "bytes_moved", "graph_captures", "graph_repoints",
-                                          "graph_rebases")}
+                                          "graph_rebases", "cache_touches")}
     delta["partitions"] = st1["partitions"]
     calls = st1["admit_calls"] - st0["admit_calls"]
     adm = np.array([r["admit_ns"] / 1e3 for r in res if not r["hit"]])
@@ -728,7 +740,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--workload", type=int, default=0, help=argparse.SUPPRESS)   # child process of --full
     ap.add_argument("--batches", default="1", help=argparse.SUPPRESS)
-    ap.add_argument("--lib-flags", type=int, default=0, help="extra TP_FLAG_* bits for --workload runs (A/B checks)")
+    ap.add_argument("--lib-flags", type=int, default=0, help="extra TP_FLAG_* bits for --workload and --tenants runs (A/B checks)")
     ap.add_argument("--trace", action="store_true",
                     help="with --full: record the per-chunk timeline of one more cold request per workload")
     a = ap.parse_args()
@@ -779,7 +791,7 @@ def main():
         dl = dict(zip(("mlp", "resnet50", "bert"), (float(v) for v in a.deadlines.split(","))))
         print(json.dumps(tenants(torch, dev, a.tenants, a.tenant_models, a.tenant_arena_gib, 16, a.evict, a.plan,
                                  None if a.queue == "none" else a.queue, a.rate, dl, alloc=a.alloc,
-                                 partition_mib=a.partition_mib)), flush=True)
+                                 partition_mib=a.partition_mib, lib_flags=a.lib_flags)), flush=True)
         return
 
     if a.ablation:

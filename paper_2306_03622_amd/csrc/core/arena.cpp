@@ -195,6 +195,7 @@ void Arena::stats(tp_arena_stats_t* s) const {
   s->bytes_swapped = swapped_;
   s->admit_calls = s->admit_ns_total = s->admit_ns_max = 0;   // timed by the runtime
   s->graph_captures = s->graph_repoints = s->graph_rebases = 0;                   // counted by the runtime
+  s->cache_touches = 0;                                                           // counted by the runtime
   s->evacuations = evacuations_;
   s->bytes_moved = moved_;
   s->partitions = parts_ ? parts_->count() : 0;

@@ -66,6 +66,7 @@ void destroy_streams(tp_ctx* c) {
   if (c->exec) (void)hipStreamDestroy(c->exec);
   if (c->exec_fork) (void)hipEventDestroy(c->exec_fork);
   if (c->exec_join) (void)hipEventDestroy(c->exec_join);
+  if (c->touch_sink) (void)hipFree(c->touch_sink);
   if (c->copy[1]) (void)hipStreamDestroy(c->copy[1]);
   if (c->capture) (void)hipStreamDestroy(c->capture);
   if (c->req_done) (void)hipEventDestroy(c->req_done);
@@ -496,9 +497,49 @@ tp_status check_request(tp_ctx* c, int32_t id, Model** out) {
   return ok();
 }
 
+// Bounds of the bytes a warm request pre-reads into the caches (a span smaller is not missed
+// for long enough to matter; one larger would not stay in the 256 MB Infinity Cache beside
+// everything else).
+constexpr uint64_t kTouchMinBytes = 4ull << 20, kTouchMaxBytes = 192ull << 20;
+
+// The part [*lo, *hi) of a model's extent that a warm request pre-reads: all of it but a
+// leading token-embedding table, of which a request reads only its ids' rows (BERT-base: 47 of
+// 218 MB). False for an MLP, whose warm pass streams its weights at the rate a second reader
+// would (the two would only compete for the same bytes), and for a span outside the bounds.
+bool touch_span(const ModelSpec& s, uint64_t* lo, uint64_t* hi) {
+  if (s.arch == TP_ARCH_MLP) return false;
+  uint64_t a = 0;
+  for (const tp_tensor_desc& t : s.tensors)
+    if (t.role == TP_ROLE_TOK_EMB && t.offset == 0) a = round_up(t.bytes, 256);
+  const uint64_t b = s.host_bytes;
+  if (a >= b || b - a < kTouchMinBytes || b - a > kTouchMaxBytes) return false;
+  *lo = a;
+  *hi = b;
+  return true;
+}
+
+// A warm request for a model other than the one the previous request served (whose bytes the
+// requests in between have likely pushed out of the Infinity Cache and the L2s; every request
+// for it otherwise, under TP_FLAG_TOUCH_ALWAYS) reads the model's touch span on the
+// execution stream, with nothing ordered before or after it, while its own kernels run on the
+// caller's stream: its later layers then find their weights in the cache. Reading bytes that
+// a later swap may overwrite meanwhile is harmless (they are discarded), and the read stays
+// inside the arena, which outlives the context. A launch failure only forgoes the touch.
+void maybe_touch(tp_ctx* c, const Model* m, uint64_t off) {
+  if (!c->exec || !c->touch_sink || (c->cfg.flags & TP_FLAG_NO_TOUCH) || m->bg_pending) return;
+  if (!(c->cfg.flags & TP_FLAG_TOUCH_ALWAYS) && c->last_served == m->id) return;
+  uint64_t lo = 0, hi = 0;
+  if (!touch_span(m->spec, &lo, &hi)) return;
+  if (k::touch(c->arena + off + lo, hi - lo, c->touch_sink, c->exec) == hipSuccess) ++c->cache_touches;
+  else (void)hipGetLastError();
+}
+
 // One request (tp_infer and its variants), with the workspace `work` of `work_bytes`.
+// allow_graphs: warm forward passes may replay a graph; allow_touch: a warm request may
+// pre-read its weights on the execution stream (maybe_touch).
 tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t batch, void* output_dev,
-                        hipStream_t stream, char* work, uint64_t work_bytes, const char* who, bool allow_graphs = true) {
+                        hipStream_t stream, char* work, uint64_t work_bytes, const char* who, bool allow_graphs = true,
+                        bool allow_touch = true) {
   Model* m = nullptr;
   tp_status s = check_request(c, id, &m);
   if (s != TP_OK) return s;
@@ -527,6 +568,8 @@ tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t ba
   bool swapped = false;
   if ((s = admit(c, m, &swapped)) != TP_OK) return s;
   const uint64_t off = c->policy->offset(id);
+  if (!swapped && allow_touch) maybe_touch(c, m, off);
+  c->last_served = id;
   const bool graphs = allow_graphs && !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed &&
                       forward_launches(m->spec) >= kGraphMinLaunches;
   // a swapping request's kernels run on the library's execution stream (see tp_create),
@@ -727,6 +770,8 @@ tp_status tp_create(const tp_config* cfg, tp_ctx** out) {
     e = create_copy_stream(c->device, &c->exec);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->exec_fork, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->exec_join, hipEventDisableTiming);
+    // the cache touch's sink (written only in the impossible case, see k::touch)
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&c->touch_sink), 64 * sizeof(uint32_t));
   }
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
   // tp_infer_noalloc's workspace on this device (a failure only disables that entry point,
@@ -881,7 +926,7 @@ tp_status tp_infer_noalloc(tp_ctx* c, int32_t id, const void* input_dev, int32_t
                                 std::to_string(kNoAllocScratchBytes));
   // kernels launched one by one: instantiating a graph may allocate device memory
   return infer_request(c, id, input_dev, batch, output_dev, static_cast<hipStream_t>(stream_), work,
-                       kNoAllocScratchBytes, "tp_infer_noalloc", false);
+                       kNoAllocScratchBytes, "tp_infer_noalloc", false, false);
 }
 
 tp_status tp_swap_in(tp_ctx* c, int32_t id, void* stream_) {
@@ -952,6 +997,7 @@ tp_status tp_arena_stats(tp_ctx* c, tp_arena_stats_t* out) {
   out->graph_captures = c->graph_captures;
   out->graph_repoints = c->graph_repoints;
   out->graph_rebases = c->graph_rebases;
+  out->cache_touches = c->cache_touches;
   return ok();
 }
 

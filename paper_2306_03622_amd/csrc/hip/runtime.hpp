@@ -143,6 +143,11 @@ struct tp_ctx {
   hipStream_t capture = nullptr;               // private stream for graph capture
   uint64_t graph_clock = 0;
   uint64_t graph_captures = 0, graph_repoints = 0, graph_rebases = 0;
+  // warm requests' cache touch (see maybe_touch): 64 words the touch kernel may write, the
+  // model the previous request served (0: none yet), touches launched
+  uint32_t* touch_sink = nullptr;
+  int32_t last_served = 0;
+  uint64_t cache_touches = 0;
   // cold (swapping) requests run on the library's execution stream, forked from and joined
   // back to the caller's stream (null under TP_FLAG_CALLER_STREAM)
   hipStream_t exec = nullptr;

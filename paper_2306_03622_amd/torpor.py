@@ -27,6 +27,7 @@ TP_ACT = {"none": 0, "relu": 1, "gelu": 2}
 TP_COPY_MEMCPY, TP_COPY_GATHER, TP_COPY_PAGEABLE, TP_COPY_ZERO = 0, 1, 2, 3
 TP_FLAG_POISON, TP_FLAG_THROTTLE, TP_FLAG_NO_GRAPH, TP_FLAG_SERIAL, TP_FLAG_PER_TENSOR, TP_FLAG_TRACE = 1, 2, 4, 8, 16, 32
 TP_FLAG_CALLER_STREAM = 64
+TP_FLAG_NO_TOUCH, TP_FLAG_TOUCH_ALWAYS = 128, 256
 TP_PLAN_GREEDY, TP_PLAN_COST = 0, 1
 TP_EVICT_LRU, TP_EVICT_HEAVINESS, TP_EVICT_LRU_WINDOW = 0, 1, 2
 TP_CLASS_AUTO, TP_CLASS_LIGHT, TP_CLASS_HEAVY = 0, 1, 2
@@ -75,7 +76,7 @@ class tp_arena_stats_t(C.Structure):
                 ("bytes_swapped", C.c_uint64), ("admit_calls", C.c_uint64), ("admit_ns_total", C.c_uint64),
                 ("admit_ns_max", C.c_uint64), ("partitions", C.c_uint32), ("partitions_free", C.c_uint32),
                 ("evacuations", C.c_uint64), ("bytes_moved", C.c_uint64), ("graph_captures", C.c_uint64),
-                ("graph_repoints", C.c_uint64), ("graph_rebases", C.c_uint64)]
+                ("graph_repoints", C.c_uint64), ("graph_rebases", C.c_uint64), ("cache_touches", C.c_uint64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
