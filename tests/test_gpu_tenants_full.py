@@ -159,7 +159,7 @@ def test_full_size_trace_matches_oracle(policy):
         "hit_rate_arena": round(float(hits.mean()), 4), "hit_rate_simulator": round(float(np.mean(want_hits)), 4),
         "hit_rate_byte_capacity_lru": round(float(np.mean(lru)), 4),
         "arena": {k: st[k] for k in ("hits", "misses", "evictions", "frag_evictions", "bytes_swapped",
-                                     "graph_captures", "graph_repoints", "graph_rebases")},
+                                     "graph_captures", "graph_repoints", "graph_rebases", "cache_touches")},
         "decisions_equal_simulator": True,
     }
     log(json.dumps(summary))
