@@ -146,7 +146,8 @@ enum {
  * one copy stream and copy_method TP_COPY_MEMCPY or TP_COPY_GATHER only.
  * A warm tp_infer request (model resident) for a model other than the one the previous
  * request served, whose bytes the requests in between have likely pushed out of the
- * Infinity Cache and the L2s, first launches on the execution stream a kernel that reads the
+ * Infinity Cache and the L2s, or for a model that tp_swap_in brought in and no request has
+ * read since, first launches on the execution stream (after the model's copies) a kernel that reads the
  * model's weights and discards them, except a leading token-embedding table (of which a
  * request reads a few rows), while the request's own kernels run on the caller's stream: the
  * later layers then find their weights in the cache (measured on MI355X at batch 1 after the

@@ -519,18 +519,24 @@ bool touch_span(const ModelSpec& s, uint64_t* lo, uint64_t* hi) {
 }
 
 // A warm request for a model other than the one the previous request served (whose bytes the
-// requests in between have likely pushed out of the Infinity Cache and the L2s; every request
-// for it otherwise, under TP_FLAG_TOUCH_ALWAYS) reads the model's touch span on the
-// execution stream, with nothing ordered before or after it, while its own kernels run on the
-// caller's stream: its later layers then find their weights in the cache. Reading bytes that
-// a later swap may overwrite meanwhile is harmless (they are discarded), and the read stays
-// inside the arena, which outlives the context. A launch failure only forgoes the touch.
-void maybe_touch(tp_ctx* c, const Model* m, uint64_t off) {
+// requests in between have likely pushed out of the Infinity Cache and the L2s), or for one
+// that tp_swap_in brought in and no request has read since (the copy engine's writes leave it
+// out of the caches; every warm request under TP_FLAG_TOUCH_ALWAYS) reads the model's touch
+// span on the execution stream while its own kernels run on the caller's stream: its later
+// layers then find their weights in the cache. The read waits for the model's last copies
+// (a tp_swap_in's may still be in flight) and for nothing else; reading bytes that a later swap
+// overwrites meanwhile is harmless (they are discarded), and the read stays inside the arena,
+// which outlives the context. A failure only forgoes the touch.
+void maybe_touch(tp_ctx* c, Model* m, uint64_t off) {
   if (!c->exec || !c->touch_sink || (c->cfg.flags & TP_FLAG_NO_TOUCH) || m->bg_pending) return;
-  if (!(c->cfg.flags & TP_FLAG_TOUCH_ALWAYS) && c->last_served == m->id) return;
+  if (!(c->cfg.flags & TP_FLAG_TOUCH_ALWAYS) && c->last_served == m->id && !m->touch_due) return;
   uint64_t lo = 0, hi = 0;
   if (!touch_span(m->spec, &lo, &hi)) return;
-  if (k::touch(c->arena + off + lo, hi - lo, c->touch_sink, c->exec) == hipSuccess) ++c->cache_touches;
+  const size_t n = m->chunk_ev.size();
+  hipError_t e = n ? hipStreamWaitEvent(c->exec, m->chunk_ev[n - 1], 0) : hipSuccess;
+  if (e == hipSuccess && c->ncopy == 2 && n > 1) e = hipStreamWaitEvent(c->exec, m->chunk_ev[n - 2], 0);
+  if (e == hipSuccess) e = k::touch(c->arena + off + lo, hi - lo, c->touch_sink, c->exec);
+  if (e == hipSuccess) ++c->cache_touches;
   else (void)hipGetLastError();
 }
 
@@ -570,6 +576,7 @@ tp_status infer_request(tp_ctx* c, int32_t id, const void* input_dev, int32_t ba
   const uint64_t off = c->policy->offset(id);
   if (!swapped && allow_touch) maybe_touch(c, m, off);
   c->last_served = id;
+  m->touch_due = false;          // this request reads the weights (a cold one as they land)
   const bool graphs = allow_graphs && !(c->cfg.flags & TP_FLAG_NO_GRAPH) && !m->graph_failed &&
                       forward_launches(m->spec) >= kGraphMinLaunches;
   // a swapping request's kernels run on the library's execution stream (see tp_create),
@@ -952,6 +959,7 @@ tp_status tp_swap_in(tp_ctx* c, int32_t id, void* stream_) {
     const size_t n = m->chunk_ev.size();
     TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev[n - 1], 0));
     if (c->ncopy == 2 && n > 1) TP_HIP(hipStreamWaitEvent(stream, m->chunk_ev[n - 2], 0));
+    m->touch_due = true;
   }
   return end_request(c, m, stream);
 }

@@ -55,6 +55,8 @@ struct Model {
   bool used = false;             // last_use has been recorded at least once
   bool bg_pending = false;       // swapped in behind a direct-access request: the next
                                  // request must wait for the last chunk's event
+  bool touch_due = false;        // swapped in by tp_swap_in and read by no request since, so
+                                 // its bytes are not in the caches (see maybe_touch)
   std::vector<GraphEntry> graphs;
   bool graph_failed = false;     // capture failed once: launch this model kernel by kernel
   float cold_est_us = 0, warm_est_us = 0;   // cost-model estimates at the context's plan batch

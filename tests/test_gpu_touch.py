@@ -49,6 +49,32 @@ def test_cache_touch_policy_and_results(flags):
     rt.close()
 
 
+def test_cache_touch_after_explicit_swap_in():
+    # a model that tp_swap_in brought in was written by the copy engine and read by nothing, so
+    # its next request touches even though the same model was served last; the touch waits for
+    # the copies, which are still in flight when the request is made here
+    ms, xs = _models()[:1], _inputs(_models())[:1]
+    rt, (mid,) = make_runtime(ms, batch_max=1)
+    torch, dev = torch_dev()
+    s = torch.cuda.Stream(device=dev)
+    want = infer(rt, mid, ms[0], xs[0])            # the miss: no touch
+    assert np.array_equal(infer(rt, mid, ms[0], xs[0]), want)
+    assert rt.stats()["cache_touches"] == 0
+    x = to_device(xs[0])
+    for rep in range(2):
+        out = torch.full(out_shape(ms[0], 1), float("nan"), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        rt.evict(mid)
+        rt.swap_in(mid, stream=s)
+        rt.infer(mid, x, out, stream=s)
+        s.synchronize()
+        assert np.array_equal(out.cpu().numpy(), want)
+        assert rt.stats()["cache_touches"] == rep + 1
+        assert np.array_equal(infer(rt, mid, ms[0], xs[0]), want)   # read since: no touch
+        assert rt.stats()["cache_touches"] == rep + 1
+    rt.close()
+
+
 def test_cache_touch_leaves_noalloc_requests_alone():
     # tp_infer_noalloc (for callers that may be capturing their stream) never touches
     ms, xs = _models()[:2], _inputs(_models())[:2]
