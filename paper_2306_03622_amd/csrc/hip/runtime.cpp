@@ -13,6 +13,7 @@
 
 #include "../core/errors.hpp"
 #include "../kernels/kernels.hpp"
+#include "../kernels/touch.hpp"
 #include "scratch.hpp"
 
 using namespace tp;

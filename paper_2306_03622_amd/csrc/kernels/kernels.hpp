@@ -98,11 +98,6 @@ hipError_t avgpool(const uint16_t* x, int B, int HW, int C, uint16_t* y, hipStre
 // memory by `wgs` workgroups of 16-byte loads.
 hipError_t gather_copy(const void* src, void* dst, uint64_t bytes, int wgs, hipStream_t s);
 
-// Reads `bytes` (multiple of 16, 16-byte aligned) at `p` and discards them, pulling them
-// into the caches; `sink` (64 words of device memory) is written only if the XOR of a
-// thread's data equals a fixed constant.
-hipError_t touch(const void* p, uint64_t bytes, uint32_t* sink, hipStream_t s);
-
 // A single-wave kernel that sleeps for about `us` microseconds (bounded loop).
 hipError_t delay(int us, hipStream_t s);
 

@@ -4,6 +4,7 @@
 
 #include "common.hpp"
 #include "kernels.hpp"
+#include "touch.hpp"
 
 namespace tp {
 namespace k {
