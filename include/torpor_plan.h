@@ -25,6 +25,13 @@ extern "C" {
 /* Validates a descriptor exactly as tp_register_model does. */
 TP_API tp_status tph_validate(const tp_model_desc* desc, uint64_t host_bytes);
 
+/* Whether a warm request of this model pre-reads its weights into the caches (the cache touch
+ * of tp_config), and which bytes of its extent: *applies = 1 and [*lo, *hi) (offsets into the
+ * extent) or *applies = 0 and both 0. The extent minus a leading token-embedding table, for
+ * ResNet-50 and BERT models whose span is 4 MB to 192 MB; never for an MLP. */
+TP_API tp_status tph_touch_span(const tp_model_desc* desc, uint64_t host_bytes, int32_t* applies, uint64_t* lo,
+                                uint64_t* hi);
+
 /* Chunk plan for group size chunk_min_bytes under context flags `flags` (only
  * TP_FLAG_PER_TENSOR matters); same outputs as tp_model_chunks. */
 TP_API tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes, int32_t flags,

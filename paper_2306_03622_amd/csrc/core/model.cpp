@@ -399,4 +399,16 @@ uint64_t activation_bytes(const ModelSpec& m, int32_t batch) {
   return 0;
 }
 
+bool touch_span(const ModelSpec& s, uint64_t* lo, uint64_t* hi) {
+  if (s.arch == TP_ARCH_MLP) return false;
+  uint64_t a = 0;
+  for (const tp_tensor_desc& t : s.tensors)
+    if (t.role == TP_ROLE_TOK_EMB && t.offset == 0) a = round_up(t.bytes, 256);
+  const uint64_t b = s.host_bytes;
+  if (a >= b || b - a < kTouchMinBytes || b - a > kTouchMaxBytes) return false;
+  *lo = a;
+  *hi = b;
+  return true;
+}
+
 }  // namespace tp

@@ -95,6 +95,18 @@ uint64_t workspace_bytes(const ModelSpec& m, int32_t batch);
 
 inline uint64_t round_up(uint64_t n, uint64_t a) { return (n + a - 1) / a * a; }
 
+// Bounds of the bytes a warm request pre-reads into the caches (a span smaller is not missed
+// for long enough to matter; one larger would not stay in the 256 MB Infinity Cache beside
+// everything else).
+constexpr uint64_t kTouchMinBytes = 4ull << 20, kTouchMaxBytes = 192ull << 20;
+
+// The part [*lo, *hi) of a model's extent that a warm request pre-reads into the caches: all
+// of it but a leading token-embedding table, of which a request reads only its ids' rows
+// (BERT-base: 47 of 218 MB). False for an MLP, whose warm pass streams its weights at the rate
+// a second reader would (the two would only compete for the same bytes), and for a span
+// outside [kTouchMinBytes, kTouchMaxBytes].
+bool touch_span(const ModelSpec& s, uint64_t* lo, uint64_t* hi);
+
 // Blocked copy of a bf16 [N][K] matrix (N % 16 == 0, K % 128 == 0): block (n/16, k/128) is
 // 2048 contiguous elements ordered [(k%128)/32][(k%32)/8][n%16][k%8], so that one 16-byte load
 // per lane of a 64-lane wave reads a whole 1 KB run of a skinny-GEMM operand.

@@ -24,6 +24,17 @@ tp_status tph_validate(const tp_model_desc* desc, uint64_t host_bytes) {
   return s == TP_OK ? ok() : fail(s, err);
 }
 
+tp_status tph_touch_span(const tp_model_desc* desc, uint64_t host_bytes, int32_t* applies, uint64_t* lo, uint64_t* hi) {
+  ModelSpec m;
+  std::string err;
+  tp_status s = validate_model(desc, host_bytes, &m, &err);
+  if (s != TP_OK) return fail(s, err);
+  if (!applies || !lo || !hi) return fail(TP_E_INVAL, "tph_touch_span: NULL output");
+  *lo = *hi = 0;
+  *applies = touch_span(m, lo, hi) ? 1 : 0;
+  return ok();
+}
+
 tp_status tph_plan(const tp_model_desc* desc, uint64_t host_bytes, uint64_t chunk_min_bytes, int32_t flags,
                    uint64_t* begin, uint64_t* end, uint32_t* first_layer, uint32_t cap, uint32_t* n) {
   ModelSpec m;

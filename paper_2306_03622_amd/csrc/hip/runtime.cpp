@@ -498,27 +498,6 @@ tp_status check_request(tp_ctx* c, int32_t id, Model** out) {
   return ok();
 }
 
-// Bounds of the bytes a warm request pre-reads into the caches (a span smaller is not missed
-// for long enough to matter; one larger would not stay in the 256 MB Infinity Cache beside
-// everything else).
-constexpr uint64_t kTouchMinBytes = 4ull << 20, kTouchMaxBytes = 192ull << 20;
-
-// The part [*lo, *hi) of a model's extent that a warm request pre-reads: all of it but a
-// leading token-embedding table, of which a request reads only its ids' rows (BERT-base: 47 of
-// 218 MB). False for an MLP, whose warm pass streams its weights at the rate a second reader
-// would (the two would only compete for the same bytes), and for a span outside the bounds.
-bool touch_span(const ModelSpec& s, uint64_t* lo, uint64_t* hi) {
-  if (s.arch == TP_ARCH_MLP) return false;
-  uint64_t a = 0;
-  for (const tp_tensor_desc& t : s.tensors)
-    if (t.role == TP_ROLE_TOK_EMB && t.offset == 0) a = round_up(t.bytes, 256);
-  const uint64_t b = s.host_bytes;
-  if (a >= b || b - a < kTouchMinBytes || b - a > kTouchMaxBytes) return false;
-  *lo = a;
-  *hi = b;
-  return true;
-}
-
 // A warm request for a model other than the one the previous request served (whose bytes the
 // requests in between have likely pushed out of the Infinity Cache and the L2s), or for one
 // that tp_swap_in brought in and no request has read since (the copy engine's writes leave it

@@ -149,6 +149,8 @@ _SIGS = {
                        C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_uint8)],
     "tph_alpha_update": [C.c_double, C.c_double, C.c_double, C.c_double, C.c_double, C.POINTER(C.c_double)],
     "tph_validate": [C.POINTER(tp_model_desc), C.c_uint64],
+    "tph_touch_span": [C.POINTER(tp_model_desc), C.c_uint64, C.POINTER(C.c_int32), C.POINTER(C.c_uint64),
+                       C.POINTER(C.c_uint64)],
     "tph_plan": [C.POINTER(tp_model_desc), C.c_uint64, C.c_uint64, C.c_int32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                  C.POINTER(C.c_uint32), C.c_uint32, C.POINTER(C.c_uint32)],
     "tph_plan_cost_model": [C.POINTER(tp_model_desc), C.c_uint64, C.c_int32, C.c_float, C.c_float,
@@ -412,6 +414,14 @@ def tp_run_trace_sched(ctx, requests, deadlines_ns, policy=TP_QUEUE_SLO, max_inf
 def tph_validate(desc: ModelDesc, host_bytes: int, L=None):
     L = L or lib()
     _check(L, L.tph_validate(C.byref(desc.desc), host_bytes))
+
+
+def tph_touch_span(desc: ModelDesc, host_bytes: int, L=None):
+    """(lo, hi) of the extent a warm request of this model pre-reads into the caches, or None."""
+    L = L or lib()
+    applies, lo, hi = C.c_int32(), C.c_uint64(), C.c_uint64()
+    _check(L, L.tph_touch_span(C.byref(desc.desc), host_bytes, C.byref(applies), C.byref(lo), C.byref(hi)))
+    return (lo.value, hi.value) if applies.value else None
 
 
 def tph_plan(desc: ModelDesc, host_bytes: int, chunk_min_bytes: int, flags: int = 0, L=None):
