@@ -27,7 +27,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     names = declared_symbols()
-    assert len(names) == 39, sorted(names)
+    assert len(names) == 40, sorted(names)
     L = tp.lib()
     for n in names:
         assert hasattr(L, n), n
